@@ -1,0 +1,147 @@
+"""CPU oracle for the DORA deployment hot path (select -> pack -> varlen attention).
+
+TEST INFRASTRUCTURE ONLY: imported by ``tests/``, by ``__graft_entry__.smoke()``
+and by the CPU-baseline leg of ``bench.py``; never by the product package.
+It shares no code with the GPU path.
+
+The arithmetic lives in ``dora_oracle.c`` (plain C, fp64 for attention):
+
+* ``select_pack`` follows the deployment keep rule (Sec. 3.2 "Sampling and
+  deployment"; App. A.3): CLS (position 0) is always kept and, of the visual
+  tokens, the ``keep-1`` highest keep-scores survive; survivors keep their
+  original order (Sec. 3.1, Eq. (1)); images are compacted into one packed
+  buffer with explicit boundaries (Sec. 3.5 "Inference").  Implemented as a
+  full sort of (score, position) per image.
+* ``varlen_attn`` is exact softmax attention inside each boundary
+  (Sec. 3.5; App. E.4), computed as a dense fp64 score matrix per
+  (image, head) from the exact values of the bf16 / fp32 inputs.
+
+Pins (tests/test_oracle_*.py): brute-force counting definition of the keep
+set over exhaustive tiny inputs, NumPy's stable argsort on NaN-free inputs,
+closed forms (keep-all, keep-one, constant scores, monotone scores), a
+hand-worked fixture; for attention a pure-Python triple loop, torch fp64
+``scaled_dot_product_attention`` on keep-all and padded+masked batches,
+one-hot V (softmax rows sum to 1), segment-permutation and key-permutation
+invariance, keep-one (O = V) and identical keys (O = mean of V).
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import Optional, Tuple
+
+import numpy as np
+
+from . import build as _build
+
+BAD_KEEP = 1
+OVERFLOW = 2
+BAD_SEGMENTS = 4
+
+_lib = None
+
+
+def load_library(path: str):
+    """Open an oracle shared library and declare its signatures."""
+    lib = ctypes.CDLL(path)
+    lib.oracle_select_pack.restype = ctypes.c_int
+    lib.oracle_select_pack.argtypes = [
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+        ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64]
+    lib.oracle_varlen_attn.restype = None
+    lib.oracle_varlen_attn.argtypes = [
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_double,
+        ctypes.c_void_p, ctypes.c_int32]
+    lib.oracle_max_threads.restype = ctypes.c_int
+    return lib
+
+
+def _load(lib=None):
+    global _lib
+    if lib is not None:
+        return lib
+    if _lib is None:
+        _lib = load_library(_build.build(force=False))
+    return _lib
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data
+
+
+def max_threads() -> int:
+    return int(_load().oracle_max_threads())
+
+
+def select_pack(scores: np.ndarray, keep: np.ndarray, tokens: np.ndarray,
+                cu_in: Optional[np.ndarray] = None, N: Optional[int] = None, lib=None
+                ) -> Tuple[np.ndarray, np.ndarray, np.ndarray, int]:
+    """Keep CLS + top-(keep-1) visual tokens per image and pack them.
+
+    scores: float32 [B,N] (dense) or [total_in] with ``cu_in`` [B+1].
+    keep:   int32 [B] (counts CLS).
+    tokens: [B,N,C] or [total_in,C] of any fixed-size dtype (rows copied as bytes).
+    Returns (idx [sum keep] int32, cu [B+1] int32, packed [sum keep, C], status).
+    On a nonzero status nothing was computed and the arrays are empty.
+    """
+    scores = np.ascontiguousarray(scores, dtype=np.float32)
+    keep = np.ascontiguousarray(keep, dtype=np.int32)
+    tokens = np.ascontiguousarray(tokens)
+    B = int(keep.shape[0])
+    if cu_in is None:
+        if N is None:
+            N = int(scores.shape[1]) if scores.ndim == 2 else int(scores.shape[0]) // max(B, 1)
+        cu_arr = None
+    else:
+        cu_arr = np.ascontiguousarray(cu_in, dtype=np.int32)
+        if N is None:
+            N = int(np.max(np.diff(cu_arr))) if B else 0
+    C = int(np.prod(tokens.shape[1:])) if cu_in is not None else int(np.prod(tokens.shape[2:]))
+    tok2 = tokens.reshape(-1, C)
+    total_in = tok2.shape[0]
+    if cu_in is not None and scores.shape[0] < total_in:
+        raise ValueError("packed scores shorter than the packed token rows")
+    row_bytes = C * tok2.dtype.itemsize
+    cap = int(keep.astype(np.int64).clip(min=0).sum())
+    idx = np.zeros(max(cap, 1), dtype=np.int32)
+    cu = np.zeros(B + 1, dtype=np.int32)
+    packed = np.zeros((max(cap, 1), C), dtype=tok2.dtype)
+    st = _load(lib).oracle_select_pack(_ptr(scores), _ptr(keep), _ptr(tok2), _ptr(cu_arr),
+                                       total_in, B, int(N), row_bytes, _ptr(idx), _ptr(cu), _ptr(packed), cap)
+    if st:
+        return (np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros((0, C), tok2.dtype), int(st))
+    return idx[:cap], cu, packed[:cap], 0
+
+
+def widen(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Exact fp64 value of bf16 bit patterns (uint16) or fp32 values."""
+    if dtype == "bf16":
+        return (np.ascontiguousarray(x, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return np.asarray(x, dtype=np.float32).astype(np.float64)
+
+
+def varlen_attn(q: np.ndarray, k: np.ndarray, v: np.ndarray, cu: np.ndarray, dtype: str,
+                scale: Optional[float] = None, threads: int = 0, lib=None) -> np.ndarray:
+    """Exact fp64 softmax attention per sequence of the packed [total, H, D] inputs."""
+    qd, kd, vd = (np.ascontiguousarray(widen(a, dtype)) for a in (q, k, v))
+    total, H, D = qd.shape
+    cu = np.ascontiguousarray(cu, dtype=np.int32)
+    B = int(cu.shape[0]) - 1
+    if scale is None:
+        scale = 1.0 / np.sqrt(D)
+    out = np.zeros_like(qd)
+    _load(lib).oracle_varlen_attn(_ptr(qd), _ptr(kd), _ptr(vd), _ptr(cu), B, H, D, float(scale),
+                               _ptr(out), int(threads))
+    return out
+
+
+def varlen_attn_segments(q, k, v, cu, segments, dtype: str, scale: Optional[float] = None,
+                         threads: int = 0):
+    """Oracle outputs for a subset of sequences only: {b: [len_b, H, D] fp64}."""
+    res = {}
+    for b in segments:
+        s, e = int(cu[b]), int(cu[b + 1])
+        sub_cu = np.array([0, e - s], dtype=np.int32)
+        res[b] = varlen_attn(q[s:e], k[s:e], v[s:e], sub_cu, dtype, scale, threads)
+    return res

@@ -1,0 +1,193 @@
+/*
+ * Plain CPU oracle for the DORA deployment hot path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the
+ * benchmark's CPU-baseline leg may load this library.  It shares no code,
+ * header, table or constant with the GPU path.
+ *
+ * What it computes (DORA, arXiv 2609.34325):
+ *   - Deployment keep rule (Sec. 3.2 "Sampling and deployment", App. A.3):
+ *     the selector removes the highest-scoring visual tokens and CLS is never
+ *     removed; deletion preserves CLS and the relative order of survivors
+ *     (Sec. 3.1, pruning operator, Eq. (1)).  Here scores are keep-scores
+ *     (higher = keep), so an image keeps CLS plus its keep-1 highest-scoring
+ *     visual tokens.  Score comparisons are FP32 values (App. E.4).
+ *   - Packing (Sec. 3.5 "Inference"): survivors of all images are compacted
+ *     into one buffer with explicit sequence boundaries.
+ *   - Attention (Sec. 3.5, App. E.4): exact softmax attention inside each
+ *     sequence boundary, with no attention between images, no bias term and
+ *     no token-size correction.
+ *
+ * Readings where the paper is silent (listed with the tests that pin them):
+ *   - Ties: equal scores are broken by the lower position (a stable order).
+ *   - NaN ranks below every number; NaNs tie with each other.  -0 == +0.
+ *   - Softmax scale is a parameter (1/sqrt(64) for ViT heads of width 64).
+ *
+ * Everything is computed the slow, direct way: a full sort per image and a
+ * dense fp64 score matrix per (image, head).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* Return codes of oracle_select_pack (bit set). */
+#define ORACLE_BAD_KEEP 1      /* some keep[b] outside [1, n_b]                 */
+#define ORACLE_OVERFLOW 2      /* sum of keep exceeds the output capacity        */
+#define ORACLE_BAD_SEGMENTS 4  /* packed input offsets are not a valid partition */
+
+typedef struct {
+  float score;
+  int32_t pos;
+} candidate;
+
+/* Total order on candidates: "a before b" when a is preferred for keeping.
+ * Non-NaN before NaN; larger score first (IEEE compare, so -0 == +0);
+ * equal scores and NaN-vs-NaN by ascending position. */
+static int candidate_order(const void* pa, const void* pb) {
+  const candidate* a = (const candidate*)pa;
+  const candidate* b = (const candidate*)pb;
+  int an = isnan(a->score), bn = isnan(b->score);
+  if (an != bn) return an ? 1 : -1;
+  if (!an) {
+    double x = (double)a->score, y = (double)b->score;
+    if (x > y) return -1;
+    if (x < y) return 1;
+  }
+  return (a->pos < b->pos) ? -1 : (a->pos > b->pos) ? 1 : 0;
+}
+
+static int ascending_int(const void* pa, const void* pb) {
+  int32_t a = *(const int32_t*)pa, b = *(const int32_t*)pb;
+  return (a < b) ? -1 : (a > b) ? 1 : 0;
+}
+
+/*
+ * Select + pack.
+ *   scores  : dense [B*N] (cu_in == NULL) or packed [total_in] fp32
+ *   keep    : [B], keep count including CLS
+ *   tokens  : rows of row_bytes bytes, dense [B*N] rows or packed [total_in] rows
+ *   cu_in   : NULL (dense, every segment has N rows) or [B+1] segment offsets
+ *   idx_out : [sum keep] kept positions, local to each segment, ascending
+ *   cu_out  : [B+1] output sequence boundaries
+ *   packed  : [sum keep] rows
+ * Returns 0 or a bitwise OR of ORACLE_* codes; on error nothing is written.
+ */
+int oracle_select_pack(const float* scores, const int32_t* keep, const uint8_t* tokens,
+                       const int32_t* cu_in, int64_t total_in, int32_t B, int32_t N,
+                       int64_t row_bytes,
+                       int32_t* idx_out, int32_t* cu_out, uint8_t* packed, int64_t cap_rows) {
+  int status = 0;
+  int64_t* off_in = (int64_t*)malloc(sizeof(int64_t) * (size_t)(B > 0 ? B : 1));
+  int64_t* n_in = (int64_t*)malloc(sizeof(int64_t) * (size_t)(B > 0 ? B : 1));
+  int64_t total = 0;
+  for (int32_t b = 0; b < B; ++b) {
+    if (cu_in) {
+      off_in[b] = cu_in[b];
+      n_in[b] = (int64_t)cu_in[b + 1] - cu_in[b];
+      if ((b == 0 && cu_in[0] != 0) || cu_in[b] < 0 || n_in[b] < 1 || n_in[b] > N ||
+          cu_in[b + 1] > total_in)
+        status |= ORACLE_BAD_SEGMENTS;
+    } else {
+      off_in[b] = (int64_t)b * N;
+      n_in[b] = N;
+    }
+    if (keep[b] < 1 || keep[b] > n_in[b]) status |= ORACLE_BAD_KEEP;
+    total += keep[b];
+  }
+  if (total > cap_rows) status |= ORACLE_OVERFLOW;
+  if (status) {
+    free(off_in);
+    free(n_in);
+    return status;
+  }
+
+  /* Sequence boundaries: running total of keep counts. */
+  cu_out[0] = 0;
+  for (int32_t b = 0; b < B; ++b) cu_out[b + 1] = cu_out[b] + keep[b];
+
+#pragma omp parallel for schedule(dynamic)
+  for (int32_t b = 0; b < B; ++b) {
+    const int64_t n = n_in[b];
+    const float* s = scores + off_in[b];
+    candidate* cand = (candidate*)malloc(sizeof(candidate) * (size_t)n);
+    int32_t* kept = idx_out + cu_out[b];
+    /* Visual tokens are positions 1..n-1; CLS (position 0) is not a candidate. */
+    for (int64_t j = 1; j < n; ++j) {
+      cand[j - 1].score = s[j];
+      cand[j - 1].pos = (int32_t)j;
+    }
+    qsort(cand, (size_t)(n - 1), sizeof(candidate), candidate_order);
+    kept[0] = 0;
+    for (int32_t r = 0; r < keep[b] - 1; ++r) kept[r + 1] = cand[r].pos;
+    /* Survivors keep their original relative order. */
+    qsort(kept, (size_t)keep[b], sizeof(int32_t), ascending_int);
+    for (int32_t r = 0; r < keep[b]; ++r)
+      memcpy(packed + (size_t)(cu_out[b] + r) * (size_t)row_bytes,
+             tokens + (size_t)(off_in[b] + kept[r]) * (size_t)row_bytes, (size_t)row_bytes);
+    free(cand);
+  }
+  free(off_in);
+  free(n_in);
+  return 0;
+}
+
+/*
+ * Dense softmax attention per sequence and head, fp64.
+ *   q, k, v, out : [total, H, D] row-major, already widened to double
+ *   cu           : [B+1] sequence boundaries
+ * O_b = softmax(scale * Q_b K_b^T) V_b for every sequence b and head h.
+ */
+void oracle_varlen_attn(const double* q, const double* k, const double* v, const int32_t* cu,
+                        int32_t B, int32_t H, int32_t D, double scale, double* out,
+                        int32_t nthreads) {
+#ifdef _OPENMP
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+  (void)nthreads;
+#endif
+#pragma omp parallel for collapse(2) schedule(dynamic)
+  for (int32_t b = 0; b < B; ++b) {
+    for (int32_t h = 0; h < H; ++h) {
+      const int64_t start = cu[b];
+      const int64_t len = (int64_t)cu[b + 1] - cu[b];
+      if (len <= 0) continue;
+      double* logits = (double*)malloc(sizeof(double) * (size_t)len);
+      for (int64_t i = 0; i < len; ++i) {
+        const double* qi = q + ((start + i) * H + h) * D;
+        double mx = -INFINITY;
+        for (int64_t j = 0; j < len; ++j) {
+          const double* kj = k + ((start + j) * H + h) * D;
+          double dot = 0.0;
+          for (int32_t d = 0; d < D; ++d) dot += qi[d] * kj[d];
+          logits[j] = scale * dot;
+          if (logits[j] > mx) mx = logits[j];
+        }
+        double z = 0.0;
+        for (int64_t j = 0; j < len; ++j) {
+          logits[j] = exp(logits[j] - mx);
+          z += logits[j];
+        }
+        double* oi = out + ((start + i) * H + h) * D;
+        for (int32_t d = 0; d < D; ++d) oi[d] = 0.0;
+        for (int64_t j = 0; j < len; ++j) {
+          const double* vj = v + ((start + j) * H + h) * D;
+          const double p = logits[j] / z;
+          for (int32_t d = 0; d < D; ++d) oi[d] += p * vj[d];
+        }
+      }
+      free(logits);
+    }
+  }
+}
+
+int oracle_max_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}

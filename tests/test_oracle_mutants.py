@@ -1,0 +1,102 @@
+"""The oracle's pins must catch plausible mistakes.
+
+Each case plants one mistake (a flipped comparison, a wrong index, a dropped
+term) into a copy of the oracle's C source, builds it on the CPU, and checks
+that the brute-force / library pins reject the mutant while the unmodified
+source passes the same battery.
+"""
+import os
+import subprocess
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from test_oracle_select import brute_keep_masks, masks_from_idx
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "dora_oracle.c")
+
+MUTANTS = {
+    "score_direction": ("if (x > y) return -1;\n    if (x < y) return 1;",
+                        "if (x < y) return -1;\n    if (x > y) return 1;"),
+    "tie_direction": ("return (a->pos < b->pos) ? -1 : (a->pos > b->pos) ? 1 : 0;",
+                      "return (a->pos > b->pos) ? -1 : (a->pos < b->pos) ? 1 : 0;"),
+    "nan_on_top": ("if (an != bn) return an ? 1 : -1;", "if (an != bn) return an ? -1 : 1;"),
+    "cls_not_pinned": ("kept[0] = 0;", "kept[0] = cand[0].pos;"),
+    "order_not_preserved": ("qsort(kept, (size_t)keep[b], sizeof(int32_t), ascending_int);", ""),
+    "one_short": ("for (int32_t r = 0; r < keep[b] - 1; ++r) kept[r + 1] = cand[r].pos;",
+                  "for (int32_t r = 0; r < keep[b] - 2; ++r) kept[r + 1] = cand[r].pos;\n"
+                  "    kept[keep[b] - 1] = kept[keep[b] > 1 ? keep[b] - 2 : 0];"),
+    "cu_not_running": ("cu_out[b + 1] = cu_out[b] + keep[b];", "cu_out[b + 1] = keep[b] + (b > 0 ? cu_out[b - 1] : 0);"),
+    "pack_wrong_segment": ("tokens + (size_t)(off_in[b] + kept[r])", "tokens + (size_t)(kept[r])"),
+    "no_scale": ("logits[j] = scale * dot;", "logits[j] = dot;"),
+    "query_for_key": ("const double* kj = k + ((start + j) * H + h) * D;",
+                      "const double* kj = q + ((start + j) * H + h) * D;"),
+    "wrong_head_stride": ("const double* vj = v + ((start + j) * H + h) * D;",
+                          "const double* vj = v + ((start + j) * H + 0) * D;"),
+    "unnormalised": ("const double p = logits[j] / z;", "const double p = logits[j];"),
+    "key_index_is_query": ("for (int32_t d = 0; d < D; ++d) dot += qi[d] * kj[d];",
+                           "for (int32_t d = 0; d < D; ++d) dot += qi[d] * k[((start + i) * H + h) * D + d];"),
+}
+
+
+def build_variant(tmp_path, name, old, new):
+    src = open(SRC).read()
+    assert src.count(old) == 1, name
+    path_c = tmp_path / f"{name}.c"
+    path_c.write_text(src.replace(old, new))
+    path_so = tmp_path / f"lib{name}.so"
+    subprocess.run(["gcc", "-O1", "-std=c99", "-fopenmp", "-fPIC", "-shared", str(path_c),
+                    "-o", str(path_so), "-lm"], check=True)
+    return oracle.load_library(str(path_so))
+
+
+def battery(lib):
+    """Return the list of pins the library fails."""
+    failed = []
+    rng = np.random.default_rng(101)
+    # selection vs counting definition, heavy ties and NaNs
+    n, B = 7, 3000
+    s = rng.choice(np.array([-2.0, -0.0, 0.0, 0.5, 3.0, np.nan], np.float32), size=(B, n))
+    keep = rng.integers(1, n + 1, size=B).astype(np.int32)
+    tok = rng.standard_normal((B, n, 4)).astype(np.float32)
+    idx, cu, packed, st = oracle.select_pack(s, keep, tok, lib=lib)
+    if st or not np.array_equal(masks_from_idx(idx, cu, B, n), brute_keep_masks(s, keep)):
+        failed.append("select")
+    if st == 0:
+        if not (cu[0] == 0 and np.array_equal(cu[1:], np.cumsum(keep))):
+            failed.append("cu")
+        elif not all(np.array_equal(packed[cu[b] + r], tok[b, idx[cu[b] + r]])
+                     for b in range(B) for r in range(keep[b])):
+            failed.append("pack")
+        elif not all(np.all(np.diff(idx[cu[b]:cu[b + 1]]) > 0) for b in range(B)):
+            failed.append("order")
+    # attention vs torch fp64 SDPA, padded + masked
+    lens = np.array([5, 1, 23, 12])
+    H, D = 3, 64
+    cuq = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    q, k, v = (rng.standard_normal((int(lens.sum()), H, D)).astype(np.float32) for _ in range(3))
+    got = oracle.varlen_attn(q, k, v, cuq, "f32", lib=lib)
+    L = int(lens.max())
+    pad = lambda a: np.stack([np.pad(a[cuq[b]:cuq[b + 1]].astype(np.float64),
+                                     ((0, L - lens[b]), (0, 0), (0, 0))) for b in range(len(lens))])
+    tq, tk, tv = (torch.from_numpy(pad(a)).transpose(1, 2) for a in (q, k, v))
+    mask = torch.from_numpy(np.arange(L)[None, :] < lens[:, None])[:, None, None, :]
+    want = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, attn_mask=mask, scale=1 / 8)
+    want = want.transpose(1, 2).numpy()
+    if any(np.max(np.abs(got[cuq[b]:cuq[b + 1]] - want[b, :lens[b]])) > 1e-12 for b in range(len(lens))):
+        failed.append("attention")
+    return failed
+
+
+def test_unmodified_source_passes(tmp_path):
+    lib = build_variant(tmp_path, "original", "int oracle_max_threads(void) {", "int oracle_max_threads(void) {")
+    assert battery(lib) == []
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(tmp_path, name):
+    old, new = MUTANTS[name]
+    lib = build_variant(tmp_path, name, old, new)
+    assert battery(lib), f"planted mistake '{name}' passed every pin"
