@@ -1,0 +1,214 @@
+"""Benchmark of the DORA deployment hot path on one MI355X.
+
+One step = one pass of the whole path over one batch:
+    dora_select_pack  (top-k with CLS pinned + cu_seqlens + packed gather)
+    dora_varlen_attn_plan     (work queue for the packed layout)
+    dora_varlen_attn_execute  (varlen attention, bf16 MFMA)
+on synthetic inputs already resident in HBM.  Prints one JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import workloads as W  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0            # MI355X HBM3E, GB/s
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # dense matrix peaks, TFLOP/s
+METRIC = "packed tokens/s + varlen-attn TFLOP/s (% MFMA peak), DeiT-B shape, B=256"
+
+
+def select_pack_bytes(w: W.Workload, keep: np.ndarray, n_in: np.ndarray) -> int:
+    """Algorithmic HBM bytes of select/pack: read scores and keep, read and write
+    each kept row once, write the kept indices and cu_seqlens."""
+    sk = int(keep.sum())
+    return 2 * sk * w.C * w.elt + 4 * (int(n_in.sum()) + sk + 2 * w.B + 1)
+
+
+def attn_flops(w: W.Workload, keep: np.ndarray) -> float:
+    k = keep.astype(np.float64)
+    return 4.0 * w.H * W.HEAD_DIM * float(np.sum(k * k))
+
+
+def attn_bytes(w: W.Workload, keep: np.ndarray) -> int:
+    return 4 * int(keep.sum()) * w.H * W.HEAD_DIM * w.elt   # Q, K, V read once, O written once
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
+
+
+def run_cpu_baseline(w: W.Workload, r: W.RoundInputs, repeats: int = 3) -> dict:
+    """The oracle as it stands, timed on this host's cores over the full batch."""
+    import oracle
+    threads = len(os.sched_getaffinity(0))
+    times = []
+    for _ in range(repeats):
+        t0 = time.perf_counter()
+        idx, cu, packed, st = oracle.select_pack(r.scores, r.keep, r.tokens)
+        oracle.varlen_attn(r.q, r.k, r.v, cu, w.dtype, threads=threads)
+        times.append(time.perf_counter() - t0)
+        assert st == 0
+    t = statistics.median(times)
+    return {"value": r.total_keep / t, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"full {w.name} batch (B={w.B}, sum keep={r.total_keep}), select+pack+attention, "
+                      f"median of {repeats}, {t:.3f} s per pass, CPU: {cpu_model()}"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--repeats", type=int, default=5)
+    ap.add_argument("--workload", default=W.HEADLINE, choices=sorted(W.WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
+                    help="measured HBM bytes per launch (from rocprofv3 counters), if present")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the path shards by image; see the design notes).", file=sys.stderr)
+        return 2
+
+    import torch
+    import paper_2609_34325_amd as dora
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dora.load_library()
+    torch.cuda.set_device(0)
+    w = W.WORKLOADS[args.workload]
+    r = W.generate(w)[0]
+    print(f"[bench] {w.name}: B={w.B} N={w.N} H={w.H} C={w.C} {w.dtype} sum_keep={r.total_keep}",
+          file=sys.stderr, flush=True)
+
+    def dev(a):
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+    scores, keep, tokens = dev(r.scores), dev(r.keep), dev(r.tokens)
+    q, k, v = dev(r.q), dev(r.k), dev(r.v)
+    sk = r.total_keep
+    max_seqlen = int(r.keep.max())
+    idx = torch.empty(sk, dtype=torch.int32, device="cuda")
+    cu = torch.empty(w.B + 1, dtype=torch.int32, device="cuda")
+    packed = torch.empty((sk, w.C), dtype=tokens.dtype, device="cuda")
+    out = torch.empty_like(q)
+    ws = dora.new_workspace(w.B, w.H, max_seqlen)
+    st = dora.new_status()
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        dora.dora_select_pack(scores, keep, tokens, idx_out=idx, cu_out=cu, packed_out=packed,
+                              cap_rows=sk, dev_status=st, stream=stream)
+        if ev is not None:
+            ev[1].record(stream)
+        dora.dora_varlen_attn_plan(cu, w.H, max_seqlen, sk, ws, st, stream=stream)
+        if ev is not None:
+            ev[2].record(stream)
+        dora.dora_varlen_attn_execute(q, k, v, cu, max_seqlen, ws, out=out, dev_status=st, stream=stream)
+        if ev is not None:
+            ev[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0, f"device status {int(st.item())}"
+
+    reps = []
+    for rep in range(args.repeats):
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+        t_start = torch.cuda.Event(enable_timing=True)
+        t_end = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t_start.record(stream)
+        for i in range(args.steps):
+            step(evs[i])
+        t_end.record(stream)
+        torch.cuda.synchronize()
+        total_ms = t_start.elapsed_time(t_end)
+        sel = np.mean([e[0].elapsed_time(e[1]) for e in evs])
+        plan = np.mean([e[1].elapsed_time(e[2]) for e in evs])
+        attn = np.mean([e[2].elapsed_time(e[3]) for e in evs])
+        reps.append((total_ms / args.steps, sel, plan, attn))
+        print(f"[bench] repeat {rep}: {total_ms / args.steps * 1e3:.1f} us/step "
+              f"(select_pack {sel * 1e3:.1f}, plan {plan * 1e3:.1f}, attention {attn * 1e3:.1f})",
+              file=sys.stderr, flush=True)
+    assert int(st.item()) == 0, f"device status {int(st.item())}"
+    med = sorted(reps, key=lambda x: x[0])[len(reps) // 2]
+    ms_step, ms_sel, ms_plan, ms_attn = med
+
+    flops = attn_flops(w, r.keep)
+    sp_bytes = select_pack_bytes(w, r.keep, r.n_in)
+    a_bytes = attn_bytes(w, r.keep)
+    attn_tflops = flops / (ms_attn * 1e-3) / 1e12
+    sp_gbs = sp_bytes / (ms_sel * 1e-3) / 1e9
+    peak = MFMA_PEAK_TFLOPS[w.dtype]
+
+    traffic = {}
+    if os.path.exists(args.traffic_json):
+        try:
+            traffic = json.load(open(args.traffic_json)).get(w.name, {})
+        except (OSError, ValueError):
+            traffic = {}
+
+    result = {
+        "metric": METRIC,
+        "value": sk / (ms_step * 1e-3),
+        "unit": "packed tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "N": w.N, "H": w.H, "head_dim": W.HEAD_DIM, "C": w.C,
+                   "sum_keep": sk, "sum_keep_sq": int(np.sum(r.keep.astype(np.int64) ** 2)),
+                   "max_seqlen": max_seqlen},
+        "roofline": {"bound": "mfma", "kernel": "attn_fwd_bf16_kernel" if w.dtype == "bf16" else "attn_fwd_f32_kernel",
+                     "achieved": attn_tflops, "peak": peak, "unit": "TFLOP/s", "frac": attn_tflops / peak,
+                     "traffic": traffic.get("attn"), "algorithmic_bytes": a_bytes,
+                     "hbm_bound_tflops": flops / (a_bytes / (HBM_PEAK_GBS * 1e9)) / 1e12},
+        "roofline_select_pack": {"bound": "hbm", "kernel": "select_pack_kernel", "achieved": sp_gbs,
+                                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": sp_gbs / HBM_PEAK_GBS,
+                                 "traffic": traffic.get("select_pack"), "algorithmic_bytes": sp_bytes},
+        "select_pack_tokens_per_s": sk / (ms_sel * 1e-3),
+        "attn_tflops": attn_tflops,
+        "us": {"select_pack": ms_sel * 1e3, "plan": ms_plan * 1e3, "attention": ms_attn * 1e3,
+               "step": ms_step * 1e3},
+        "repeats": args.repeats,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = run_cpu_baseline(w, r)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

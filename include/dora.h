@@ -1,0 +1,183 @@
+/*
+ * dora.h -- C ABI of the DORA deployment hot path on AMD Instinct MI355X (gfx950).
+ *
+ * DORA (arXiv 2609.34325) prunes Vision Transformer tokens per image.  At
+ * deployment the actor keeps CLS, removes the visual tokens the selector
+ * ranks highest for removal, and preserves the order of the survivors
+ * (Sec. 3.1, Eq. (1); Sec. 3.2 "Sampling and deployment"; App. A.3).  The
+ * survivors of all images are compacted into one packed buffer with
+ * explicit sequence boundaries and processed by variable-length attention
+ * that never attends across images (Sec. 3.5 "Inference"; App. E.4).
+ *
+ * This library implements that path as two calls:
+ *   dora_select_pack  -- per-image top-k selection with CLS pinned, the
+ *                        running total of keep counts (cu_seqlens) and the
+ *                        gather of kept rows into the packed buffer;
+ *   dora_varlen_attn  -- softmax attention inside each packed sequence
+ *                        (split into _plan and _execute so one plan can
+ *                        serve every layer that shares the same layout).
+ *
+ * Conventions shared by every entry point
+ *   - All array arguments are DEVICE pointers allocated by the caller; the
+ *     library never allocates device memory, never frees caller memory and
+ *     keeps no state between calls other than a per-device cache of the
+ *     compute-unit count.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *     Every call only enqueues work on that stream and returns without
+ *     synchronising the host.
+ *   - Argument errors that the host can see are returned as a negative
+ *     dora_status before anything is enqueued.
+ *   - Errors that depend on device data (keep counts, offsets) are reported
+ *     by OR-ing DORA_DEV_* bits into *dev_status (an int32 in device memory
+ *     that the caller zeroes beforehand and reads after synchronising).
+ *     When a bit is set the affected outputs are unspecified, but no write
+ *     ever lands outside the output buffers' stated extents.
+ *   - Row-major layouts; int32 indices; element types per dora_dtype.
+ */
+#ifndef DORA_H_
+#define DORA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { DORA_F32 = 0, DORA_BF16 = 1 } dora_dtype;
+
+typedef enum {
+  DORA_OK = 0,
+  DORA_ERR_NULL = -1,        /* a required pointer is NULL                          */
+  DORA_ERR_SHAPE = -2,       /* a size is out of range (B, N, C, H, D, max_seqlen)  */
+  DORA_ERR_DTYPE = -3,       /* unknown dora_dtype                                  */
+  DORA_ERR_ALIGN = -4,       /* a row-data pointer is not 16-byte aligned           */
+  DORA_ERR_UNSUPPORTED = -5, /* valid request outside what this build implements    */
+  DORA_ERR_CAPACITY = -6,    /* an output capacity cannot be represented            */
+  DORA_ERR_HIP = -7,         /* the HIP runtime reported an error at launch         */
+  DORA_ERR_WORKSPACE = -8    /* workspace NULL, misaligned or smaller than required */
+} dora_status;
+
+/* Bits OR-ed into *dev_status by the kernels. */
+#define DORA_DEV_KEEP_RANGE 0x1  /* some keep[b] < 1 or keep[b] > n_b; image b was skipped         */
+#define DORA_DEV_CAPACITY 0x2    /* sum(keep) > cap_rows; rows at or past cap_rows were not written */
+#define DORA_DEV_CU_IN 0x4       /* cu_in not a partition of [0,total_in) into segments of 1..N     */
+#define DORA_DEV_CU_SEQLENS 0x8  /* attention offsets invalid (non-monotone, past total, or a
+                                    sequence longer than max_seqlen); such sequences were skipped */
+#define DORA_DEV_PLAN 0x10       /* execute called with a workspace not planned for these sizes    */
+
+/* Limits of this build. */
+#define DORA_MAX_ROW_TOKENS 2048     /* dora_select_pack: N (tokens per image, CLS included)  */
+#define DORA_MAX_SEQLEN 16384        /* dora_varlen_attn: max_seqlen                          */
+#define DORA_HEAD_DIM 64             /* dora_varlen_attn: D                                   */
+
+/*
+ * dora_select_pack -- hard deletion + packing (Sec. 3.1 Eq. (1); Sec. 3.2
+ * "Sampling and deployment"; Sec. 3.5 "Inference"; App. A.3).
+ *
+ * For every image b with input segment of n_b tokens (position 0 is CLS):
+ *   keep CLS and the keep[b]-1 visual positions with the highest score,
+ *   comparing scores as FP32 values (App. E.4); equal scores go to the lower
+ *   position, NaN ranks below every number, -0 equals +0.  The kept
+ *   positions are written in ascending order, so CLS and the survivors'
+ *   relative order are preserved.
+ *
+ * Scores are KEEP-scores (higher = keep).  The paper's selector scores
+ * removal preference (higher = remove; Sec. 3.2, selector equation (2)), so a DORA caller
+ * passes their negation; its removal budget k_l maps to keep = n_b - k_l
+ * (n_b counts CLS).
+ *
+ *   scores     fp32.  Dense input (cu_in == NULL): [B, N], n_b = N.
+ *              Packed input: [total_in], segment b = [cu_in[b], cu_in[b+1]).
+ *   keep       int32 [B]   keep count of image b including CLS, 1..n_b.
+ *   tokens     dtype [B, N, C] (dense) or [total_in, C] (packed); 16-byte aligned.
+ *   cu_in      NULL or int32 [B+1] with cu_in[0] = 0, non-decreasing,
+ *              1 <= cu_in[b+1]-cu_in[b] <= N, cu_in[B] <= total_in.
+ *              Chaining rounds: pass the previous round's cu_out and packed_out.
+ *   total_in   rows of the packed input (ignored for dense input).
+ *   B          images, >= 1.
+ *   N          dense: tokens per image; packed: an upper bound on n_b.
+ *              1 <= N <= DORA_MAX_ROW_TOKENS.
+ *   C          channels per token; C * sizeof(dtype) must be a multiple of 16.
+ *   idx_out    int32 [cap_rows]: kept positions, local to each input segment,
+ *              ascending within each image; idx_out[cu_out[b]] == 0 (CLS).
+ *   cu_out     int32 [B+1]: cu_out[0] = 0, cu_out[b+1] = cu_out[b] + keep[b].
+ *   packed_out dtype [cap_rows, C]: packed_out[cu_out[b] + r] is a bitwise copy
+ *              of token row idx_out[cu_out[b] + r] of image b.  16-byte aligned.
+ *   cap_rows   rows available in idx_out / packed_out, 1 .. 2^31-1.
+ *   dev_status int32 device word, see DORA_DEV_*.
+ *
+ * Returns DORA_OK or a negative dora_status; enqueues one kernel.
+ */
+int dora_select_pack(const float* scores, const int32_t* keep, const void* tokens,
+                     const int32_t* cu_in, int64_t total_in, int32_t B, int32_t N, int32_t C,
+                     dora_dtype dtype, int32_t* idx_out, int32_t* cu_out, void* packed_out,
+                     int64_t cap_rows, int32_t* dev_status, void* stream);
+
+/*
+ * dora_varlen_attn_workspace_size -- bytes of device workspace that
+ * dora_varlen_attn_plan / _execute / dora_varlen_attn need for B sequences,
+ * H heads and sequences of at most max_seqlen tokens.  Returns 0 for sizes
+ * out of range.
+ */
+size_t dora_varlen_attn_workspace_size(int32_t B, int32_t H, int32_t max_seqlen);
+
+/*
+ * dora_varlen_attn_plan -- build the attention work queue for one packed
+ * layout (the sequence boundaries of Sec. 3.5 "Inference").
+ *
+ * Writes into `workspace` the list of (sequence, head, query-tile) items of
+ * the layout, ordered by decreasing sequence length so that long sequences
+ * start first and short ones fill the tail, and resets the queue counters.
+ * A plan stays valid for any number of _execute calls with the same
+ * cu_seqlens contents and sizes (e.g. every layer between two pruning steps).
+ *
+ *   cu_seqlens int32 [B+1]: 0 = cu[0] <= cu[1] <= ... <= cu[B] <= total and
+ *              cu[b+1]-cu[b] <= max_seqlen; empty sequences are allowed.
+ *   B >= 1, 1 <= H <= 256, 1 <= max_seqlen <= DORA_MAX_SEQLEN, total >= 0.
+ *   workspace  device, 256-byte aligned, >= dora_varlen_attn_workspace_size bytes.
+ *   dev_status DORA_DEV_CU_SEQLENS when the offsets are invalid (the plan is
+ *              then empty and _execute writes nothing).
+ */
+int dora_varlen_attn_plan(const int32_t* cu_seqlens, int32_t B, int32_t H, int32_t max_seqlen,
+                          int64_t total, void* workspace, size_t workspace_bytes,
+                          int32_t* dev_status, void* stream);
+
+/*
+ * dora_varlen_attn_execute -- exact softmax attention inside each packed
+ * sequence (Sec. 3.5 "Inference"; App. E.4): for every sequence b and head h
+ *   O_b,h = softmax(softmax_scale * Q_b,h K_b,h^T) V_b,h
+ * with no causal mask, no bias and no attention across sequence boundaries.
+ *
+ *   q, k, v    dtype [total, H, D] contiguous, 16-byte aligned.
+ *   out        dtype [total, H, D]; rows outside every sequence are not written.
+ *   D          must be DORA_HEAD_DIM (64).
+ *   softmax_scale  <= 0 selects 1/sqrt(D).
+ *   dtype      DORA_BF16: bf16 inputs, fp32 accumulation and softmax, P rounded
+ *              to bf16 for the P.V product, output rounded once to bf16.
+ *              DORA_F32: fp32 throughout.
+ *   workspace  as filled by dora_varlen_attn_plan with the same cu_seqlens,
+ *              B, H, max_seqlen and total; otherwise DORA_DEV_PLAN is set and
+ *              nothing is written.
+ * Execute calls that share one workspace must not overlap in time.
+ */
+int dora_varlen_attn_execute(const void* q, const void* k, const void* v,
+                             const int32_t* cu_seqlens, int32_t B, int32_t H, int32_t D,
+                             int32_t max_seqlen, int64_t total, float softmax_scale,
+                             dora_dtype dtype, void* out, void* workspace,
+                             size_t workspace_bytes, int32_t* dev_status, void* stream);
+
+/* dora_varlen_attn -- dora_varlen_attn_plan followed by dora_varlen_attn_execute. */
+int dora_varlen_attn(const void* q, const void* k, const void* v, const int32_t* cu_seqlens,
+                     int32_t B, int32_t H, int32_t D, int32_t max_seqlen, int64_t total,
+                     float softmax_scale, dora_dtype dtype, void* out, void* workspace,
+                     size_t workspace_bytes, int32_t* dev_status, void* stream);
+
+/* Human-readable name of a dora_status value (static string). */
+const char* dora_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DORA_H_ */

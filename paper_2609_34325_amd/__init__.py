@@ -1,0 +1,275 @@
+"""DORA deployment hot path on AMD Instinct MI355X (gfx950).
+
+Thin ctypes binding over ``libdora.so`` (C ABI in ``include/dora.h``).  Every
+step of the path runs in the library's HIP kernels; this module only checks
+tensor arguments, allocates outputs with torch when the caller does not pass
+them, and forwards raw device pointers and the current HIP stream.
+
+DORA (arXiv 2609.34325): hard deletion keeps CLS and the survivors' order
+(Sec. 3.1, Eq. (1)); deployment removes the highest-scoring visual tokens
+(Sec. 3.2 "Sampling and deployment"; App. A.3); survivors are packed with
+explicit sequence boundaries and run through variable-length attention that
+never attends across images (Sec. 3.5 "Inference"; App. E.4).
+
+There is no fallback: if the library is missing, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdora.so")
+
+DORA_F32 = 0
+DORA_BF16 = 1
+
+DORA_OK = 0
+DORA_ERR_NULL = -1
+DORA_ERR_SHAPE = -2
+DORA_ERR_DTYPE = -3
+DORA_ERR_ALIGN = -4
+DORA_ERR_UNSUPPORTED = -5
+DORA_ERR_CAPACITY = -6
+DORA_ERR_HIP = -7
+DORA_ERR_WORKSPACE = -8
+
+DORA_DEV_KEEP_RANGE = 0x1
+DORA_DEV_CAPACITY = 0x2
+DORA_DEV_CU_IN = 0x4
+DORA_DEV_CU_SEQLENS = 0x8
+DORA_DEV_PLAN = 0x10
+
+DORA_MAX_ROW_TOKENS = 2048
+DORA_MAX_SEQLEN = 16384
+DORA_HEAD_DIM = 64
+
+EXPORTS = (
+    "dora_select_pack",
+    "dora_varlen_attn_workspace_size",
+    "dora_varlen_attn_plan",
+    "dora_varlen_attn_execute",
+    "dora_varlen_attn",
+    "dora_status_string",
+)
+
+_lib = None
+
+
+class DoraError(RuntimeError):
+    def __init__(self, fn: str, code: int):
+        super().__init__(f"{fn} failed: {dora_status_string(code)} ({code})")
+        self.code = code
+
+
+def load_library(path: Optional[str] = None) -> ctypes.CDLL:
+    """Load libdora.so (built in-tree by ``paper_2609_34325_amd.build``)."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError(f"libdora.so not found at {p}; build it with "
+                           "`python -m paper_2609_34325_amd.build` (no fallback path exists)")
+    lib = ctypes.CDLL(p)
+    vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    lib.dora_select_pack.restype = ctypes.c_int
+    lib.dora_select_pack.argtypes = [vp, vp, vp, vp, i64, i32, i32, i32, ctypes.c_int,
+                                     vp, vp, vp, i64, vp, vp]
+    lib.dora_varlen_attn_workspace_size.restype = sz
+    lib.dora_varlen_attn_workspace_size.argtypes = [i32, i32, i32]
+    lib.dora_varlen_attn_plan.restype = ctypes.c_int
+    lib.dora_varlen_attn_plan.argtypes = [vp, i32, i32, i32, i64, vp, sz, vp, vp]
+    lib.dora_varlen_attn_execute.restype = ctypes.c_int
+    lib.dora_varlen_attn_execute.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i64,
+                                             ctypes.c_float, ctypes.c_int, vp, vp, sz, vp, vp]
+    lib.dora_varlen_attn.restype = ctypes.c_int
+    lib.dora_varlen_attn.argtypes = lib.dora_varlen_attn_execute.argtypes
+    lib.dora_status_string.restype = ctypes.c_char_p
+    lib.dora_status_string.argtypes = [ctypes.c_int]
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def dora_status_string(code: int) -> str:
+    return load_library().dora_status_string(int(code)).decode()
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return DORA_BF16
+    if t.dtype == torch.float32:
+        return DORA_F32
+    raise TypeError(f"unsupported dtype {t.dtype}; expected bfloat16 or float32")
+
+
+def _dev(t: torch.Tensor, name: str, dtype=None) -> int:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    return t.data_ptr()
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _check(fn: str, code: int) -> None:
+    if code != DORA_OK:
+        raise DoraError(fn, code)
+
+
+def new_status(device=None) -> torch.Tensor:
+    """A zeroed int32 device status word."""
+    return torch.zeros(1, dtype=torch.int32, device=device or "cuda")
+
+
+def dora_select_pack(scores: torch.Tensor, keep: torch.Tensor, tokens: torch.Tensor,
+                     cu_in: Optional[torch.Tensor] = None, N: Optional[int] = None,
+                     idx_out: Optional[torch.Tensor] = None,
+                     cu_out: Optional[torch.Tensor] = None,
+                     packed_out: Optional[torch.Tensor] = None,
+                     cap_rows: Optional[int] = None,
+                     dev_status: Optional[torch.Tensor] = None,
+                     stream=None) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor, torch.Tensor]:
+    """Keep CLS + the keep-1 highest keep-scores per image, pack the kept rows.
+
+    Dense input: scores [B,N] fp32, tokens [B,N,C].  Packed input (a cascaded
+    round): scores [total_in], tokens [total_in,C], cu_in [B+1] and N = an
+    upper bound on the segment lengths.  keep: int32 [B] (counts CLS).
+    Outputs (allocated if not given; capacity defaults to B*N rows so no
+    host synchronisation is needed): idx [cap], cu [B+1], packed [cap,C],
+    dev_status [1].  Returns (idx_out, cu_out, packed_out, dev_status).
+    """
+    lib = load_library()
+    B = int(keep.shape[0])
+    if cu_in is None:
+        if tokens.dim() != 3:
+            raise ValueError("dense tokens must be [B,N,C]")
+        N = int(tokens.shape[1])
+        C = int(tokens.shape[2])
+        total_in = B * N
+        if tuple(scores.shape) != (B, N):
+            raise ValueError("scores must be [B,N]")
+    else:
+        if tokens.dim() != 2:
+            raise ValueError("packed tokens must be [total_in,C]")
+        if N is None:
+            raise ValueError("packed input needs N (an upper bound on segment lengths)")
+        C = int(tokens.shape[1])
+        total_in = int(tokens.shape[0])
+        if scores.dim() != 1 or int(scores.shape[0]) < total_in:
+            raise ValueError("packed scores must be [total_in]")
+        if tuple(cu_in.shape) != (B + 1,):
+            raise ValueError("cu_in must be [B+1]")
+    dev = tokens.device
+    if cap_rows is None:
+        cap_rows = int(packed_out.shape[0]) if packed_out is not None else B * int(N)
+    if idx_out is None:
+        idx_out = torch.empty(cap_rows, dtype=torch.int32, device=dev)
+    if cu_out is None:
+        cu_out = torch.empty(B + 1, dtype=torch.int32, device=dev)
+    if packed_out is None:
+        packed_out = torch.empty((cap_rows, C), dtype=tokens.dtype, device=dev)
+    if dev_status is None:
+        dev_status = new_status(dev)
+    if packed_out.dtype != tokens.dtype or int(packed_out.shape[-1]) != C:
+        raise ValueError("packed_out must match the tokens' dtype and C")
+    if int(idx_out.numel()) < cap_rows or int(packed_out.shape[0]) < cap_rows:
+        raise ValueError("outputs smaller than cap_rows")
+    rc = lib.dora_select_pack(
+        _dev(scores, "scores", torch.float32), _dev(keep, "keep", torch.int32),
+        _dev(tokens, "tokens"), None if cu_in is None else _dev(cu_in, "cu_in", torch.int32),
+        total_in, B, int(N), C, _dtype_code(tokens),
+        _dev(idx_out, "idx_out", torch.int32), _dev(cu_out, "cu_out", torch.int32),
+        _dev(packed_out, "packed_out"), int(cap_rows), _dev(dev_status, "dev_status", torch.int32),
+        _stream(stream))
+    _check("dora_select_pack", rc)
+    return idx_out, cu_out, packed_out, dev_status
+
+
+def dora_varlen_attn_workspace_size(B: int, H: int, max_seqlen: int) -> int:
+    return int(load_library().dora_varlen_attn_workspace_size(int(B), int(H), int(max_seqlen)))
+
+
+def new_workspace(B: int, H: int, max_seqlen: int, device=None) -> torch.Tensor:
+    n = dora_varlen_attn_workspace_size(B, H, max_seqlen)
+    if n == 0:
+        raise DoraError("dora_varlen_attn_workspace_size", DORA_ERR_SHAPE)
+    return torch.empty(n, dtype=torch.uint8, device=device or "cuda")
+
+
+def dora_varlen_attn_plan(cu_seqlens: torch.Tensor, H: int, max_seqlen: int, total: int,
+                          workspace: torch.Tensor, dev_status: torch.Tensor, stream=None) -> None:
+    lib = load_library()
+    B = int(cu_seqlens.shape[0]) - 1
+    rc = lib.dora_varlen_attn_plan(_dev(cu_seqlens, "cu_seqlens", torch.int32), B, int(H),
+                                   int(max_seqlen), int(total), _dev(workspace, "workspace"),
+                                   workspace.numel() * workspace.element_size(),
+                                   _dev(dev_status, "dev_status", torch.int32), _stream(stream))
+    _check("dora_varlen_attn_plan", rc)
+
+
+def _attn_args(q, k, v, cu_seqlens, out):
+    if q.dim() != 3 or q.shape != k.shape or q.shape != v.shape:
+        raise ValueError("q, k, v must share the shape [total, H, 64]")
+    if q.dtype != k.dtype or q.dtype != v.dtype:
+        raise TypeError("q, k, v must share one dtype")
+    total, H, D = (int(x) for x in q.shape)
+    if out is None:
+        out = torch.empty_like(q)
+    if out.shape != q.shape or out.dtype != q.dtype:
+        raise ValueError("out must match q")
+    return total, H, D, out
+
+
+def dora_varlen_attn_execute(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
+                             cu_seqlens: torch.Tensor, max_seqlen: int, workspace: torch.Tensor,
+                             out: Optional[torch.Tensor] = None, softmax_scale: float = 0.0,
+                             dev_status: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    lib = load_library()
+    total, H, D, out = _attn_args(q, k, v, cu_seqlens, out)
+    if dev_status is None:
+        dev_status = new_status(q.device)
+    B = int(cu_seqlens.shape[0]) - 1
+    rc = lib.dora_varlen_attn_execute(
+        _dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(cu_seqlens, "cu_seqlens", torch.int32),
+        B, H, D, int(max_seqlen), total, float(softmax_scale), _dtype_code(q), _dev(out, "out"),
+        _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
+        _dev(dev_status, "dev_status", torch.int32), _stream(stream))
+    _check("dora_varlen_attn_execute", rc)
+    return out
+
+
+def dora_varlen_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, cu_seqlens: torch.Tensor,
+                     max_seqlen: int, out: Optional[torch.Tensor] = None,
+                     workspace: Optional[torch.Tensor] = None, softmax_scale: float = 0.0,
+                     dev_status: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """softmax(scale * Q K^T) V inside each packed sequence; q/k/v/out [total, H, 64]."""
+    lib = load_library()
+    total, H, D, out = _attn_args(q, k, v, cu_seqlens, out)
+    B = int(cu_seqlens.shape[0]) - 1
+    if workspace is None:
+        workspace = new_workspace(B, H, max_seqlen, q.device)
+    if dev_status is None:
+        dev_status = new_status(q.device)
+    rc = lib.dora_varlen_attn(
+        _dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(cu_seqlens, "cu_seqlens", torch.int32),
+        B, H, D, int(max_seqlen), total, float(softmax_scale), _dtype_code(q), _dev(out, "out"),
+        _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
+        _dev(dev_status, "dev_status", torch.int32), _stream(stream))
+    _check("dora_varlen_attn", rc)
+    return out

@@ -1,0 +1,63 @@
+// Internal definitions shared by the HIP translation units of libdora.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "dora.h"
+
+namespace dora {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+// Number of compute units of the current device (cached per device id).
+int device_cu_count(int* device_out);
+
+// Wave64 helpers.
+__device__ __forceinline__ int lanes_below(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
+                                   __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
+}
+
+// ---------------------------------------------------------------------------
+// Attention work-queue workspace layout (device memory owned by the caller).
+//
+//   [0, 256)                       AttnPlanHeader
+//   [256, 256 + 4*B)               order[B]      sequences by decreasing length
+//   next, 4*(B+1) rounded to 16    item_base[B+1]
+//   next, 8*max_items              items[]       {sequence, head << 16 | q-tile}
+// ---------------------------------------------------------------------------
+constexpr int32_t kPlanMagic = 0x444F5241;  // "DORA"
+constexpr int kAttnQTile = 128;             // queries per work item (4 waves x 32)
+
+struct AttnPlanHeader {
+  int32_t counter;     // next ticket of the dynamic queue
+  int32_t exit_count;  // workgroups that have left the current execute
+  int32_t n_items;     // items in this plan
+  int32_t magic;       // kPlanMagic once planned
+  int32_t B, H, max_seqlen, q_tile;
+  int64_t total;
+  int32_t reserved[6];
+};
+static_assert(sizeof(AttnPlanHeader) <= 256, "header must fit its slot");
+
+struct AttnWorkspaceLayout {
+  size_t order_off, base_off, items_off, bytes;
+  int64_t max_items;
+};
+
+inline AttnWorkspaceLayout attn_workspace_layout(int32_t B, int32_t H, int32_t max_seqlen) {
+  AttnWorkspaceLayout L;
+  const int64_t tiles = (static_cast<int64_t>(max_seqlen) + kAttnQTile - 1) / kAttnQTile;
+  L.max_items = static_cast<int64_t>(B) * H * tiles;
+  L.order_off = 256;
+  L.base_off = L.order_off + ((static_cast<size_t>(B) * 4 + 15) & ~size_t(15));
+  L.items_off = L.base_off + ((static_cast<size_t>(B + 1) * 4 + 15) & ~size_t(15));
+  L.bytes = L.items_off + static_cast<size_t>(L.max_items) * 8;
+  L.bytes = (L.bytes + 255) & ~size_t(255);
+  return L;
+}
+
+}  // namespace dora

@@ -1,0 +1,255 @@
+// Hard deletion + packing: per-image top-k with CLS pinned, running total of
+// keep counts, and the gather of kept rows into one packed buffer.
+// DORA (arXiv 2609.34325): Sec. 3.1 Eq. (1) (delete rows, keep CLS and the
+// survivors' order), Sec. 3.2 "Sampling and deployment" and App. A.3 (remove
+// the highest-scoring visual tokens), Sec. 3.5 "Inference" (packed buffer with
+// explicit sequence boundaries), App. E.4 (FP32 score comparisons).
+//
+// One launch.  Workgroup (b, s) handles image b; the `split` workgroups of an
+// image each repeat the (cheap) selection and then copy a disjoint share of
+// the kept rows, so the HBM-bound copy is spread over many workgroups.
+//
+//   wave 0        radix select on order-preserving uint32 keys, one bit per
+//                 step, counting with wave ballots (keys live in VGPRs);
+//                 ordered compaction of the keep flags with ballot + mbcnt.
+//   waves 1..3    sum keep[0..b) -> this image's output offset (cu_out[b]).
+//   all waves     16-byte row copies, 8 loads in flight per lane.
+#include <limits.h>
+#include <stdlib.h>
+
+#include "dora_internal.h"
+
+namespace dora {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kCopyUnroll = 8;
+
+struct SelectPackParams {
+  const float* scores;
+  const int32_t* keep;
+  const uint4* tokens;
+  const int32_t* cu_in;
+  int64_t total_in;
+  int32_t B, N, row_vecs, split;
+  int32_t* idx_out;
+  int32_t* cu_out;
+  uint4* packed;
+  int64_t cap_rows;
+  int32_t* status;
+};
+
+// Order-preserving key: larger key = preferred for keeping.  -0 and +0 map
+// to the same key; every NaN maps to 0, below -inf (0x007FFFFF).
+__device__ __forceinline__ uint32_t keep_key(float x) {
+  uint32_t u = __float_as_uint(x);
+  if (x != x) return 0u;
+  if (x == 0.0f) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ long long wave_sum(long long v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+template <int SLOTS>
+__global__ __launch_bounds__(kThreads) void select_pack_kernel(SelectPackParams p) {
+  __shared__ int32_t s_idx[SLOTS * 64];
+  __shared__ long long s_part[kThreads / 64];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int b = blockIdx.x / p.split;
+  const int s = blockIdx.x - b * p.split;
+
+  // Segment of image b in the input.
+  long long off_in, n;
+  bool seg_ok = true;
+  if (p.cu_in != nullptr) {
+    const long long a = p.cu_in[b], e = p.cu_in[b + 1];
+    off_in = a;
+    n = e - a;
+    seg_ok = a >= 0 && e <= p.total_in && n >= 1 && n <= p.N && (b != 0 || a == 0);
+  } else {
+    off_in = static_cast<long long>(b) * p.N;
+    n = p.N;
+  }
+  const int kb = p.keep[b];
+  if (!seg_ok || kb < 1 || kb > n) {
+    if (s == 0 && tid == 0) atomicOr(p.status, seg_ok ? DORA_DEV_KEEP_RANGE : DORA_DEV_CU_IN);
+    return;
+  }
+
+  if (wave != 0) {
+    // Output offset of image b: keep[0] + ... + keep[b-1].
+    long long part = 0;
+    for (int j = tid - 64; j < b; j += kThreads - 64) part += p.keep[j];
+    part = wave_sum(part);
+    if (lane == 0) s_part[wave] = part;
+  } else {
+    // Candidates are positions 1..n-1 (CLS, position 0, is not a candidate).
+    // Position pos = r*64 + lane lives in key[r] of that lane.
+    uint32_t key[SLOTS];
+    uint64_t valid[SLOTS];
+#pragma unroll
+    for (int r = 0; r < SLOTS; ++r) {
+      const int pos = r * 64 + lane;
+      const bool v = pos >= 1 && pos < n;
+      key[r] = v ? keep_key(p.scores[off_in + pos]) : 0u;
+      valid[r] = __ballot(v);
+    }
+    // Threshold T = the need-th largest candidate key; q = how many of the
+    // candidates equal to T are kept (the lowest positions among them).
+    const int need = kb - 1;
+    uint32_t T = 0xFFFFFFFFu;  // need == 0: nothing compares above or equal
+    int q = 0;
+    if (need > 0) {
+      T = 0u;
+      for (int bit = 31; bit >= 0; --bit) {
+        const uint32_t t = T | (1u << bit);
+        int cnt = 0;
+#pragma unroll
+        for (int r = 0; r < SLOTS; ++r) cnt += __popcll(__ballot(key[r] >= t));  // t >= 1: invalid keys (0) never count
+        if (cnt >= need) T = t;
+      }
+      int gt = 0;
+#pragma unroll
+      for (int r = 0; r < SLOTS; ++r) gt += __popcll(__ballot(key[r] > T) & valid[r]);
+      q = need - gt;
+    }
+    // Ordered compaction: kept positions in ascending order.
+    int cum_eq = 0, cum_keep = 0;
+#pragma unroll
+    for (int r = 0; r < SLOTS; ++r) {
+      const int pos = r * 64 + lane;
+      const bool is_valid = (valid[r] >> lane) & 1ull;
+      const bool above = is_valid && key[r] > T;
+      const bool tie = is_valid && key[r] == T;
+      const uint64_t tie_mask = __ballot(tie);
+      const bool kept = pos == 0 || above || (tie && cum_eq + lanes_below(tie_mask) < q);
+      const uint64_t kept_mask = __ballot(kept);
+      if (kept) s_idx[cum_keep + lanes_below(kept_mask)] = pos;
+      cum_eq += __popcll(tie_mask);
+      cum_keep += __popcll(kept_mask);
+    }
+  }
+  __syncthreads();
+  const long long off_out = s_part[1] + s_part[2] + s_part[3];
+
+  if (s == 0) {
+    if (tid == 0) {
+      if (off_out + kb > p.cap_rows) atomicOr(p.status, DORA_DEV_CAPACITY);
+      p.cu_out[b + 1] = static_cast<int32_t>(off_out + kb);
+      if (b == 0) p.cu_out[0] = 0;
+    }
+    for (int i = tid; i < kb; i += kThreads) {
+      const long long row = off_out + i;
+      if (row >= 0 && row < p.cap_rows) p.idx_out[row] = s_idx[i];
+    }
+  }
+
+  // This workgroup's share of the kept rows.
+  const int rows_per = (kb + p.split - 1) / p.split;
+  const int r0 = s * rows_per;
+  const int r1 = min(kb, r0 + rows_per);
+  if (r0 >= r1) return;
+  const int vpr = p.row_vecs;
+  const int nvec = (r1 - r0) * vpr;
+  const int step_rows = kThreads / vpr;
+  const int step_vecs = kThreads - step_rows * vpr;
+  int row = tid / vpr;
+  int vec = tid - row * vpr;
+  for (int base = tid; base < nvec; base += kThreads * kCopyUnroll) {
+    uint4 buf[kCopyUnroll];
+    long long dst[kCopyUnroll];
+#pragma unroll
+    for (int u = 0; u < kCopyUnroll; ++u) {
+      const bool in_range = base + u * kThreads < nvec;
+      const int pos = s_idx[in_range ? r0 + row : r0];
+      const long long src_row = off_in + min(max(pos, 0), static_cast<int>(n) - 1);  // always inside the segment
+      const long long out_row = off_out + r0 + row;
+      buf[u] = in_range ? p.tokens[src_row * vpr + vec] : make_uint4(0u, 0u, 0u, 0u);
+      dst[u] = (in_range && out_row >= 0 && out_row < p.cap_rows) ? out_row * vpr + vec : -1;
+      row += step_rows;
+      vec += step_vecs;
+      if (vec >= vpr) {
+        vec -= vpr;
+        ++row;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kCopyUnroll; ++u)
+      if (dst[u] >= 0) p.packed[dst[u]] = buf[u];
+  }
+}
+
+template <int SLOTS>
+hipError_t launch(const SelectPackParams& p, hipStream_t stream) {
+  hipLaunchKernelGGL(select_pack_kernel<SLOTS>, dim3(p.B * p.split), dim3(kThreads), 0, stream, p);
+  return hipGetLastError();
+}
+
+int pick_split(int B, int N) {
+  static int override_split = -1;
+  if (override_split < 0) {
+    const char* e = getenv("DORA_SELECT_SPLIT");
+    override_split = e ? atoi(e) : 0;
+  }
+  int split = override_split > 0 ? override_split : (2048 + B - 1) / B;
+  const int max_split = N / 16 > 1 ? N / 16 : 1;  // at least ~16 rows per workgroup
+  if (split > max_split) split = max_split;
+  if (split < 1) split = 1;
+  while (static_cast<long long>(split) * B > INT_MAX) --split;
+  return split;
+}
+
+}  // namespace
+}  // namespace dora
+
+extern "C" int dora_select_pack(const float* scores, const int32_t* keep, const void* tokens,
+                                const int32_t* cu_in, int64_t total_in, int32_t B, int32_t N,
+                                int32_t C, dora_dtype dtype, int32_t* idx_out, int32_t* cu_out,
+                                void* packed_out, int64_t cap_rows, int32_t* dev_status,
+                                void* stream) {
+  using namespace dora;
+  if (!scores || !keep || !tokens || !idx_out || !cu_out || !packed_out || !dev_status)
+    return DORA_ERR_NULL;
+  if (dtype != DORA_F32 && dtype != DORA_BF16) return DORA_ERR_DTYPE;
+  if (B < 1 || N < 1 || N > DORA_MAX_ROW_TOKENS || C < 1) return DORA_ERR_SHAPE;
+  if (cu_in != nullptr && total_in < 0) return DORA_ERR_SHAPE;
+  const int64_t row_bytes = static_cast<int64_t>(C) * (dtype == DORA_F32 ? 4 : 2);
+  if (row_bytes % 16 != 0) return DORA_ERR_ALIGN;
+  if (row_bytes > (int64_t(1) << 20)) return DORA_ERR_UNSUPPORTED;
+  if ((reinterpret_cast<uintptr_t>(tokens) | reinterpret_cast<uintptr_t>(packed_out)) & 15u)
+    return DORA_ERR_ALIGN;
+  if (cap_rows < 1 || cap_rows > INT_MAX) return DORA_ERR_CAPACITY;
+
+  SelectPackParams p;
+  p.scores = scores;
+  p.keep = keep;
+  p.tokens = static_cast<const uint4*>(tokens);
+  p.cu_in = cu_in;
+  p.total_in = total_in;
+  p.B = B;
+  p.N = N;
+  p.row_vecs = static_cast<int32_t>(row_bytes / 16);
+  p.split = pick_split(B, N);
+  p.idx_out = idx_out;
+  p.cu_out = cu_out;
+  p.packed = static_cast<uint4*>(packed_out);
+  p.cap_rows = cap_rows;
+  p.status = dev_status;
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t err;
+  if (N <= 64) err = launch<1>(p, st);
+  else if (N <= 128) err = launch<2>(p, st);
+  else if (N <= 256) err = launch<4>(p, st);
+  else if (N <= 512) err = launch<8>(p, st);
+  else if (N <= 1024) err = launch<16>(p, st);
+  else err = launch<32>(p, st);
+  return err == hipSuccess ? DORA_OK : DORA_ERR_HIP;
+}

@@ -1,0 +1,116 @@
+"""The C ABI library loads, exports every declared symbol, and rejects bad
+arguments on the host before touching the GPU (CPU only; no compute calls)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_34325_amd as dora
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dora.h")
+FAKE = 0x100000  # never dereferenced: every call below fails validation first
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dora_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_and_binding_agree():
+    assert declared_functions() == sorted(dora.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = dora.load_library()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_constants_match_header():
+    text = open(HEADER).read()
+    for name in ["DORA_DEV_KEEP_RANGE", "DORA_DEV_CAPACITY", "DORA_DEV_CU_IN", "DORA_DEV_CU_SEQLENS",
+                 "DORA_DEV_PLAN", "DORA_MAX_ROW_TOKENS", "DORA_MAX_SEQLEN", "DORA_HEAD_DIM"]:
+        m = re.search(r"#define\s+%s\s+(0x[0-9a-fA-F]+|\d+)" % name, text)
+        assert m and int(m.group(1), 0) == getattr(dora, name), name
+    for name, val in re.findall(r"(DORA_(?:OK|ERR_[A-Z]+))\s*=\s*(-?\d+)", text):
+        assert getattr(dora, name) == int(val), name
+
+
+def test_status_strings():
+    assert dora.dora_status_string(0) == "DORA_OK"
+    for code in range(-8, 0):
+        assert dora.dora_status_string(code).startswith("DORA_ERR_")
+    assert "unknown" in dora.dora_status_string(-99)
+
+
+def call_select(lib, **kw):
+    a = dict(scores=FAKE, keep=FAKE, tokens=FAKE, cu_in=None, total_in=0, B=4, N=197, C=768, dtype=1,
+             idx=FAKE, cu=FAKE, packed=FAKE, cap=100, status=FAKE, stream=None)
+    a.update(kw)
+    return lib.dora_select_pack(a["scores"], a["keep"], a["tokens"], a["cu_in"], a["total_in"], a["B"],
+                                a["N"], a["C"], a["dtype"], a["idx"], a["cu"], a["packed"], a["cap"],
+                                a["status"], a["stream"])
+
+
+def test_select_pack_host_validation():
+    lib = dora.load_library()
+    assert call_select(lib, scores=None) == dora.DORA_ERR_NULL
+    assert call_select(lib, status=None) == dora.DORA_ERR_NULL
+    assert call_select(lib, dtype=7) == dora.DORA_ERR_DTYPE
+    assert call_select(lib, B=0) == dora.DORA_ERR_SHAPE
+    assert call_select(lib, N=0) == dora.DORA_ERR_SHAPE
+    assert call_select(lib, N=dora.DORA_MAX_ROW_TOKENS + 1) == dora.DORA_ERR_SHAPE
+    assert call_select(lib, C=3) == dora.DORA_ERR_ALIGN            # 6-byte bf16 rows
+    assert call_select(lib, C=6, dtype=0) == dora.DORA_ERR_ALIGN    # 24-byte fp32 rows
+    assert call_select(lib, tokens=FAKE + 8) == dora.DORA_ERR_ALIGN
+    assert call_select(lib, packed=FAKE + 2) == dora.DORA_ERR_ALIGN
+    assert call_select(lib, cap=0) == dora.DORA_ERR_CAPACITY
+    assert call_select(lib, cap=2 ** 31) == dora.DORA_ERR_CAPACITY
+    assert call_select(lib, cu_in=FAKE, total_in=-1) == dora.DORA_ERR_SHAPE
+
+
+def test_workspace_size():
+    assert dora.dora_varlen_attn_workspace_size(256, 12, 197) > 0
+    assert dora.dora_varlen_attn_workspace_size(0, 12, 197) == 0
+    assert dora.dora_varlen_attn_workspace_size(4, 0, 197) == 0
+    assert dora.dora_varlen_attn_workspace_size(4, 3, dora.DORA_MAX_SEQLEN + 1) == 0
+    a = dora.dora_varlen_attn_workspace_size(256, 12, 197)
+    b = dora.dora_varlen_attn_workspace_size(256, 12, 577)
+    assert b > a and a % 256 == 0
+
+
+def test_attention_host_validation():
+    lib = dora.load_library()
+    ws = dora.dora_varlen_attn_workspace_size(4, 3, 197)
+
+    def ex(**kw):
+        a = dict(q=FAKE, k=FAKE, v=FAKE, cu=FAKE, B=4, H=3, D=64, max_seqlen=197, total=100, scale=0.0,
+                 dtype=1, out=FAKE, ws=FAKE, ws_bytes=ws, status=FAKE, stream=None)
+        a.update(kw)
+        args = (a["q"], a["k"], a["v"], a["cu"], a["B"], a["H"], a["D"], a["max_seqlen"], a["total"],
+                a["scale"], a["dtype"], a["out"], a["ws"], a["ws_bytes"], a["status"], a["stream"])
+        return lib.dora_varlen_attn_execute(*args), lib.dora_varlen_attn(*args)
+
+    assert ex(q=None) == (dora.DORA_ERR_NULL,) * 2
+    assert ex(dtype=5) == (dora.DORA_ERR_DTYPE,) * 2
+    assert ex(D=128) == (dora.DORA_ERR_SHAPE,) * 2
+    assert ex(q=FAKE + 4) == (dora.DORA_ERR_ALIGN,) * 2
+    assert ex(ws=FAKE + 16) == (dora.DORA_ERR_WORKSPACE,) * 2
+    assert ex(ws_bytes=ws - 1) == (dora.DORA_ERR_WORKSPACE,) * 2
+    assert ex(B=0) == (dora.DORA_ERR_SHAPE,) * 2
+    assert ex(max_seqlen=0) == (dora.DORA_ERR_SHAPE,) * 2
+    assert ex(total=-1) == (dora.DORA_ERR_SHAPE,) * 2
+    assert lib.dora_varlen_attn_plan(None, 4, 3, 197, 100, FAKE, ws, FAKE, None) == dora.DORA_ERR_NULL
+    assert lib.dora_varlen_attn_plan(FAKE, 4, 3, 197, 100, None, ws, FAKE, None) == dora.DORA_ERR_WORKSPACE
+
+
+def test_product_package_does_not_touch_the_oracle():
+    pkg = os.path.dirname(dora.__file__)
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert "oracle" not in text.lower(), f

@@ -14,8 +14,10 @@ scores, tokens and Q/K/V are drawn from the stated distributions instead.
 
 Conventions
 -----------
-* ``numpy.random.default_rng(seed)`` (PCG64), fixed draw order per round:
-  keep -> scores -> tokens (first round only) -> Q -> K -> V.
+* Every quantity of every round draws from its own PCG64 stream,
+  ``numpy.random.default_rng([seed, round, part])`` with part 0..5 for
+  keep, scores, tokens (first round only), Q, K, V, so any subset can be
+  drawn without changing the others.
 * Keep counts derived from a ratio r use ``clip(rint(r * n), 1, n)``.
 * bf16 values are the round-to-nearest-even truncation of the float32 draw,
   stored as raw ``uint16`` bit patterns.
@@ -23,7 +25,7 @@ Conventions
 """
 from __future__ import annotations
 
-from dataclasses import dataclass, field
+from dataclasses import dataclass
 from typing import List, Optional
 
 import numpy as np
@@ -93,12 +95,12 @@ HEADLINE = "deit_b_bf16"
 class RoundInputs:
     """Inputs of one select -> pack -> attention pass."""
     keep: np.ndarray                 # int32 [B]
-    scores: np.ndarray               # float32 [B,N] (dense) or [sum n_in] (packed, later rounds)
+    scores: Optional[np.ndarray]     # float32 [B,N] (dense) or [sum n_in] (packed, later rounds)
     n_in: np.ndarray                 # int32 [B] segment lengths of the input
     tokens: Optional[np.ndarray]     # [B,N,C] or None (later cascade rounds use the previous packed output)
-    q: np.ndarray                    # [sum keep, H, 64]
-    k: np.ndarray
-    v: np.ndarray
+    q: Optional[np.ndarray]          # [sum keep, H, 64]
+    k: Optional[np.ndarray]
+    v: Optional[np.ndarray]
 
     @property
     def total_keep(self) -> int:
@@ -150,36 +152,44 @@ def _draw_scores(w: Workload, rng: np.random.Generator, n: np.ndarray) -> np.nda
     return s
 
 
-def generate(w: Workload, seed: Optional[int] = None, batch: Optional[int] = None) -> List[RoundInputs]:
+PARTS = ("keep", "scores", "tokens", "qkv")
+
+
+def _rng(seed: int, rnd: int, part: int) -> np.random.Generator:
+    return np.random.default_rng([seed, rnd, part])
+
+
+def generate(w: Workload, seed: Optional[int] = None, batch: Optional[int] = None,
+             parts=PARTS) -> List[RoundInputs]:
     """Draw all rounds of workload ``w``.
 
     ``batch`` optionally overrides B (used for reduced-size parity cases); the
-    seed then still fixes every draw.  Later cascade rounds take their segment
-    lengths from the previous round's keep counts; their token input is the
-    previous round's packed output and their segment offsets are the previous
-    round's ``cu_seqlens``, both produced by whichever side (oracle or GPU) ran
-    that round, so ``tokens`` is None there.
+    seed then still fixes every draw.  ``parts`` limits what is drawn (keep
+    counts are always drawn; missing parts are None).  Later cascade rounds
+    take their segment lengths from the previous round's keep counts; their
+    token input is the previous round's packed output and their segment
+    offsets are the previous round's ``cu_seqlens``, both produced by
+    whichever side (oracle or GPU) ran that round, so ``tokens`` is None there.
     """
     if batch is not None:
         w = Workload(w.name, w.seed, batch, w.N, w.H, w.dtype, w.keep_rule, w.rounds, w.description)
-    rng = np.random.default_rng(w.seed if seed is None else seed)
+    sd = w.seed if seed is None else seed
     n = np.full(w.B, w.N, dtype=np.int32)
     rounds: List[RoundInputs] = []
     for r in range(w.rounds):
-        keep = _draw_keep(w, rng, n)
-        scores = _draw_scores(w, rng, n)
-        dense = r == 0
-        if dense:
-            scores = scores.reshape(w.B, w.N)
-            tokens = _normal(rng, (w.B, w.N, w.C), w.dtype)
-        else:
-            tokens = None
+        keep = _draw_keep(w, _rng(sd, r, 0), n)
+        scores = _draw_scores(w, _rng(sd, r, 1), n) if "scores" in parts else None
+        tokens = None
+        if r == 0:
+            if scores is not None:
+                scores = scores.reshape(w.B, w.N)
+            if "tokens" in parts:
+                tokens = _normal(_rng(sd, r, 2), (w.B, w.N, w.C), w.dtype)
         tot = int(keep.astype(np.int64).sum())
-        q = _normal(rng, (tot, w.H, HEAD_DIM), w.dtype)
-        k = _normal(rng, (tot, w.H, HEAD_DIM), w.dtype)
-        v = _normal(rng, (tot, w.H, HEAD_DIM), w.dtype)
-        rounds.append(RoundInputs(keep=keep, scores=scores, n_in=n.copy(),
-                                  tokens=tokens, q=q, k=k, v=v))
+        q = k = v = None
+        if "qkv" in parts:
+            q, k, v = (_normal(_rng(sd, r, 3 + i), (tot, w.H, HEAD_DIM), w.dtype) for i in range(3))
+        rounds.append(RoundInputs(keep=keep, scores=scores, n_in=n.copy(), tokens=tokens, q=q, k=k, v=v))
         n = keep.copy()
     return rounds
 
