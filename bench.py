@@ -81,6 +81,9 @@ def main() -> int:
     ap.add_argument("--repeats", type=int, default=5)
     ap.add_argument("--workload", default=W.HEADLINE, choices=sorted(W.WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="before timing, run one plain device copy of MIB MiB (a reference dispatch "
+                         "for scaling hardware byte counters)")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM bytes per launch (from rocprofv3 counters), if present")
     args = ap.parse_args()
@@ -131,6 +134,14 @@ def main() -> int:
         dora.dora_varlen_attn_execute(q, k, v, cu, max_seqlen, ws, out=out, dev_status=st, stream=stream)
         if ev is not None:
             ev[3].record(stream)
+
+    if args.calibrate_copy > 0:
+        src = torch.ones(args.calibrate_copy * 2 ** 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     for _ in range(args.warmup):
         step()

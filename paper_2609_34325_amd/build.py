@@ -26,6 +26,9 @@ HIPCC_FLAGS = [
     "-Wno-unused-function",
     # Keep the compiler from forming packed-fp32 VALU ops (v_pk_*_f32).
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # Queue tickets are taken by one lane; keep the atomic as written so its
+    # result is not broadcast to scalar registers (and waited on) at issue.
+    "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
     "-I", INCLUDE,
 ]
 

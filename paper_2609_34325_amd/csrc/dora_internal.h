@@ -24,13 +24,16 @@ __device__ __forceinline__ int lanes_below(uint64_t mask) {
 // ---------------------------------------------------------------------------
 // Attention work-queue workspace layout (device memory owned by the caller).
 //
-//   [0, 256)                       AttnPlanHeader
-//   [256, 256 + 4*B)               order[B]      sequences by decreasing length
-//   next, 4*(B+1) rounded to 16    item_base[B+1]
-//   next, 8*max_items              items[]       {sequence, head << 16 | q-tile}
+//   [0, 256)      AttnPlanHeader
+//   [256, ...)    items[max_items]: int2 {x = first row of the sequence,
+//                 y = len << 17 | head << 9 | query chunk}
+//
+// A work item is one (sequence, head, chunk of kAttnQTile queries); items are
+// ordered by decreasing sequence length.
 // ---------------------------------------------------------------------------
 constexpr int32_t kPlanMagic = 0x444F5241;  // "DORA"
-constexpr int kAttnQTile = 128;             // queries per work item (4 waves x 32)
+constexpr int kAttnQTile = 256;             // queries per work item (8 waves x 32)
+constexpr int kPlanMaxB = 8192;             // sequences one plan can order
 
 struct AttnPlanHeader {
   int32_t counter;     // next ticket of the dynamic queue
@@ -44,17 +47,15 @@ struct AttnPlanHeader {
 static_assert(sizeof(AttnPlanHeader) <= 256, "header must fit its slot");
 
 struct AttnWorkspaceLayout {
-  size_t order_off, base_off, items_off, bytes;
+  size_t items_off, bytes;
   int64_t max_items;
 };
 
 inline AttnWorkspaceLayout attn_workspace_layout(int32_t B, int32_t H, int32_t max_seqlen) {
   AttnWorkspaceLayout L;
-  const int64_t tiles = (static_cast<int64_t>(max_seqlen) + kAttnQTile - 1) / kAttnQTile;
-  L.max_items = static_cast<int64_t>(B) * H * tiles;
-  L.order_off = 256;
-  L.base_off = L.order_off + ((static_cast<size_t>(B) * 4 + 15) & ~size_t(15));
-  L.items_off = L.base_off + ((static_cast<size_t>(B + 1) * 4 + 15) & ~size_t(15));
+  const int64_t chunks = (static_cast<int64_t>(max_seqlen) + kAttnQTile - 1) / kAttnQTile;
+  L.max_items = static_cast<int64_t>(B) * H * chunks;
+  L.items_off = 256;
   L.bytes = L.items_off + static_cast<size_t>(L.max_items) * 8;
   L.bytes = (L.bytes + 255) & ~size_t(255);
   return L;

@@ -5,22 +5,32 @@
 // boundaries, no bias, no token-size term).
 //
 // Work decomposition (persistent, queue-driven):
-//   plan     one workgroup builds the list of (sequence, head, 128-query tile)
-//            items, sequences sorted by decreasing length (longest first), and
-//            resets the queue counters.
-//   execute  #CU x occupancy persistent workgroups; each takes item tickets
-//            from an atomic counter until the list is drained; the last
-//            workgroup to leave resets the counters so the plan can be
-//            executed again (e.g. by the next layer).
+//   plan     one workgroup validates cu_seqlens, orders the sequences by
+//            decreasing length (counting sort) and writes the item list
+//            (sequence, head, chunk of 256 queries), each item carrying its
+//            first row and length so the executing kernel needs no other
+//            lookup; it also resets the queue counters.
+//   execute  one 512-thread workgroup per compute unit takes item tickets from
+//            an atomic counter until the list is drained; the last workgroup
+//            to leave resets the counters so the plan can run again (e.g. for
+//            every layer between two pruning steps).
 //
-// Per item, 4 waves x 32 queries.  K/V are streamed through LDS in blocks of
-// 64 keys (K row-major, V transposed so both MFMA operands read contiguous
-// runs).  S^T = K Q^T is computed with v_mfma_f32_16x16x32_bf16 so each lane
-// owns one query column and the softmax reductions over keys stay mostly
-// in-lane; the online softmax runs in fp32 with exp2 and a pre-folded
-// scale*log2(e); P is rounded to bf16 and O^T += V^T P^T reuses the MFMA
-// output registers of S^T directly as the B operand (the key order inside a
-// 32-key step is permuted identically on both operands).
+// bf16 kernel, per work item: 8 waves x 2 tiles of 16 queries.  Up to 256
+// keys of K and V (both row-major) are resident in LDS per stage, so a
+// ViT-sized sequence is staged once.  While a stage computes, the next stage's K/V and
+// Q are already in flight into registers (register-staged double buffering),
+// and the queue ticket / item descriptor two items ahead are fetched too, so
+// the HBM traffic of item i+1 overlaps the MFMA work of item i.
+//
+// V^T operands come from the transposing LDS read (ds_read_b64_tr_b16), so V
+// needs no transpose on its way into LDS.
+// S^T = K Q^T is computed with v_mfma_f32_16x16x32_bf16 so each lane owns one
+// query column and the softmax reductions over keys stay mostly in-lane; the
+// online softmax runs in fp32 with exp2 of one FMA per score (scale*log2(e)
+// folded in) and lazy rescaling; P is rounded to bf16 and O^T += V^T P^T takes
+// the S^T output registers directly as its B operand (the key order inside a
+// 32-key step is permuted the same way on both operands).  The softmax
+// denominators come from the matrix unit as well: a block of ones times P^T.
 #include <limits.h>
 #include <math.h>
 
@@ -30,11 +40,12 @@ namespace dora {
 namespace {
 
 constexpr int kD = 64;
-constexpr int kBlockKeys = 64;
-constexpr int kWaves = 4;
+constexpr int kWaves = 8;
+constexpr int kThreads = kWaves * 64;
 constexpr int kQPerWave = 32;
 static_assert(kWaves * kQPerWave == kAttnQTile, "tile size");
-constexpr int kThreads = kWaves * 64;
+constexpr int kKRes = 256;             // keys resident in LDS per stage (bf16)
+constexpr int kKStride = kD + 8;       // bf16 elements per K / V row in LDS (conflict-free reads)
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanBins = 1024;
 constexpr float kLog2e = 1.4426950408889634f;
@@ -44,10 +55,7 @@ struct PlanParams {
   int32_t B, H, max_seqlen;
   int64_t total;
   AttnPlanHeader* hdr;
-  int32_t* order;
-  int32_t* item_base;
   int2* items;
-  int64_t max_items;
   int32_t* status;
 };
 
@@ -56,7 +64,6 @@ struct AttnParams {
   const void* k;
   const void* v;
   void* out;
-  const int32_t* cu;
   int32_t B, H, max_seqlen;
   int64_t total;
   float scale_log2;  // softmax_scale * log2(e)
@@ -66,26 +73,55 @@ struct AttnParams {
   int32_t* status;
 };
 
-__device__ __forceinline__ int block_exclusive_scan(int v, int* tmp, int* total_out) {
-  // kPlanThreads-wide exclusive scan through LDS (Hillis-Steele).
-  const int tid = threadIdx.x;
-  tmp[tid] = v;
-  __syncthreads();
-  for (int off = 1; off < kPlanThreads; off <<= 1) {
-    const int add = tid >= off ? tmp[tid - off] : 0;
-    __syncthreads();
-    tmp[tid] += add;
-    __syncthreads();
+// ------------------------------- plan -------------------------------------
+
+__device__ __forceinline__ int wave_inclusive_scan(int v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int t = __shfl_up(v, off, 64);
+    if (lane >= off) v += t;
   }
-  const int incl = tmp[tid];
-  *total_out = tmp[kPlanThreads - 1];
+  return v;
+}
+
+// Exclusive scan of one value per thread across the 1024-thread block.
+__device__ int block_exclusive_scan(int v, int* wave_sums, int* total) {
+  constexpr int kW = kPlanThreads / 64;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int incl = wave_inclusive_scan(v);
+  if (lane == 63) wave_sums[wave] = incl;
   __syncthreads();
-  return incl - v;
+  if (wave == 0) {
+    const int x = lane < kW ? wave_sums[lane] : 0;
+    const int xi = wave_inclusive_scan(x);
+    if (lane < kW) wave_sums[lane] = xi - x;
+    if (lane == kW - 1) wave_sums[kW] = xi;
+  }
+  __syncthreads();
+  const int r = incl - v + wave_sums[wave];
+  *total = wave_sums[kW];
+  __syncthreads();
+  return r;
+}
+
+__device__ __forceinline__ void write_header(const PlanParams& p, int n_items) {
+  p.hdr->n_items = n_items;
+  p.hdr->counter = 0;
+  p.hdr->exit_count = 0;
+  p.hdr->B = p.B;
+  p.hdr->H = p.H;
+  p.hdr->max_seqlen = p.max_seqlen;
+  p.hdr->q_tile = kAttnQTile;
+  p.hdr->total = p.total;
+  p.hdr->magic = kPlanMagic;
 }
 
 __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanParams p) {
   __shared__ int hist[kPlanBins];
-  __shared__ int scan_tmp[kPlanThreads];
+  __shared__ uint32_t order[kPlanMaxB];  // sequence | len << 13, by decreasing length
+  __shared__ int base[kPlanMaxB + 1];    // first item of each sorted position
+  __shared__ int wave_sums[kPlanThreads / 64 + 1];
   __shared__ int s_bad;
   const int tid = threadIdx.x;
   int shift = 0;
@@ -94,93 +130,113 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanParams p) {
   for (int i = tid; i < kPlanBins; i += kPlanThreads) hist[i] = 0;
   if (tid == 0) s_bad = (p.cu[0] != 0);
   __syncthreads();
-
-  // Validate the offsets and histogram the lengths.
   for (int b = tid; b < p.B; b += kPlanThreads) {
     const long long a = p.cu[b], e = p.cu[b + 1];
     const long long len = e - a;
-    if (a < 0 || e > p.total || len < 0 || len > p.max_seqlen) {
-      s_bad = 1;
-    } else {
-      atomicAdd(&hist[static_cast<int>(len) >> shift], 1);
-    }
+    if (a < 0 || e > p.total || len < 0 || len > p.max_seqlen) s_bad = 1;
+    else atomicAdd(&hist[static_cast<int>(len) >> shift], 1);
   }
   __syncthreads();
   if (s_bad) {
     if (tid == 0) {
       atomicOr(p.status, DORA_DEV_CU_SEQLENS);
-      p.hdr->n_items = 0;
-      p.hdr->counter = 0;
-      p.hdr->exit_count = 0;
-      p.hdr->B = p.B;
-      p.hdr->H = p.H;
-      p.hdr->max_seqlen = p.max_seqlen;
-      p.hdr->q_tile = kAttnQTile;
-      p.hdr->total = p.total;
-      p.hdr->magic = kPlanMagic;
+      write_header(p, 0);
     }
     return;
   }
 
-  // Start position of each length bin in decreasing-length order.
+  // Counting sort by length, longest first.
   {
-    int sum_total;
-    const int bin = kPlanBins - 1 - tid;  // thread t scans bin (top - t)
-    const int cnt = hist[bin];
-    __syncthreads();
-    const int start = block_exclusive_scan(cnt, scan_tmp, &sum_total);
+    const int bin = kPlanBins - 1 - tid;
+    int unused;
+    const int start = block_exclusive_scan(hist[bin], wave_sums, &unused);
     hist[bin] = start;
-    __syncthreads();
   }
+  __syncthreads();
   for (int b = tid; b < p.B; b += kPlanThreads) {
     const int len = p.cu[b + 1] - p.cu[b];
     const int pos = atomicAdd(&hist[len >> shift], 1);
-    p.order[pos] = b;
+    order[pos] = static_cast<uint32_t>(b) | (static_cast<uint32_t>(len) << 13);
   }
-  __threadfence_block();
   __syncthreads();
 
-  // Item offsets per sorted position, then the items themselves.
-  int carry = 0;
-  for (int base = 0; base < p.B; base += kPlanThreads) {
-    const int pos = base + tid;
-    int cnt = 0;
-    if (pos < p.B) {
-      const int b = p.order[pos];
-      const int len = p.cu[b + 1] - p.cu[b];
-      cnt = p.H * ((len + kAttnQTile - 1) / kAttnQTile);
-    }
-    int chunk_total;
-    const int off = block_exclusive_scan(cnt, scan_tmp, &chunk_total);
-    if (pos < p.B) {
-      p.item_base[pos] = carry + off;
-      const int b = p.order[pos];
-      const int len = p.cu[b + 1] - p.cu[b];
-      const int tiles = (len + kAttnQTile - 1) / kAttnQTile;
-      int2* dst = p.items + carry + off;
-      for (int h = 0; h < p.H; ++h)
-        for (int t = 0; t < tiles; ++t) dst[h * tiles + t] = make_int2(b, (h << 16) | t);
-    }
-    carry += chunk_total;
+  // Items per sorted position, then their offsets.
+  const int per = (p.B + kPlanThreads - 1) / kPlanThreads;
+  int local = 0;
+  for (int i = 0; i < per; ++i) {
+    const int pos = tid * per + i;
+    if (pos < p.B) local += p.H * static_cast<int>(((order[pos] >> 13) + kAttnQTile - 1) / kAttnQTile);
   }
-  if (tid == 0) {
-    p.item_base[p.B] = carry;
-    p.hdr->n_items = carry;
-    p.hdr->counter = 0;
-    p.hdr->exit_count = 0;
-    p.hdr->B = p.B;
-    p.hdr->H = p.H;
-    p.hdr->max_seqlen = p.max_seqlen;
-    p.hdr->q_tile = kAttnQTile;
-    p.hdr->total = p.total;
-    p.hdr->magic = kPlanMagic;
+  int n_items;
+  int run = block_exclusive_scan(local, wave_sums, &n_items);
+  for (int i = 0; i < per; ++i) {
+    const int pos = tid * per + i;
+    if (pos < p.B) {
+      base[pos] = run;
+      run += p.H * static_cast<int>(((order[pos] >> 13) + kAttnQTile - 1) / kAttnQTile);
+    }
   }
+  if (tid == 0) base[p.B] = n_items;
+  __syncthreads();
+
+  // Emit: item t belongs to the last sorted position whose first item <= t.
+  for (int t = tid; t < n_items; t += kPlanThreads) {
+    int lo = 0, hi = p.B - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (base[mid] <= t) lo = mid;
+      else hi = mid - 1;
+    }
+    const uint32_t o = order[lo];
+    const int b = static_cast<int>(o & 0x1FFFu);
+    const int len = static_cast<int>(o >> 13);
+    const int chunks = (len + kAttnQTile - 1) / kAttnQTile;
+    const int li = t - base[lo];
+    const int h = li / chunks, c = li - h * chunks;
+    p.items[t] = make_int2(p.cu[b], static_cast<int>((static_cast<uint32_t>(len) << 17) |
+                                                     (static_cast<uint32_t>(h) << 9) |
+                                                     static_cast<uint32_t>(c)));
+  }
+  if (tid == 0) write_header(p, n_items);
 }
+
+// ------------------------------ execute -----------------------------------
+
+struct Item {
+  int seq0, len, h, chunk;
+};
 
 __device__ __forceinline__ bool plan_matches(const AttnParams& p) {
   const AttnPlanHeader* h = p.hdr;
   return h->magic == kPlanMagic && h->B == p.B && h->H == p.H && h->max_seqlen == p.max_seqlen &&
          h->q_tile == kAttnQTile && h->total == p.total;
+}
+
+// Decodes an item; an item that does not fit the sizes (a stale plan) is
+// reported and replaced by an empty one so that nothing is read or written.
+__device__ __forceinline__ Item decode_item(const AttnParams& p, int2 raw) {
+  Item it;
+  const uint32_t y = static_cast<uint32_t>(raw.y);
+  it.seq0 = raw.x;
+  it.len = static_cast<int>(y >> 17);
+  it.h = static_cast<int>((y >> 9) & 0xFFu);
+  it.chunk = static_cast<int>(y & 0x1FFu);
+  const bool ok = raw.x >= 0 && it.len <= p.max_seqlen &&
+                  static_cast<long long>(raw.x) + it.len <= p.total && it.h < p.H &&
+                  it.chunk * kAttnQTile < it.len;
+  if (!ok) {
+    if (threadIdx.x == 0) atomicOr(p.status, DORA_DEV_CU_SEQLENS);
+    it.seq0 = 0;
+    it.len = 0;
+    it.h = 0;
+    it.chunk = 0;
+  }
+  // Descriptors are the same in every lane; keep them in scalar registers.
+  it.seq0 = __builtin_amdgcn_readfirstlane(it.seq0);
+  it.len = __builtin_amdgcn_readfirstlane(it.len);
+  it.h = __builtin_amdgcn_readfirstlane(it.h);
+  it.chunk = __builtin_amdgcn_readfirstlane(it.chunk);
+  return it;
 }
 
 __device__ __forceinline__ void leave_queue(AttnPlanHeader* hdr) {
@@ -195,31 +251,231 @@ __device__ __forceinline__ void leave_queue(AttnPlanHeader* hdr) {
   }
 }
 
-__device__ __forceinline__ bool item_bounds(const AttnParams& p, int b, int h, int tile,
-                                            long long* seq0, int* len) {
-  if (b < 0 || b >= p.B || h < 0 || h >= p.H) return false;
-  const long long a = p.cu[b], e = p.cu[b + 1];
-  if (a < 0 || e > p.total || e - a < 0 || e - a > p.max_seqlen) return false;
-  *seq0 = a;
-  *len = static_cast<int>(e - a);
-  return static_cast<long long>(tile) * kAttnQTile < e - a;
-}
-
-// ---------------------------------------------------------------------------
-// bf16 inputs, v_mfma_f32_16x16x32_bf16.
+// ------------------------- bf16 kernel helpers ------------------------------
 //
 // MFMA 16x16x32 operand layout (lane l, g = l / 16, c = l % 16):
 //   A[16 x 32]: lane holds row c, k = 8g .. 8g+7
 //   B[32 x 16]: lane holds column c, k = 8g .. 8g+7
 //   D[16 x 16]: lane holds column c, rows 4g .. 4g+3
-// ---------------------------------------------------------------------------
-constexpr int kKStride = kD + 8;          // bf16 elements per K row in LDS
-constexpr int kVStride = kBlockKeys + 8;  // bf16 elements per V^T row in LDS
+
+struct KVStage {
+  // 16-byte pieces of K and V rows: key = u >> 3, column = u & 7, u = tid + 512 i.
+  uint4 k0, k1, k2, k3;
+  uint4 v0, v1, v2, v3;
+};
+
+template <int I>
+__device__ __forceinline__ uint4& kpiece(KVStage& st) {
+  static_assert(I >= 0 && I < 4, "piece");
+  return I == 0 ? st.k0 : I == 1 ? st.k1 : I == 2 ? st.k2 : st.k3;
+}
+template <int I>
+__device__ __forceinline__ uint4& vpiece(KVStage& st) {
+  static_assert(I >= 0 && I < 4, "piece");
+  return I == 0 ? st.v0 : I == 1 ? st.v1 : I == 2 ? st.v2 : st.v3;
+}
+
+// 16-byte load that yields zeros when `ok` is false (the address is not touched then).
+__device__ __forceinline__ uint4 load16_or_zero(const uint16_t* ptr, bool ok) {
+  uint4 r;
+  if (ok) {
+    r = *reinterpret_cast<const uint4*>(ptr);
+  } else {
+    r.x = 0u;
+    r.y = 0u;
+    r.z = 0u;
+    r.w = 0u;
+  }
+  return r;
+}
+
+template <int I>
+__device__ __forceinline__ void kv_load_piece(const uint16_t* K, const uint16_t* V, long long row0, int nk,
+                                              long long row_elems, int hoff, KVStage& st) {
+  const int u = threadIdx.x + I * kThreads;
+  const int key = u >> 3, dv = u & 7;
+  const long long off = (row0 + key) * row_elems + hoff + dv * 8;
+  kpiece<I>(st) = load16_or_zero(K + off, key < nk);
+  vpiece<I>(st) = load16_or_zero(V + off, key < nk);
+}
+
+__device__ __forceinline__ void kv_load(const uint16_t* K, const uint16_t* V, long long row0, int nk,
+                                        long long row_elems, int hoff, KVStage& st) {
+  kv_load_piece<0>(K, V, row0, nk, row_elems, hoff, st);
+  kv_load_piece<1>(K, V, row0, nk, row_elems, hoff, st);
+  kv_load_piece<2>(K, V, row0, nk, row_elems, hoff, st);
+  kv_load_piece<3>(K, V, row0, nk, row_elems, hoff, st);
+}
+
+template <int I>
+__device__ __forceinline__ void kv_store_piece(KVStage& st, uint16_t* Ks, uint16_t* Vs) {
+  const int u = threadIdx.x + I * kThreads;
+  const int off = (u >> 3) * kKStride + (u & 7) * 8;
+  *reinterpret_cast<uint4*>(&Ks[off]) = kpiece<I>(st);
+  *reinterpret_cast<uint4*>(&Vs[off]) = vpiece<I>(st);
+}
+
+// K and V are both kept row-major ([key][64 dims], padded rows).
+__device__ __forceinline__ void kv_store(KVStage& st, uint16_t* Ks, uint16_t* Vs) {
+  kv_store_piece<0>(st, Ks, Vs);
+  kv_store_piece<1>(st, Ks, Vs);
+  kv_store_piece<2>(st, Ks, Vs);
+  kv_store_piece<3>(st, Ks, Vs);
+}
+
+// Four V values of one dimension for four keys, read with the gfx950
+// transposing LDS load.  In each group of 16 lanes, lane m = 4e + r points at
+// V[row(e)][col0 + 4r .. +3]; lane j then receives V[row(e)][col0 + j] for
+// e = 0..3 (the instruction hands lane j element j % 4 of the addresses of
+// lanes 4e + j / 4).
+__device__ __forceinline__ bf16x4 v_column4(const uint16_t* Vs, int row0, int col0) {
+  const int m = threadIdx.x & 15;
+  const uint16_t* p = &Vs[(row0 + (m >> 2)) * kKStride + col0 + 4 * (m & 3)];
+  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(const_cast<uint16_t*>(p)));
+}
+
+// Query tile j of wave w is 16-query tile (w + 8 j) of the item's chunk, so
+// the busy waves of a short sequence spread over all four SIMDs.
+__device__ __forceinline__ int tile_q0(const Item& it, int wave, int j) {
+  return it.chunk * kAttnQTile + (wave + kWaves * j) * 16;
+}
+
+__device__ __forceinline__ void q_load(const uint16_t* Q, const Item& it, long long row_elems,
+                                       bf16x8 (&qn)[2][2]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int c16 = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int qi = tile_q0(it, wave, j) + c16;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      if (qi < it.len) {
+        qn[j][ks] = *reinterpret_cast<const bf16x8*>(Q + (static_cast<long long>(it.seq0) + qi) * row_elems +
+                                                     it.h * kD + ks * 32 + g * 8);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qn[j][ks][e] = static_cast<__bf16>(0.0f);
+      }
+    }
+  }
+}
+
+// S^T[key][query] for keys kb .. kb+63 of the staged block: 4 key tiles of 16
+// against query tile 0 (and tile 1 when it holds queries).
+__device__ __forceinline__ void qk_block(const uint16_t* Ks, int kb, const bf16x8 (&qf)[2][2], bool act1,
+                                         floatx4 (&s)[2][4]) {
+  const int lane = threadIdx.x & 63;
+  const int c16 = lane & 15, g = lane >> 4;
+  const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt) {
+    const uint16_t* krow = &Ks[(kb + kt * 16 + c16) * kKStride + g * 8];
+    const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(krow);
+    const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(krow + 32);
+    s[0][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+        a1, qf[0][1], __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, qf[0][0], zero, 0, 0, 0), 0, 0, 0);
+    s[1][kt] = act1 ? __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                          a1, qf[1][1], __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, qf[1][0], zero, 0, 0, 0), 0, 0, 0)
+                    : zero;
+  }
+}
+
+struct SoftmaxState {
+  floatx4 o[2][4];  // O^T accumulators: dims dt*16 + 4g .. +3 of the lane's query
+  floatx4 l[2];     // softmax denominators (every component holds the same sum)
+  float m[2];       // running max, log2 units
+};
+
+// Online softmax of one 64-key block followed by O^T += V^T P^T.
+__device__ __forceinline__ void softmax_pv_block(const uint16_t* Vs, int kb, int kvalid, float scale_log2,
+                                                 bool act1, const bf16x8& ones, floatx4 (&s)[2][4],
+                                                 SoftmaxState& st) {
+  const int lane = threadIdx.x & 63;
+  const int c16 = lane & 15, g = lane >> 4;
+  if (kvalid < 64) {  // last, partial block: keys past the end get zero weight
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (kt * 16 + 4 * g + i >= kvalid) s[j][kt][i] = -INFINITY;
+  }
+  float mx[2] = {-INFINITY, -INFINITY};
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    if (j == 1 && !act1) break;
+    float m = -INFINITY;
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) m = fmaxf(m, s[j][kt][i]);
+    m = fmaxf(m, __shfl_xor(m, 16, 64));
+    m = fmaxf(m, __shfl_xor(m, 32, 64));
+    mx[j] = m * scale_log2;
+  }
+  // Lazy rescaling: the running max only moves when a block exceeds it by
+  // more than 2^8, so most blocks skip the rescale and the unnormalised
+  // weights stay below 256.
+  const bool grow = mx[0] > st.m[0] + 8.0f || (act1 && mx[1] > st.m[1] + 8.0f);
+  if (__ballot(grow) != 0ull) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const float m_new = fmaxf(st.m[j], mx[j]);
+      const float alpha = __builtin_amdgcn_exp2f(st.m[j] - m_new);
+      st.m[j] = m_new;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) st.o[j][dt] *= alpha;
+      st.l[j] *= alpha;
+    }
+  }
+  bf16x8 pb[2][2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    if (j == 1 && !act1) {
+      pb[1][0] = ones;  // unused: every MFMA that would read it is skipped
+      pb[1][1] = ones;
+      break;
+    }
+    const float neg_m = -st.m[j];
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) s[j][kt][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[j][kt][i], scale_log2, neg_m));
+    // PV step ks, B operand k = 8g + e <-> key ks*32 + (e < 4 ? 4g + e : 16 + 4g + e - 4).
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        pb[j][ks][e] = static_cast<__bf16>(s[j][2 * ks][e]);
+        pb[j][ks][4 + e] = static_cast<__bf16>(s[j][2 * ks + 1][e]);
+      }
+  }
+  // O^T[dim][query] += V^T[dim][key] P^T[key][query]; a block of ones times
+  // P^T accumulates the denominators (row sums of the bf16 weights).
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+    st.l[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[0][ks], st.l[0], 0, 0, 0);
+    if (act1) st.l[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[1][ks], st.l[1], 0, 0, 0);
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+      // A operand V^T: lane (c16, g) needs dim dt*16 + c16 at keys ks*32 + 4g + 0..3 (lo)
+      // and ks*32 + 16 + 4g + 0..3 (hi), matching the key order of P^T.
+      const bf16x4 lo = v_column4(Vs, kb + ks * 32 + 4 * g, dt * 16);
+      const bf16x4 hi = v_column4(Vs, kb + ks * 32 + 16 + 4 * g, dt * 16);
+      const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      st.o[0][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[0][ks], st.o[0][dt], 0, 0, 0);
+      if (act1) st.o[1][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[1][ks], st.o[1][dt], 0, 0, 0);
+    }
+  }
+}
 
 __global__ __launch_bounds__(kThreads) void attn_fwd_bf16_kernel(AttnParams p) {
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[kBlockKeys * kKStride];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[kD * kVStride];
-  __shared__ int s_ticket;
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[kKRes * kKStride];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[kKRes * kKStride];
+  __shared__ int2 s_raw[2];   // item descriptors handed from thread 0 to the workgroup
+  __shared__ int s_first;
 
   if (!plan_matches(p)) {
     if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(p.status, DORA_DEV_PLAN);
@@ -231,179 +487,156 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16_kernel(AttnParams p) {
   const int wave = tid >> 6;
   const int c16 = lane & 15;
   const int g = lane >> 4;
+  const int G = static_cast<int>(gridDim.x);
   const uint16_t* Q = static_cast<const uint16_t*>(p.q);
   const uint16_t* K = static_cast<const uint16_t*>(p.k);
   const uint16_t* V = static_cast<const uint16_t*>(p.v);
   uint16_t* O = static_cast<uint16_t*>(p.out);
   const long long row_elems = static_cast<long long>(p.H) * kD;
 
+  // Queue.  Tickets 0 .. 3G-1 are dealt statically (workgroup w takes w, w+G
+  // and w+2G, the longest items), the rest come from the atomic counter, so
+  // the start of the kernel is not a burst of atomics on one address.
+  // `cur` computes while the K/V/Q of the next stage load.  Thread 0 alone
+  // talks to the queue: it holds the ticket of the item after `nx` (t_nn),
+  // loads that item's descriptor during the stage and publishes it in LDS at
+  // the end of the stage, so no wave waits on the queue mid-stage.
+  int t_nn = 0;
+  if (tid == 0) {
+    const int t0 = blockIdx.x, t1 = blockIdx.x + G;
+    t_nn = blockIdx.x + 2 * G;
+    s_first = t0;
+    int2 r0, r1;
+    r0.x = -1;
+    r0.y = 0;
+    r1 = r0;
+    if (t0 < n_items) r0 = p.items[t0];
+    if (t1 < n_items) r1 = p.items[t1];
+    s_raw[0] = r0;
+    s_raw[1] = r1;
+  }
+  __syncthreads();
+  if (s_first >= n_items) {
+    leave_queue(p.hdr);
+    return;
+  }
+  Item cur = decode_item(p, s_raw[0]);
+  bool nx_valid = s_raw[1].x != -1;
+  Item nx = nx_valid ? decode_item(p, s_raw[1]) : Item{0, 0, 0, 0};
+  __syncthreads();
+
+  KVStage stage;
+  bf16x8 qn[2][2], qf[2][2];
+  kv_load(K, V, cur.seq0, min(cur.len, kKRes), row_elems, cur.h * kD, stage);
+  q_load(Q, cur, row_elems, qn);
+
+  SoftmaxState sm;
+  bf16x8 ones;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ones[e] = static_cast<__bf16>(1.0f);
+  int sb = 0;
+  bool shift = false;  // the previous stage finished an item
   for (;;) {
-    if (tid == 0) s_ticket = atomicAdd(&p.hdr->counter, 1);
+    __syncthreads();  // every wave is done with the previous stage; s_raw[0] is published
+    kv_store(stage, Ks, Vs);
+    if (shift) {
+      const int2 raw = s_raw[0];
+      const bool nn_valid = raw.x != -1;
+      const Item nn = nn_valid ? decode_item(p, raw) : Item{0, 0, 0, 0};
+      cur = nx;
+      nx = nn;
+      nx_valid = nn_valid;
+      sb = 0;
+    }
     __syncthreads();
-    const int ticket = s_ticket;
-    if (ticket >= n_items) break;
-    const int2 item = p.items[ticket];
-    const int b = item.x, h = item.y >> 16, tile = item.y & 0xFFFF;
-    long long seq0;
-    int len;
-    if (!item_bounds(p, b, h, tile, &seq0, &len)) {
-      if (tid == 0) atomicOr(p.status, DORA_DEV_CU_SEQLENS);
-      __syncthreads();
-      continue;
-    }
-    const int q0 = tile * kAttnQTile + wave * kQPerWave;
-    const bool active = q0 < len;
 
-    // Q^T operands (B side of S^T = K Q^T): lane holds query c16, dims 8g..8g+7 (+32).
-    bf16x8 qf[2][2];
+    const int kb0 = sb * kKRes;
+    const int nk = min(kKRes, cur.len - kb0);
+    const bool act0 = tile_q0(cur, wave, 0) < cur.len;
+    const bool act1 = tile_q0(cur, wave, 1) < cur.len;
+    if (sb == 0) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int qi = q0 + 16 * j + c16;
+      for (int j = 0; j < 2; ++j) {
+        qf[j][0] = qn[j][0];
+        qf[j][1] = qn[j][1];
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        if (qi < len) {
-          qf[j][ks] = *reinterpret_cast<const bf16x8*>(Q + (seq0 + qi) * row_elems + h * kD + ks * 32 + g * 8);
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) qf[j][ks][e] = static_cast<__bf16>(0.0f);
-        }
+        for (int dt = 0; dt < 4; ++dt) sm.o[j][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+        sm.l[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+        sm.m[j] = -INFINITY;
       }
     }
 
-    floatx4 o[2][4];
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt) o[j][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    float m_run[2] = {-INFINITY, -INFINITY};
-    float l_run[2] = {0.f, 0.f};
+    // Next stage: the rest of this item's keys, or the next item.
+    const bool more_keys = kb0 + kKRes < cur.len;
+    const bool have_next = more_keys || nx_valid;
+    const Item kv_item = more_keys ? cur : nx;
+    const int kv_first = more_keys ? kb0 + kKRes : 0;
+    const int kv_n = have_next ? min(kKRes, kv_item.len - kv_first) : 0;
+    const Item q_item = (!more_keys && nx_valid) ? nx : Item{0, 0, 0, 0};
+    kv_load(K, V, static_cast<long long>(kv_item.seq0) + kv_first, kv_n, row_elems, kv_item.h * kD, stage);
+    q_load(Q, q_item, row_elems, qn);
+    // Queue traffic goes out after the prefetch; its results are only
+    // consumed at the end of the stage (no wait in between).
+    int2 raw_next;
+    raw_next.x = -1;
+    raw_next.y = 0;
+    int t_got = 0;
+    if (tid == 0 && !more_keys) {
+      if (t_nn < n_items) raw_next = p.items[t_nn];
+      t_got = atomicAdd(&p.hdr->counter, 1);
+    }
 
-    for (int kb0 = 0; kb0 < len; kb0 += kBlockKeys) {
-      __syncthreads();
-      // Stage K (row-major) and V (transposed) for keys kb0 .. kb0+63.
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int e = tid + u * kThreads;
-        const int key = e >> 3, dv = e & 7;
-        uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-        if (kb0 + key < len) {
-          const long long off = (seq0 + kb0 + key) * row_elems + h * kD + dv * 8;
-          kv = *reinterpret_cast<const uint4*>(K + off);
-          vv = *reinterpret_cast<const uint4*>(V + off);
-        }
-        *reinterpret_cast<uint4*>(&Ks[key * kKStride + dv * 8]) = kv;
-        const uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          Vt[(dv * 8 + 2 * i) * kVStride + key] = static_cast<uint16_t>(w[i] & 0xFFFFu);
-          Vt[(dv * 8 + 2 * i + 1) * kVStride + key] = static_cast<uint16_t>(w[i] >> 16);
-        }
+    if (act0) {
+      // Two key blocks in flight: the MFMAs of block kb+64 are issued before
+      // the softmax of block kb, so the matrix unit and the VALU overlap.
+      floatx4 sa[2][4], sbk[2][4];
+      qk_block(Ks, 0, qf, act1, sa);
+      for (int kb = 0; kb < nk; kb += 128) {
+        if (kb + 64 < nk) qk_block(Ks, kb + 64, qf, act1, sbk);
+        softmax_pv_block(Vs, kb, nk - kb, p.scale_log2, act1, ones, sa, sm);
+        if (kb + 64 >= nk) break;
+        if (kb + 128 < nk) qk_block(Ks, kb + 128, qf, act1, sa);
+        softmax_pv_block(Vs, kb + 64, nk - kb - 64, p.scale_log2, act1, ones, sbk, sm);
       }
-      __syncthreads();
-      if (!active) continue;
-
-      // S^T[key][query] for 4 key tiles of 16 and 2 query tiles of 16.
-      floatx4 s[2][4];
-#pragma unroll
-      for (int kt = 0; kt < 4; ++kt) {
-        const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(&Ks[(kt * 16 + c16) * kKStride + g * 8]);
-        const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(&Ks[(kt * 16 + c16) * kKStride + 32 + g * 8]);
+      if (!more_keys) {
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-          floatx4 acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, qf[j][0], floatx4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-          s[j][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, qf[j][1], acc, 0, 0, 0);
-        }
-      }
-
-      // Online softmax (log2 domain).  Lane holds keys kt*16 + 4g + i of its query.
-      const int kvalid = len - kb0;
-      bf16x8 pb[2][2];
+          const float inv = __builtin_amdgcn_rcpf(sm.l[j][0]);
+          const int qi = tile_q0(cur, wave, j) + c16;
+          if (qi < cur.len) {
+            uint16_t* dst = O + (static_cast<long long>(cur.seq0) + qi) * row_elems + cur.h * kD + 4 * g;
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        float mx = -INFINITY;
+            for (int dt = 0; dt < 4; ++dt) {
+              bf16x4 r;
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int key = kt * 16 + 4 * g + i;
-            const float x = key < kvalid ? s[j][kt][i] * p.scale_log2 : -INFINITY;
-            s[j][kt][i] = x;
-            mx = fmaxf(mx, x);
-          }
-        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        const float m_new = fmaxf(m_run[j], mx);
-        const float alpha = __builtin_amdgcn_exp2f(m_run[j] - m_new);
-        m_run[j] = m_new;
-        float rs = 0.f;
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float pv = __builtin_amdgcn_exp2f(s[j][kt][i] - m_new);
-            s[j][kt][i] = pv;
-            rs += pv;
-          }
-        l_run[j] = l_run[j] * alpha + rs;
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt) o[j][dt] *= alpha;
-        // B operand of the PV step ks: k = 8g + e <-> key ks*32 + (e<4 ? 4g+e : 16+4g+e-4).
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            pb[j][ks][e] = static_cast<__bf16>(s[j][2 * ks][e]);
-            pb[j][ks][4 + e] = static_cast<__bf16>(s[j][2 * ks + 1][e]);
-          }
-      }
-
-      // O^T[dim][query] += V^T[dim][key] P^T[key][query].
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt) {
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-          const uint16_t* vrow = &Vt[(dt * 16 + c16) * kVStride + ks * 32 + 4 * g];
-          const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow);
-          const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 16);
-          const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-#pragma unroll
-          for (int j = 0; j < 2; ++j)
-            o[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[j][ks], o[j][dt], 0, 0, 0);
-        }
-      }
-    }
-
-    if (active) {
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        float l = l_run[j] + __shfl_xor(l_run[j], 16, 64);
-        l += __shfl_xor(l, 32, 64);
-        const float inv = 1.0f / l;
-        const int qi = q0 + 16 * j + c16;
-        if (qi < len) {
-          uint16_t* dst = O + (seq0 + qi) * row_elems + h * kD + 4 * g;
-#pragma unroll
-          for (int dt = 0; dt < 4; ++dt) {
-            bf16x4 r;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) r[i] = static_cast<__bf16>(o[j][dt][i] * inv);
-            *reinterpret_cast<bf16x4*>(dst + dt * 16) = r;
+              for (int i = 0; i < 4; ++i) r[i] = static_cast<__bf16>(sm.o[j][dt][i] * inv);
+              *reinterpret_cast<bf16x4*>(dst + dt * 16) = r;
+            }
           }
         }
       }
     }
-    __syncthreads();
+
+    if (tid == 0 && !more_keys) {
+      s_raw[0] = raw_next;
+      t_nn = t_got + 3 * G;
+    }
+    shift = !more_keys;
+    if (!have_next) break;
+    if (more_keys) ++sb;
   }
   leave_queue(p.hdr);
 }
 
 // ---------------------------------------------------------------------------
 // fp32 inputs, v_mfma_f32_16x16x4_f32 (true fp32 products, fp32 accumulate).
+// Same items; K/V streamed through LDS in blocks of 64 keys.
 //
 // MFMA 16x16x4 f32 operand layout (lane l, g = l / 16, c = l % 16):
 //   A[16 x 4]: lane holds row c, k = g;  B[4 x 16]: lane holds column c, k = g
 //   D[16 x 16]: lane holds column c, rows 4g .. 4g+3
 // ---------------------------------------------------------------------------
+constexpr int kBlockKeys = 64;
 constexpr int kFStride = kD + 4;  // floats per K / V row in LDS
 
 __global__ __launch_bounds__(kThreads) void attn_fwd_f32_kernel(AttnParams p) {
@@ -431,17 +664,12 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_f32_kernel(AttnParams p) {
     if (tid == 0) s_ticket = atomicAdd(&p.hdr->counter, 1);
     __syncthreads();
     const int ticket = s_ticket;
+    __syncthreads();
     if (ticket >= n_items) break;
-    const int2 item = p.items[ticket];
-    const int b = item.x, h = item.y >> 16, tile = item.y & 0xFFFF;
-    long long seq0;
-    int len;
-    if (!item_bounds(p, b, h, tile, &seq0, &len)) {
-      if (tid == 0) atomicOr(p.status, DORA_DEV_CU_SEQLENS);
-      __syncthreads();
-      continue;
-    }
-    const int q0 = tile * kAttnQTile + wave * kQPerWave;
+    const Item it = decode_item(p, p.items[ticket]);
+    const long long seq0 = it.seq0;
+    const int len = it.len;
+    const int q0 = it.chunk * kAttnQTile + wave * kQPerWave;
     const bool active = q0 < len;
 
     float qf[2][16];
@@ -450,7 +678,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_f32_kernel(AttnParams p) {
       const int qi = q0 + 16 * j + c16;
 #pragma unroll
       for (int ks = 0; ks < 16; ++ks)
-        qf[j][ks] = qi < len ? Q[(seq0 + qi) * row_elems + h * kD + 4 * ks + g] : 0.f;
+        qf[j][ks] = qi < len ? Q[(seq0 + qi) * row_elems + it.h * kD + 4 * ks + g] : 0.f;
     }
     floatx4 o[2][4];
 #pragma unroll
@@ -463,12 +691,12 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_f32_kernel(AttnParams p) {
     for (int kb0 = 0; kb0 < len; kb0 += kBlockKeys) {
       __syncthreads();
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < 2; ++u) {
         const int e = tid + u * kThreads;  // 64 keys x 16 float4
         const int key = e >> 4, dv = e & 15;
         float4 kv = make_float4(0.f, 0.f, 0.f, 0.f), vv = kv;
         if (kb0 + key < len) {
-          const long long off = (seq0 + kb0 + key) * row_elems + h * kD + dv * 4;
+          const long long off = (seq0 + kb0 + key) * row_elems + it.h * kD + dv * 4;
           kv = *reinterpret_cast<const float4*>(K + off);
           vv = *reinterpret_cast<const float4*>(V + off);
         }
@@ -546,7 +774,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_f32_kernel(AttnParams p) {
         const float inv = 1.0f / l;
         const int qi = q0 + 16 * j + c16;
         if (qi < len) {
-          float* dst = O + (seq0 + qi) * row_elems + h * kD + 4 * g;
+          float* dst = O + (seq0 + qi) * row_elems + it.h * kD + 4 * g;
 #pragma unroll
           for (int dt = 0; dt < 4; ++dt)
             *reinterpret_cast<float4*>(dst + dt * 16) =
@@ -554,7 +782,6 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_f32_kernel(AttnParams p) {
         }
       }
     }
-    __syncthreads();
   }
   leave_queue(p.hdr);
 }
@@ -578,23 +805,12 @@ int persistent_grid(KernelT kernel, int slot, int* grid) {
 }
 
 int check_attn_sizes(int32_t B, int32_t H, int32_t max_seqlen, int64_t total) {
-  if (B < 1 || H < 1 || H > 256 || max_seqlen < 1 || max_seqlen > DORA_MAX_SEQLEN || total < 0 ||
-      total > INT_MAX)
+  if (B < 1 || B > kPlanMaxB || H < 1 || H > 256 || max_seqlen < 1 || max_seqlen > DORA_MAX_SEQLEN ||
+      total < 0 || total > INT_MAX)
     return DORA_ERR_SHAPE;
   const AttnWorkspaceLayout L = attn_workspace_layout(B, H, max_seqlen);
   if (L.max_items > INT_MAX) return DORA_ERR_UNSUPPORTED;
   return DORA_OK;
-}
-
-void fill_views(void* workspace, int32_t B, int32_t H, int32_t max_seqlen, AttnPlanHeader** hdr,
-                int32_t** order, int32_t** base, int2** items, int64_t* max_items) {
-  const AttnWorkspaceLayout L = attn_workspace_layout(B, H, max_seqlen);
-  char* w = static_cast<char*>(workspace);
-  *hdr = reinterpret_cast<AttnPlanHeader*>(w);
-  *order = reinterpret_cast<int32_t*>(w + L.order_off);
-  *base = reinterpret_cast<int32_t*>(w + L.base_off);
-  *items = reinterpret_cast<int2*>(w + L.items_off);
-  *max_items = L.max_items;
 }
 
 }  // namespace
@@ -627,8 +843,8 @@ extern "C" int dora_varlen_attn_plan(const int32_t* cu_seqlens, int32_t B, int32
   if (!cu_seqlens || !dev_status) return DORA_ERR_NULL;
   const int sz = check_attn_sizes(B, H, max_seqlen, total);
   if (sz != DORA_OK) return sz;
-  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) ||
-      workspace_bytes < attn_workspace_layout(B, H, max_seqlen).bytes)
+  const AttnWorkspaceLayout L = attn_workspace_layout(B, H, max_seqlen);
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) || workspace_bytes < L.bytes)
     return DORA_ERR_WORKSPACE;
   PlanParams p;
   p.cu = cu_seqlens;
@@ -637,7 +853,8 @@ extern "C" int dora_varlen_attn_plan(const int32_t* cu_seqlens, int32_t B, int32
   p.max_seqlen = max_seqlen;
   p.total = total;
   p.status = dev_status;
-  fill_views(workspace, B, H, max_seqlen, &p.hdr, &p.order, &p.item_base, &p.items, &p.max_items);
+  p.hdr = static_cast<AttnPlanHeader*>(workspace);
+  p.items = reinterpret_cast<int2*>(static_cast<char*>(workspace) + L.items_off);
   hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(kPlanThreads), 0, static_cast<hipStream_t>(stream), p);
   return hipGetLastError() == hipSuccess ? DORA_OK : DORA_ERR_HIP;
 }
@@ -656,8 +873,8 @@ extern "C" int dora_varlen_attn_execute(const void* q, const void* k, const void
   if ((reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(k) | reinterpret_cast<uintptr_t>(v) |
        reinterpret_cast<uintptr_t>(out)) & 15u)
     return DORA_ERR_ALIGN;
-  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) ||
-      workspace_bytes < attn_workspace_layout(B, H, max_seqlen).bytes)
+  const AttnWorkspaceLayout L = attn_workspace_layout(B, H, max_seqlen);
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) || workspace_bytes < L.bytes)
     return DORA_ERR_WORKSPACE;
   if (!(softmax_scale > 0.0f)) softmax_scale = 1.0f / sqrtf(static_cast<float>(D));
 
@@ -666,20 +883,15 @@ extern "C" int dora_varlen_attn_execute(const void* q, const void* k, const void
   p.k = k;
   p.v = v;
   p.out = out;
-  p.cu = cu_seqlens;
   p.B = B;
   p.H = H;
   p.max_seqlen = max_seqlen;
   p.total = total;
   p.scale_log2 = softmax_scale * kLog2e;
+  p.hdr = static_cast<AttnPlanHeader*>(workspace);
+  p.items = reinterpret_cast<const int2*>(static_cast<char*>(workspace) + L.items_off);
+  p.max_items = static_cast<int32_t>(L.max_items);
   p.status = dev_status;
-  int32_t* order;
-  int32_t* base;
-  int2* items;
-  int64_t max_items;
-  fill_views(workspace, B, H, max_seqlen, &p.hdr, &order, &base, &items, &max_items);
-  p.items = items;
-  p.max_items = static_cast<int32_t>(max_items);
 
   int grid = 0;
   const int rc = dtype == DORA_BF16 ? persistent_grid(attn_fwd_bf16_kernel, 0, &grid)
