@@ -239,6 +239,12 @@ __device__ __forceinline__ Item decode_item(const AttnParams& p, int2 raw) {
   return it;
 }
 
+// An item descriptor read from LDS is the same in every lane; say so, so the
+// item's fields and the branches on them stay scalar.
+__device__ __forceinline__ int2 uniform_raw(int2 r) {
+  return make_int2(__builtin_amdgcn_readfirstlane(r.x), __builtin_amdgcn_readfirstlane(r.y));
+}
+
 __device__ __forceinline__ void leave_queue(AttnPlanHeader* hdr) {
   // The last workgroup out resets the counters for the next execute.
   if (threadIdx.x == 0) {
@@ -264,63 +270,54 @@ struct KVStage {
   uint4 v0, v1, v2, v3;
 };
 
-template <int I>
-__device__ __forceinline__ uint4& kpiece(KVStage& st) {
-  static_assert(I >= 0 && I < 4, "piece");
-  return I == 0 ? st.k0 : I == 1 ? st.k1 : I == 2 ? st.k2 : st.k3;
-}
-template <int I>
-__device__ __forceinline__ uint4& vpiece(KVStage& st) {
-  static_assert(I >= 0 && I < 4, "piece");
-  return I == 0 ? st.v0 : I == 1 ? st.v1 : I == 2 ? st.v2 : st.v3;
+// Byte address of element (row0, head h, dim 0) of a packed [rows, H, 64]
+// tensor.  Every argument is the same in all lanes, so this is scalar
+// arithmetic and per-lane offsets can stay 32-bit.
+__device__ __forceinline__ const char* head_base(const void* X, long long row0, long long row_elems, int h) {
+  return static_cast<const char*>(X) + (row0 * row_elems + h * kD) * 2;
 }
 
-// 16-byte load that yields zeros when `ok` is false (the address is not touched then).
-__device__ __forceinline__ uint4 load16_or_zero(const uint16_t* ptr, bool ok) {
-  uint4 r;
-  if (ok) {
-    r = *reinterpret_cast<const uint4*>(ptr);
-  } else {
-    r.x = 0u;
-    r.y = 0u;
-    r.z = 0u;
-    r.w = 0u;
-  }
-  return r;
+// Byte offset of this thread's piece i of a stage, its row clamped to `last`.
+__device__ __forceinline__ uint32_t kv_piece_offset(int i, uint32_t last, uint32_t row_bytes) {
+  const uint32_t key = min((threadIdx.x >> 3) + i * (kThreads / 8), last);
+  return key * row_bytes + (threadIdx.x & 7) * 16;
 }
 
-template <int I>
-__device__ __forceinline__ void kv_load_piece(const uint16_t* K, const uint16_t* V, long long row0, int nk,
-                                              long long row_elems, int hoff, KVStage& st) {
-  const int u = threadIdx.x + I * kThreads;
-  const int key = u >> 3, dv = u & 7;
-  const long long off = (row0 + key) * row_elems + hoff + dv * 8;
-  kpiece<I>(st) = load16_or_zero(K + off, key < nk);
-  vpiece<I>(st) = load16_or_zero(V + off, key < nk);
+__device__ __forceinline__ uint4 load16(const char* base, uint32_t off) {
+  return *reinterpret_cast<const uint4*>(base + off);
 }
 
-__device__ __forceinline__ void kv_load(const uint16_t* K, const uint16_t* V, long long row0, int nk,
-                                        long long row_elems, int hoff, KVStage& st) {
-  kv_load_piece<0>(K, V, row0, nk, row_elems, hoff, st);
-  kv_load_piece<1>(K, V, row0, nk, row_elems, hoff, st);
-  kv_load_piece<2>(K, V, row0, nk, row_elems, hoff, st);
-  kv_load_piece<3>(K, V, row0, nk, row_elems, hoff, st);
-}
-
-template <int I>
-__device__ __forceinline__ void kv_store_piece(KVStage& st, uint16_t* Ks, uint16_t* Vs) {
-  const int u = threadIdx.x + I * kThreads;
-  const int off = (u >> 3) * kKStride + (u & 7) * 8;
-  *reinterpret_cast<uint4*>(&Ks[off]) = kpiece<I>(st);
-  *reinterpret_cast<uint4*>(&Vs[off]) = vpiece<I>(st);
+// Rows [0, nk) of one stage, nk >= 1.  Lanes whose row is past the end read
+// row nk-1 again, so every load is in bounds and nothing needs zeroing: those
+// keys only reach a block's masked tail, and the copied V rows are finite.
+__device__ __forceinline__ KVStage kv_load(const char* kbase, const char* vbase, int nk, uint32_t row_bytes) {
+  const uint32_t last = static_cast<uint32_t>(nk - 1);
+  const uint32_t o0 = kv_piece_offset(0, last, row_bytes), o1 = kv_piece_offset(1, last, row_bytes);
+  const uint32_t o2 = kv_piece_offset(2, last, row_bytes), o3 = kv_piece_offset(3, last, row_bytes);
+  KVStage st;
+  st.k0 = load16(kbase, o0);
+  st.v0 = load16(vbase, o0);
+  st.k1 = load16(kbase, o1);
+  st.v1 = load16(vbase, o1);
+  st.k2 = load16(kbase, o2);
+  st.v2 = load16(vbase, o2);
+  st.k3 = load16(kbase, o3);
+  st.v3 = load16(vbase, o3);
+  return st;
 }
 
 // K and V are both kept row-major ([key][64 dims], padded rows).
-__device__ __forceinline__ void kv_store(KVStage& st, uint16_t* Ks, uint16_t* Vs) {
-  kv_store_piece<0>(st, Ks, Vs);
-  kv_store_piece<1>(st, Ks, Vs);
-  kv_store_piece<2>(st, Ks, Vs);
-  kv_store_piece<3>(st, Ks, Vs);
+__device__ __forceinline__ void kv_store(const KVStage& st, uint16_t* Ks, uint16_t* Vs) {
+  const int off = (threadIdx.x >> 3) * kKStride + (threadIdx.x & 7) * 8;
+  constexpr int kStep = (kThreads / 8) * kKStride;  // 64 rows
+  *reinterpret_cast<uint4*>(&Ks[off]) = st.k0;
+  *reinterpret_cast<uint4*>(&Vs[off]) = st.v0;
+  *reinterpret_cast<uint4*>(&Ks[off + kStep]) = st.k1;
+  *reinterpret_cast<uint4*>(&Vs[off + kStep]) = st.v1;
+  *reinterpret_cast<uint4*>(&Ks[off + 2 * kStep]) = st.k2;
+  *reinterpret_cast<uint4*>(&Vs[off + 2 * kStep]) = st.v2;
+  *reinterpret_cast<uint4*>(&Ks[off + 3 * kStep]) = st.k3;
+  *reinterpret_cast<uint4*>(&Vs[off + 3 * kStep]) = st.v3;
 }
 
 // Four V values of one dimension for four keys, read with the gfx950
@@ -337,33 +334,45 @@ __device__ __forceinline__ bf16x4 v_column4(const uint16_t* Vs, int row0, int co
 
 // Query tile j of wave w is 16-query tile (w + 8 j) of the item's chunk, so
 // the busy waves of a short sequence spread over all four SIMDs.
-__device__ __forceinline__ int tile_q0(const Item& it, int wave, int j) {
-  return it.chunk * kAttnQTile + (wave + kWaves * j) * 16;
-}
+__device__ __forceinline__ int tile_q(int wave, int j) { return (wave + kWaves * j) * 16; }
 
-__device__ __forceinline__ void q_load(const uint16_t* Q, const Item& it, long long row_elems,
-                                       bf16x8 (&qn)[2][2]) {
+// Queries of one chunk (qbase = its first row, nq >= 1 of them).  Lanes past
+// the end re-read the last query; their scores are computed and never stored.
+__device__ __forceinline__ void q_load(const char* qbase, int nq, uint32_t row_bytes, bf16x8 (&qn)[2][2]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int c16 = lane & 15, g = lane >> 4;
+  const uint32_t last = static_cast<uint32_t>(nq - 1);
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
-    const int qi = tile_q0(it, wave, j) + c16;
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      if (qi < it.len) {
-        qn[j][ks] = *reinterpret_cast<const bf16x8*>(Q + (static_cast<long long>(it.seq0) + qi) * row_elems +
-                                                     it.h * kD + ks * 32 + g * 8);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) qn[j][ks][e] = static_cast<__bf16>(0.0f);
-      }
-    }
+    const uint32_t qi = min(static_cast<uint32_t>(tile_q(wave, j) + (lane & 15)), last);
+    const char* row = qbase + qi * row_bytes + (lane >> 4) * 16;
+    qn[j][0] = *reinterpret_cast<const bf16x8*>(row);
+    qn[j][1] = *reinterpret_cast<const bf16x8*>(row + 64);
   }
 }
 
+// K/V rows [first, first + n) of an item's head into the staging registers;
+// with n == 0 it re-reads row 0 of head 0 (harmless, never stored).
+__device__ __forceinline__ KVStage kv_stage_load(const AttnParams& p, const Item& it, int first, int n,
+                                                 long long row_elems, uint32_t row_bytes) {
+  const long long row0 = n > 0 ? static_cast<long long>(it.seq0) + first : 0;
+  const int h = n > 0 ? it.h : 0;
+  return kv_load(head_base(p.k, row0, row_elems, h), head_base(p.v, row0, row_elems, h), max(n, 1), row_bytes);
+}
+
+// The queries of an item's chunk; an empty item re-reads row 0 of head 0.
+__device__ __forceinline__ void q_chunk_load(const AttnParams& p, const Item& it, long long row_elems,
+                                             uint32_t row_bytes, bf16x8 (&qn)[2][2]) {
+  const int q0 = it.chunk * kAttnQTile;
+  const int nq = min(kAttnQTile, it.len - q0);
+  const long long row0 = nq > 0 ? static_cast<long long>(it.seq0) + q0 : 0;
+  const int h = nq > 0 ? it.h : 0;
+  q_load(head_base(p.q, row0, row_elems, h), max(nq, 1), row_bytes, qn);
+}
+
 // S^T[key][query] for keys kb .. kb+63 of the staged block: 4 key tiles of 16
-// against query tile 0 (and tile 1 when it holds queries).
-__device__ __forceinline__ void qk_block(const uint16_t* Ks, int kb, const bf16x8 (&qf)[2][2], bool act1,
+// against query tile 0 (and tile 1 when ACT1).
+template <bool ACT1>
+__device__ __forceinline__ void qk_block(const uint16_t* Ks, int kb, const bf16x8 (&qf)[2][2],
                                          floatx4 (&s)[2][4]) {
   const int lane = threadIdx.x & 63;
   const int c16 = lane & 15, g = lane >> 4;
@@ -375,9 +384,9 @@ __device__ __forceinline__ void qk_block(const uint16_t* Ks, int kb, const bf16x
     const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(krow + 32);
     s[0][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
         a1, qf[0][1], __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, qf[0][0], zero, 0, 0, 0), 0, 0, 0);
-    s[1][kt] = act1 ? __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                          a1, qf[1][1], __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, qf[1][0], zero, 0, 0, 0), 0, 0, 0)
-                    : zero;
+    if (ACT1)
+      s[1][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+          a1, qf[1][1], __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, qf[1][0], zero, 0, 0, 0), 0, 0, 0);
   }
 }
 
@@ -387,57 +396,65 @@ struct SoftmaxState {
   float m[2];       // running max, log2 units
 };
 
-// Online softmax of one 64-key block followed by O^T += V^T P^T.
+// Online softmax of one 64-key block followed by O^T += V^T P^T.  FIRST marks
+// an item's first block: the running max starts at the block max and the
+// accumulators start from zero.
+template <bool ACT1, bool FIRST>
 __device__ __forceinline__ void softmax_pv_block(const uint16_t* Vs, int kb, int kvalid, float scale_log2,
-                                                 bool act1, const bf16x8& ones, floatx4 (&s)[2][4],
-                                                 SoftmaxState& st) {
+                                                 const bf16x8& ones, floatx4 (&s)[2][4], SoftmaxState& st) {
+  constexpr int kTiles = ACT1 ? 2 : 1;
   const int lane = threadIdx.x & 63;
-  const int c16 = lane & 15, g = lane >> 4;
+  const int g = lane >> 4;
   if (kvalid < 64) {  // last, partial block: keys past the end get zero weight
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (kt * 16 + 4 * g + i >= kvalid) s[j][kt][i] = -INFINITY;
-  }
-  float mx[2] = {-INFINITY, -INFINITY};
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    if (j == 1 && !act1) break;
-    float m = -INFINITY;
+    const int lim = kvalid - 4 * g;
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) m = fmaxf(m, s[j][kt][i]);
+      for (int i = 0; i < 4; ++i) {
+        const bool dead = kt * 16 + i >= lim;
+#pragma unroll
+        for (int j = 0; j < kTiles; ++j) s[j][kt][i] = dead ? -INFINITY : s[j][kt][i];
+      }
+  }
+  float mx[2];
+#pragma unroll
+  for (int j = 0; j < kTiles; ++j) {
+    float m = fmaxf(fmaxf(s[j][0][0], s[j][0][1]), s[j][0][2]);
+    m = fmaxf(fmaxf(m, s[j][0][3]), s[j][1][0]);
+#pragma unroll
+    for (int kt = 1; kt < 4; ++kt) {
+      const int i0 = kt == 1 ? 1 : 0;
+#pragma unroll
+      for (int i = i0; i < 4; ++i) m = fmaxf(m, s[j][kt][i]);
+    }
     m = fmaxf(m, __shfl_xor(m, 16, 64));
     m = fmaxf(m, __shfl_xor(m, 32, 64));
     mx[j] = m * scale_log2;
   }
-  // Lazy rescaling: the running max only moves when a block exceeds it by
-  // more than 2^8, so most blocks skip the rescale and the unnormalised
-  // weights stay below 256.
-  const bool grow = mx[0] > st.m[0] + 8.0f || (act1 && mx[1] > st.m[1] + 8.0f);
-  if (__ballot(grow) != 0ull) {
+  if (FIRST) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const float m_new = fmaxf(st.m[j], mx[j]);
-      const float alpha = __builtin_amdgcn_exp2f(st.m[j] - m_new);
-      st.m[j] = m_new;
+    for (int j = 0; j < kTiles; ++j) st.m[j] = mx[j];
+  } else {
+    // Lazy rescaling: the running max only moves when a block exceeds it by
+    // more than 2^8, so most blocks skip the rescale and the unnormalised
+    // weights stay below 256.
+    bool grow = mx[0] > st.m[0] + 8.0f;
+    if (ACT1) grow = grow || mx[1] > st.m[1] + 8.0f;
+    if (__ballot(grow) != 0ull) {
 #pragma unroll
-      for (int dt = 0; dt < 4; ++dt) st.o[j][dt] *= alpha;
-      st.l[j] *= alpha;
+      for (int j = 0; j < kTiles; ++j) {
+        const float m_new = fmaxf(st.m[j], mx[j]);
+        const float alpha = __builtin_amdgcn_exp2f(st.m[j] - m_new);
+        st.m[j] = m_new;
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt) st.o[j][dt] *= alpha;
+        st.l[j] *= alpha;
+      }
     }
   }
   bf16x8 pb[2][2];
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    if (j == 1 && !act1) {
-      pb[1][0] = ones;  // unused: every MFMA that would read it is skipped
-      pb[1][1] = ones;
-      break;
-    }
+  for (int j = 0; j < kTiles; ++j) {
     const float neg_m = -st.m[j];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
@@ -454,10 +471,13 @@ __device__ __forceinline__ void softmax_pv_block(const uint16_t* Vs, int kb, int
   }
   // O^T[dim][query] += V^T[dim][key] P^T[key][query]; a block of ones times
   // P^T accumulates the denominators (row sums of the bf16 weights).
+  const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) {
-    st.l[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[0][ks], st.l[0], 0, 0, 0);
-    if (act1) st.l[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[1][ks], st.l[1], 0, 0, 0);
+    const bool init = FIRST && ks == 0;
+#pragma unroll
+    for (int j = 0; j < kTiles; ++j)
+      st.l[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[j][ks], init ? zero : st.l[j], 0, 0, 0);
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) {
       // A operand V^T: lane (c16, g) needs dim dt*16 + c16 at keys ks*32 + 4g + 0..3 (lo)
@@ -465,8 +485,51 @@ __device__ __forceinline__ void softmax_pv_block(const uint16_t* Vs, int kb, int
       const bf16x4 lo = v_column4(Vs, kb + ks * 32 + 4 * g, dt * 16);
       const bf16x4 hi = v_column4(Vs, kb + ks * 32 + 16 + 4 * g, dt * 16);
       const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-      st.o[0][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[0][ks], st.o[0][dt], 0, 0, 0);
-      if (act1) st.o[1][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[1][ks], st.o[1][dt], 0, 0, 0);
+#pragma unroll
+      for (int j = 0; j < kTiles; ++j)
+        st.o[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[j][ks], init ? zero : st.o[j][dt], 0, 0, 0);
+    }
+  }
+}
+
+// All key blocks of one stage (nk >= 1 keys in LDS).  Two key blocks are in
+// flight: the MFMAs of block kb+64 are issued before the softmax of block kb,
+// so the matrix unit and the VALU overlap.
+template <bool ACT1>
+__device__ __forceinline__ void attend_stage(const uint16_t* Ks, const uint16_t* Vs, int nk, bool first,
+                                             float scale_log2, const bf16x8& ones, const bf16x8 (&qf)[2][2],
+                                             SoftmaxState& sm) {
+  floatx4 sa[2][4], sbk[2][4];
+  qk_block<ACT1>(Ks, 0, qf, sa);
+  if (nk > 64) qk_block<ACT1>(Ks, 64, qf, sbk);
+  if (first) softmax_pv_block<ACT1, true>(Vs, 0, nk, scale_log2, ones, sa, sm);
+  else softmax_pv_block<ACT1, false>(Vs, 0, nk, scale_log2, ones, sa, sm);
+  for (int kb = 64; kb < nk; kb += 128) {
+    if (kb + 64 < nk) qk_block<ACT1>(Ks, kb + 64, qf, sa);
+    softmax_pv_block<ACT1, false>(Vs, kb, nk - kb, scale_log2, ones, sbk, sm);
+    if (kb + 64 >= nk) break;
+    if (kb + 128 < nk) qk_block<ACT1>(Ks, kb + 128, qf, sbk);
+    softmax_pv_block<ACT1, false>(Vs, kb + 64, nk - kb - 64, scale_log2, ones, sa, sm);
+  }
+}
+
+// O = O^T / l for the wave's active query tiles (obase = first row of the chunk).
+template <bool ACT1>
+__device__ __forceinline__ void store_out(char* obase, int nq, uint32_t row_bytes, const SoftmaxState& sm) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int j = 0; j < (ACT1 ? 2 : 1); ++j) {
+    const float inv = __builtin_amdgcn_rcpf(sm.l[j][0]);
+    const int qi = tile_q(wave, j) + (lane & 15);
+    if (qi < nq) {
+      char* dst = obase + static_cast<uint32_t>(qi) * row_bytes + (lane >> 4) * 8;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+        bf16x4 r;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) r[i] = static_cast<__bf16>(sm.o[j][dt][i] * inv);
+        *reinterpret_cast<bf16x4*>(dst + dt * 32) = r;
+      }
     }
   }
 }
@@ -483,16 +546,10 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16_kernel(AttnParams p) {
   }
   const int n_items = min(p.hdr->n_items, p.max_items);
   const int tid = threadIdx.x;
-  const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int c16 = lane & 15;
-  const int g = lane >> 4;
   const int G = static_cast<int>(gridDim.x);
-  const uint16_t* Q = static_cast<const uint16_t*>(p.q);
-  const uint16_t* K = static_cast<const uint16_t*>(p.k);
-  const uint16_t* V = static_cast<const uint16_t*>(p.v);
-  uint16_t* O = static_cast<uint16_t*>(p.out);
   const long long row_elems = static_cast<long long>(p.H) * kD;
+  const uint32_t row_bytes = static_cast<uint32_t>(row_elems) * 2u;
 
   // Queue.  Tickets 0 .. 3G-1 are dealt statically (workgroup w takes w, w+G
   // and w+2G, the longest items), the rest come from the atomic counter, so
@@ -520,15 +577,18 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16_kernel(AttnParams p) {
     leave_queue(p.hdr);
     return;
   }
-  Item cur = decode_item(p, s_raw[0]);
-  bool nx_valid = s_raw[1].x != -1;
-  Item nx = nx_valid ? decode_item(p, s_raw[1]) : Item{0, 0, 0, 0};
+  Item cur = decode_item(p, uniform_raw(s_raw[0]));
+  const int2 raw1 = uniform_raw(s_raw[1]);
+  bool nx_valid = raw1.x != -1;
+  Item nx = nx_valid ? decode_item(p, raw1) : Item{0, 0, 0, 0};
   __syncthreads();
 
-  KVStage stage;
   bf16x8 qn[2][2], qf[2][2];
-  kv_load(K, V, cur.seq0, min(cur.len, kKRes), row_elems, cur.h * kD, stage);
-  q_load(Q, cur, row_elems, qn);
+  // Loads are issued unconditionally (a stage with nothing to load re-reads
+  // row 0, which exists whenever there is an item), so the staging registers
+  // are never live across a branch.
+  KVStage stage = kv_stage_load(p, cur, 0, min(cur.len, kKRes), row_elems, row_bytes);
+  q_chunk_load(p, cur, row_elems, row_bytes, qn);
 
   SoftmaxState sm;
   bf16x8 ones;
@@ -540,7 +600,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16_kernel(AttnParams p) {
     __syncthreads();  // every wave is done with the previous stage; s_raw[0] is published
     kv_store(stage, Ks, Vs);
     if (shift) {
-      const int2 raw = s_raw[0];
+      const int2 raw = uniform_raw(s_raw[0]);
       const bool nn_valid = raw.x != -1;
       const Item nn = nn_valid ? decode_item(p, raw) : Item{0, 0, 0, 0};
       cur = nx;
@@ -552,29 +612,28 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16_kernel(AttnParams p) {
 
     const int kb0 = sb * kKRes;
     const int nk = min(kKRes, cur.len - kb0);
-    const bool act0 = tile_q0(cur, wave, 0) < cur.len;
-    const bool act1 = tile_q0(cur, wave, 1) < cur.len;
+    const int q0 = cur.chunk * kAttnQTile;
+    const int nq = min(kAttnQTile, cur.len - q0);
+    const bool act0 = tile_q(wave, 0) < nq;
+    const bool act1 = tile_q(wave, 1) < nq;
     if (sb == 0) {
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         qf[j][0] = qn[j][0];
         qf[j][1] = qn[j][1];
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt) sm.o[j][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
-        sm.l[j] = floatx4{0.f, 0.f, 0.f, 0.f};
-        sm.m[j] = -INFINITY;
       }
     }
 
     // Next stage: the rest of this item's keys, or the next item.
     const bool more_keys = kb0 + kKRes < cur.len;
     const bool have_next = more_keys || nx_valid;
-    const Item kv_item = more_keys ? cur : nx;
-    const int kv_first = more_keys ? kb0 + kKRes : 0;
-    const int kv_n = have_next ? min(kKRes, kv_item.len - kv_first) : 0;
-    const Item q_item = (!more_keys && nx_valid) ? nx : Item{0, 0, 0, 0};
-    kv_load(K, V, static_cast<long long>(kv_item.seq0) + kv_first, kv_n, row_elems, kv_item.h * kD, stage);
-    q_load(Q, q_item, row_elems, qn);
+    {
+      const Item kv_item = more_keys ? cur : nx;
+      const int kv_first = more_keys ? kb0 + kKRes : 0;
+      const int kv_n = have_next ? min(kKRes, kv_item.len - kv_first) : 0;
+      stage = kv_stage_load(p, kv_item, kv_first, kv_n, row_elems, row_bytes);
+      if (!more_keys) q_chunk_load(p, nx_valid ? nx : Item{0, 0, 0, 0}, row_elems, row_bytes, qn);
+    }
     // Queue traffic goes out after the prefetch; its results are only
     // consumed at the end of the stage (no wait in between).
     int2 raw_next;
@@ -587,33 +646,13 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16_kernel(AttnParams p) {
     }
 
     if (act0) {
-      // Two key blocks in flight: the MFMAs of block kb+64 are issued before
-      // the softmax of block kb, so the matrix unit and the VALU overlap.
-      floatx4 sa[2][4], sbk[2][4];
-      qk_block(Ks, 0, qf, act1, sa);
-      for (int kb = 0; kb < nk; kb += 128) {
-        if (kb + 64 < nk) qk_block(Ks, kb + 64, qf, act1, sbk);
-        softmax_pv_block(Vs, kb, nk - kb, p.scale_log2, act1, ones, sa, sm);
-        if (kb + 64 >= nk) break;
-        if (kb + 128 < nk) qk_block(Ks, kb + 128, qf, act1, sa);
-        softmax_pv_block(Vs, kb + 64, nk - kb - 64, p.scale_log2, act1, ones, sbk, sm);
-      }
-      if (!more_keys) {
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const float inv = __builtin_amdgcn_rcpf(sm.l[j][0]);
-          const int qi = tile_q0(cur, wave, j) + c16;
-          if (qi < cur.len) {
-            uint16_t* dst = O + (static_cast<long long>(cur.seq0) + qi) * row_elems + cur.h * kD + 4 * g;
-#pragma unroll
-            for (int dt = 0; dt < 4; ++dt) {
-              bf16x4 r;
-#pragma unroll
-              for (int i = 0; i < 4; ++i) r[i] = static_cast<__bf16>(sm.o[j][dt][i] * inv);
-              *reinterpret_cast<bf16x4*>(dst + dt * 16) = r;
-            }
-          }
-        }
+      char* obase = const_cast<char*>(head_base(p.out, static_cast<long long>(cur.seq0) + q0, row_elems, cur.h));
+      if (act1) {
+        attend_stage<true>(Ks, Vs, nk, sb == 0, p.scale_log2, ones, qf, sm);
+        if (!more_keys) store_out<true>(obase, nq, row_bytes, sm);
+      } else {
+        attend_stage<false>(Ks, Vs, nk, sb == 0, p.scale_log2, ones, qf, sm);
+        if (!more_keys) store_out<false>(obase, nq, row_bytes, sm);
       }
     }
 
