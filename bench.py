@@ -46,6 +46,106 @@ def attn_bytes(w: W.Workload, keep: np.ndarray) -> int:
     return 4 * int(keep.sum()) * w.H * W.HEAD_DIM * w.elt   # Q, K, V read once, O written once
 
 
+KERNEL_SOURCES = {"attn": "paper_2609_34325_amd/csrc/varlen_attn.hip",
+                  "select_pack": "paper_2609_34325_amd/csrc/select_pack.hip"}
+KERNEL_NAMES = {"attn": ("attn_fwd_bf16_kernel", "attn_fwd_f32_kernel"), "select_pack": ("select_pack_kernel",),
+                "plan": ("attn_plan_kernel",)}
+
+
+def source_digest(rel: str) -> str:
+    import hashlib
+    return hashlib.sha256(open(os.path.join(ROOT, rel), "rb").read()).hexdigest()[:16]
+
+
+def load_traffic(path: str, workload: str) -> dict:
+    """HBM bytes per launch measured by hardware counters, per kernel; a kernel
+    whose source changed since the counters were taken gets None."""
+    try:
+        entry = json.load(open(path)).get(workload, {})
+    except (OSError, ValueError):
+        return {}
+    out = {}
+    for k, rel in KERNEL_SOURCES.items():
+        e = entry.get(k)
+        out[k] = e["bytes_per_launch"] if e and e.get("source_sha") == source_digest(rel) else None
+    return out
+
+
+def _kernel_key(name: str):
+    for k, pats in KERNEL_NAMES.items():
+        if any(p in name for p in pats):
+            return k
+    return None
+
+
+def summarize_profile(d: str, workload: str, traffic_json: str, calib_mib: int) -> int:
+    """Reads the rocprofv3 CSV output of three runs of this script under
+    DIR/stats (--kernel-trace --stats), DIR/fetch (--pmc FETCH_SIZE) and
+    DIR/write (--pmc WRITE_SIZE), each run with --calibrate-copy; scales the
+    counters by what they read for the plain calibration copy; prints a
+    markdown summary and stores the per-launch bytes in the traffic file."""
+    import csv
+    import collections
+    lines = []
+    stats = os.path.join(d, "stats", "run_kernel_stats.csv")
+    if os.path.exists(stats):
+        lines += ["| Kernel | Calls | Average (ns) | Min (ns) | Max (ns) | Share |", "|---|---|---|---|---|---|"]
+        for r in csv.DictReader(open(stats)):
+            name = r["Name"].replace("dora::(anonymous namespace)::", "").replace("void ", "").split("(")[0]
+            lines.append(f"| {name} | {r['Calls']} | {float(r['AverageNs']):,.0f} | {int(r['MinNs']):,} | "
+                         f"{int(r['MaxNs']):,} | {float(r['Percentage']):.1f} % |")
+        lines.append("")
+    calib_kib = calib_mib * 1024.0
+    measured = collections.defaultdict(dict)
+    factors = {}
+    for counter, sub in (("FETCH_SIZE", "fetch"), ("WRITE_SIZE", "write")):
+        f = os.path.join(d, sub, "run_counter_collection.csv")
+        if not os.path.exists(f):
+            continue
+        per = collections.defaultdict(lambda: collections.defaultdict(float))
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] == counter:
+                per[r["Kernel_Name"]][int(r["Dispatch_Id"])] += float(r["Counter_Value"])
+        copies = [v for name, ds in per.items() if "copyBuffer" in name for v in ds.values()]
+        ref = max(copies) if copies else 0.0
+        if ref <= 0:
+            continue
+        factors[counter] = calib_kib / ref
+        lines.append(f"{counter}: the {calib_mib} MiB calibration copy reads {ref:,.0f} KiB "
+                     f"(scale factor {factors[counter]:.3f})")
+        for name, ds in per.items():
+            k = _kernel_key(name)
+            if k is None:
+                continue
+            vals = [ds[i] for i in sorted(ds)]
+            vals = vals[2:] if len(vals) > 3 else vals   # skip the first launches (cold caches)
+            kib = sum(vals) / len(vals)
+            measured[k][counter] = (kib, kib * 1024.0 * factors[counter], len(vals))
+    lines.append("")
+    if measured:
+        lines += ["| Kernel | FETCH_SIZE KiB/launch | WRITE_SIZE KiB/launch | scaled HBM bytes/launch |",
+                  "|---|---|---|---|"]
+    try:
+        allt = json.load(open(traffic_json))
+    except (OSError, ValueError):
+        allt = {}
+    entry = allt.setdefault(workload, {})
+    for k, m in sorted(measured.items()):
+        if "FETCH_SIZE" not in m or "WRITE_SIZE" not in m:
+            continue
+        total = m["FETCH_SIZE"][1] + m["WRITE_SIZE"][1]
+        lines.append(f"| {k} | {m['FETCH_SIZE'][0]:,.0f} | {m['WRITE_SIZE'][0]:,.0f} | {total:,.0f} |")
+        if k in KERNEL_SOURCES:
+            entry[k] = {"bytes_per_launch": total, "fetch_bytes": m["FETCH_SIZE"][1],
+                        "write_bytes": m["WRITE_SIZE"][1], "source_sha": source_digest(KERNEL_SOURCES[k]),
+                        "fetch_factor": factors["FETCH_SIZE"], "write_factor": factors["WRITE_SIZE"]}
+    with open(traffic_json, "w") as fh:
+        json.dump(allt, fh, indent=1, sort_keys=True)
+        fh.write("\n")
+    print("\n".join(lines))
+    return 0
+
+
 def cpu_model() -> str:
     try:
         for line in open("/proc/cpuinfo"):
@@ -86,7 +186,13 @@ def main() -> int:
                          "for scaling hardware byte counters)")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM bytes per launch (from rocprofv3 counters), if present")
+    ap.add_argument("--summarize-profile", metavar="DIR",
+                    help="no benchmark: summarise rocprofv3 output under DIR/{stats,fetch,write} "
+                         "for --workload and update --traffic-json")
     args = ap.parse_args()
+    if args.summarize_profile:
+        return summarize_profile(args.summarize_profile, args.workload, args.traffic_json,
+                                 args.calibrate_copy or 256)
 
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -178,12 +284,7 @@ def main() -> int:
     sp_gbs = sp_bytes / (ms_sel * 1e-3) / 1e9
     peak = MFMA_PEAK_TFLOPS[w.dtype]
 
-    traffic = {}
-    if os.path.exists(args.traffic_json):
-        try:
-            traffic = json.load(open(args.traffic_json)).get(w.name, {})
-        except (OSError, ValueError):
-            traffic = {}
+    traffic = load_traffic(args.traffic_json, w.name)
 
     result = {
         "metric": METRIC,

@@ -45,7 +45,6 @@ constexpr int kThreads = kWaves * 64;
 constexpr int kQPerWave = 32;
 static_assert(kWaves * kQPerWave == kAttnQTile, "tile size");
 constexpr int kKRes = 256;             // keys resident in LDS per stage (bf16)
-constexpr int kKStride = kD + 8;       // bf16 elements per K / V row in LDS (conflict-free reads)
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanBins = 1024;
 constexpr float kLog2e = 1.4426950408889634f;
@@ -263,12 +262,20 @@ __device__ __forceinline__ void leave_queue(AttnPlanHeader* hdr) {
 //   A[16 x 32]: lane holds row c, k = 8g .. 8g+7
 //   B[32 x 16]: lane holds column c, k = 8g .. 8g+7
 //   D[16 x 16]: lane holds column c, rows 4g .. 4g+3
+//
+// LDS layout of a staged K or V block: up to 256 rows of 128 bytes (64 bf16),
+// unpadded, with the eight 16-byte chunks of row r XOR-swizzled (chunk c at
+// position c ^ (r & 7)), so the row reads of K and the transposing reads of V
+// both spread over all banks.  Rows arrive by LDS DMA (global_load_lds_dwordx4):
+// one wave instruction fills 1 KB = 8 consecutive rows, lane l writing
+// position l & 7 of row l >> 3, so lane l fetches chunk (l & 7) ^ (l >> 3).
+// Two such K/V buffers alternate: the DMA of the next stage fills one while
+// the waves compute on the other.
 
-struct KVStage {
-  // 16-byte pieces of K and V rows: key = u >> 3, column = u & 7, u = tid + 512 i.
-  uint4 k0, k1, k2, k3;
-  uint4 v0, v1, v2, v3;
-};
+constexpr int kRowBytes = kD * 2;
+constexpr int kStageElems = kKRes * kD;
+
+typedef __attribute__((address_space(3))) void lds_void;
 
 // Byte address of element (row0, head h, dim 0) of a packed [rows, H, 64]
 // tensor.  Every argument is the same in all lanes, so this is scalar
@@ -277,47 +284,69 @@ __device__ __forceinline__ const char* head_base(const void* X, long long row0, 
   return static_cast<const char*>(X) + (row0 * row_elems + h * kD) * 2;
 }
 
-// Byte offset of this thread's piece i of a stage, its row clamped to `last`.
-__device__ __forceinline__ uint32_t kv_piece_offset(int i, uint32_t last, uint32_t row_bytes) {
-  const uint32_t key = min((threadIdx.x >> 3) + i * (kThreads / 8), last);
-  return key * row_bytes + (threadIdx.x & 7) * 16;
+// Issues the DMA of rows [0, n) of one head's K and V (1 <= n <= 256) into
+// Kd / Vd.  Rows up to the next multiple of 64 are filled as well, with
+// copies of row n-1, so every row a key block reads holds finite data (those
+// keys are masked out of the softmax).
+__device__ __forceinline__ void kv_dma(const char* kbase, const char* vbase, int n, uint32_t row_bytes,
+                                       uint16_t* Kd, uint16_t* Vd) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
+  const uint32_t last = static_cast<uint32_t>(n - 1);
+  const uint32_t chunk = static_cast<uint32_t>(((lane & 7) ^ (lane >> 3)) * 16);
+#pragma unroll
+  for (int i = 0; i < kKRes / 64; ++i) {
+    if (i * 64 < n) {
+      const int row0 = i * 64 + wave * 8;
+      const uint32_t off = min(static_cast<uint32_t>(row0 + (lane >> 3)), last) * row_bytes + chunk;
+      __builtin_amdgcn_global_load_lds(kbase + off, (lds_void*)(Kd + row0 * kD), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(vbase + off, (lds_void*)(Vd + row0 * kD), 16, 0, 0);
+    }
+  }
 }
 
-__device__ __forceinline__ uint4 load16(const char* base, uint32_t off) {
-  return *reinterpret_cast<const uint4*>(base + off);
+// Per-lane byte offsets into a staged block (relative to the first row of a
+// 16- or 32-key step; steps start at multiples of 8 rows, so the swizzle only
+// depends on the lane).
+struct LdsOffsets {
+  uint32_t k0, k1;  // K row c16, dims 8g..8g+7 and 32+8g..32+8g+7
+  uint32_t v[4];    // transposing V read for dims 16 dt .. 16 dt + 15
+};
+
+__device__ __forceinline__ LdsOffsets lds_offsets() {
+  const int lane = threadIdx.x & 63;
+  const int c16 = lane & 15, g = lane >> 4;
+  LdsOffsets o;
+  o.k0 = static_cast<uint32_t>(c16 * kRowBytes + ((g ^ (c16 & 7)) * 16));
+  o.k1 = o.k0 ^ 64u;  // chunk g + 4 sits at position (g ^ (c16 & 7)) ^ 4
+  // ds_read_b64_tr_b16: lane m = 4e + r of each 16-lane group points at
+  // V[row 4g + e][16 dt + 4r .. +3], i.e. chunk 2 dt + r / 2, byte 8 (r & 1).
+  const int e = c16 >> 2, r = c16 & 3;
+  const int row = 4 * g + e;
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+    o.v[dt] = static_cast<uint32_t>(row * kRowBytes + (((2 * dt + (r >> 1)) ^ (row & 7)) * 16) + 8 * (r & 1));
+  return o;
 }
 
-// Rows [0, nk) of one stage, nk >= 1.  Lanes whose row is past the end read
-// row nk-1 again, so every load is in bounds and nothing needs zeroing: those
-// keys only reach a block's masked tail, and the copied V rows are finite.
-__device__ __forceinline__ KVStage kv_load(const char* kbase, const char* vbase, int nk, uint32_t row_bytes) {
-  const uint32_t last = static_cast<uint32_t>(nk - 1);
-  const uint32_t o0 = kv_piece_offset(0, last, row_bytes), o1 = kv_piece_offset(1, last, row_bytes);
-  const uint32_t o2 = kv_piece_offset(2, last, row_bytes), o3 = kv_piece_offset(3, last, row_bytes);
-  KVStage st;
-  st.k0 = load16(kbase, o0);
-  st.v0 = load16(vbase, o0);
-  st.k1 = load16(kbase, o1);
-  st.v1 = load16(vbase, o1);
-  st.k2 = load16(kbase, o2);
-  st.v2 = load16(vbase, o2);
-  st.k3 = load16(kbase, o3);
-  st.v3 = load16(vbase, o3);
-  return st;
-}
+// Per-lane read pointers into one staged K/V buffer.  They are formed once
+// per stage, outside the key-block loop, so the buffer's base (which lies past
+// the 16-bit offset range of LDS instructions for the second buffer) sits in
+// the lane's address register and each read inside the loop carries only the
+// block and step offsets.
+struct LanePtrs {
+  const char* k0;
+  const char* k1;
+  const char* v[4];
+};
 
-// K and V are both kept row-major ([key][64 dims], padded rows).
-__device__ __forceinline__ void kv_store(const KVStage& st, uint16_t* Ks, uint16_t* Vs) {
-  const int off = (threadIdx.x >> 3) * kKStride + (threadIdx.x & 7) * 8;
-  constexpr int kStep = (kThreads / 8) * kKStride;  // 64 rows
-  *reinterpret_cast<uint4*>(&Ks[off]) = st.k0;
-  *reinterpret_cast<uint4*>(&Vs[off]) = st.v0;
-  *reinterpret_cast<uint4*>(&Ks[off + kStep]) = st.k1;
-  *reinterpret_cast<uint4*>(&Vs[off + kStep]) = st.v1;
-  *reinterpret_cast<uint4*>(&Ks[off + 2 * kStep]) = st.k2;
-  *reinterpret_cast<uint4*>(&Vs[off + 2 * kStep]) = st.v2;
-  *reinterpret_cast<uint4*>(&Ks[off + 3 * kStep]) = st.k3;
-  *reinterpret_cast<uint4*>(&Vs[off + 3 * kStep]) = st.v3;
+__device__ __forceinline__ LanePtrs lane_ptrs(const char* Ks, const char* Vs, const LdsOffsets& lo) {
+  LanePtrs lp;
+  lp.k0 = Ks + lo.k0;
+  lp.k1 = Ks + lo.k1;
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) lp.v[dt] = Vs + lo.v[dt];
+  return lp;
 }
 
 // Four V values of one dimension for four keys, read with the gfx950
@@ -325,11 +354,9 @@ __device__ __forceinline__ void kv_store(const KVStage& st, uint16_t* Ks, uint16
 // V[row(e)][col0 + 4r .. +3]; lane j then receives V[row(e)][col0 + j] for
 // e = 0..3 (the instruction hands lane j element j % 4 of the addresses of
 // lanes 4e + j / 4).
-__device__ __forceinline__ bf16x4 v_column4(const uint16_t* Vs, int row0, int col0) {
-  const int m = threadIdx.x & 15;
-  const uint16_t* p = &Vs[(row0 + (m >> 2)) * kKStride + col0 + 4 * (m & 3)];
+__device__ __forceinline__ bf16x4 v_column4(const char* p) {
   typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
-  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(const_cast<uint16_t*>(p)));
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(const_cast<char*>(p)));
 }
 
 // Query tile j of wave w is 16-query tile (w + 8 j) of the item's chunk, so
@@ -350,16 +377,8 @@ __device__ __forceinline__ void q_load(const char* qbase, int nq, uint32_t row_b
   }
 }
 
-// K/V rows [first, first + n) of an item's head into the staging registers;
-// with n == 0 it re-reads row 0 of head 0 (harmless, never stored).
-__device__ __forceinline__ KVStage kv_stage_load(const AttnParams& p, const Item& it, int first, int n,
-                                                 long long row_elems, uint32_t row_bytes) {
-  const long long row0 = n > 0 ? static_cast<long long>(it.seq0) + first : 0;
-  const int h = n > 0 ? it.h : 0;
-  return kv_load(head_base(p.k, row0, row_elems, h), head_base(p.v, row0, row_elems, h), max(n, 1), row_bytes);
-}
-
-// The queries of an item's chunk; an empty item re-reads row 0 of head 0.
+// The queries of an item's chunk; an empty item re-reads row 0 of head 0
+// (which exists whenever there is an item), so the load is unconditional.
 __device__ __forceinline__ void q_chunk_load(const AttnParams& p, const Item& it, long long row_elems,
                                              uint32_t row_bytes, bf16x8 (&qn)[2][2]) {
   const int q0 = it.chunk * kAttnQTile;
@@ -372,16 +391,14 @@ __device__ __forceinline__ void q_chunk_load(const AttnParams& p, const Item& it
 // S^T[key][query] for keys kb .. kb+63 of the staged block: 4 key tiles of 16
 // against query tile 0 (and tile 1 when ACT1).
 template <bool ACT1>
-__device__ __forceinline__ void qk_block(const uint16_t* Ks, int kb, const bf16x8 (&qf)[2][2],
+__device__ __forceinline__ void qk_block(const LanePtrs& lp, int kb, const bf16x8 (&qf)[2][2],
                                          floatx4 (&s)[2][4]) {
-  const int lane = threadIdx.x & 63;
-  const int c16 = lane & 15, g = lane >> 4;
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int kt = 0; kt < 4; ++kt) {
-    const uint16_t* krow = &Ks[(kb + kt * 16 + c16) * kKStride + g * 8];
-    const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(krow);
-    const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(krow + 32);
+    const int off = (kb + kt * 16) * kRowBytes;
+    const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(lp.k0 + off);
+    const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(lp.k1 + off);
     s[0][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
         a1, qf[0][1], __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, qf[0][0], zero, 0, 0, 0), 0, 0, 0);
     if (ACT1)
@@ -400,8 +417,9 @@ struct SoftmaxState {
 // an item's first block: the running max starts at the block max and the
 // accumulators start from zero.
 template <bool ACT1, bool FIRST>
-__device__ __forceinline__ void softmax_pv_block(const uint16_t* Vs, int kb, int kvalid, float scale_log2,
-                                                 const bf16x8& ones, floatx4 (&s)[2][4], SoftmaxState& st) {
+__device__ __forceinline__ void softmax_pv_block(const LanePtrs& lp, int kb, int kvalid, float scale_log2,
+                                                 const bf16x8& ones, floatx4 (&s)[2][4],
+                                                 SoftmaxState& st) {
   constexpr int kTiles = ACT1 ? 2 : 1;
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4;
@@ -480,11 +498,11 @@ __device__ __forceinline__ void softmax_pv_block(const uint16_t* Vs, int kb, int
       st.l[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[j][ks], init ? zero : st.l[j], 0, 0, 0);
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) {
-      // A operand V^T: lane (c16, g) needs dim dt*16 + c16 at keys ks*32 + 4g + 0..3 (lo)
-      // and ks*32 + 16 + 4g + 0..3 (hi), matching the key order of P^T.
-      const bf16x4 lo = v_column4(Vs, kb + ks * 32 + 4 * g, dt * 16);
-      const bf16x4 hi = v_column4(Vs, kb + ks * 32 + 16 + 4 * g, dt * 16);
-      const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      // A operand V^T: lane (c16, g) holds dim dt*16 + c16 at keys ks*32 + 4g + 0..3
+      // and ks*32 + 16 + 4g + 0..3, the key order of P^T.
+      const char* lo_rows = lp.v[dt] + (kb + ks * 32) * kRowBytes;
+      const bf16x8 a = __builtin_shufflevector(v_column4(lo_rows), v_column4(lo_rows + 16 * kRowBytes),
+                                               0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
       for (int j = 0; j < kTiles; ++j)
         st.o[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[j][ks], init ? zero : st.o[j][dt], 0, 0, 0);
@@ -496,20 +514,19 @@ __device__ __forceinline__ void softmax_pv_block(const uint16_t* Vs, int kb, int
 // flight: the MFMAs of block kb+64 are issued before the softmax of block kb,
 // so the matrix unit and the VALU overlap.
 template <bool ACT1>
-__device__ __forceinline__ void attend_stage(const uint16_t* Ks, const uint16_t* Vs, int nk, bool first,
-                                             float scale_log2, const bf16x8& ones, const bf16x8 (&qf)[2][2],
-                                             SoftmaxState& sm) {
+__device__ __forceinline__ void attend_stage(const LanePtrs& lp, int nk, bool first, float scale_log2,
+                                             const bf16x8& ones, const bf16x8 (&qf)[2][2], SoftmaxState& sm) {
   floatx4 sa[2][4], sbk[2][4];
-  qk_block<ACT1>(Ks, 0, qf, sa);
-  if (nk > 64) qk_block<ACT1>(Ks, 64, qf, sbk);
-  if (first) softmax_pv_block<ACT1, true>(Vs, 0, nk, scale_log2, ones, sa, sm);
-  else softmax_pv_block<ACT1, false>(Vs, 0, nk, scale_log2, ones, sa, sm);
+  qk_block<ACT1>(lp, 0, qf, sa);
+  if (nk > 64) qk_block<ACT1>(lp, 64, qf, sbk);
+  if (first) softmax_pv_block<ACT1, true>(lp, 0, nk, scale_log2, ones, sa, sm);
+  else softmax_pv_block<ACT1, false>(lp, 0, nk, scale_log2, ones, sa, sm);
   for (int kb = 64; kb < nk; kb += 128) {
-    if (kb + 64 < nk) qk_block<ACT1>(Ks, kb + 64, qf, sa);
-    softmax_pv_block<ACT1, false>(Vs, kb, nk - kb, scale_log2, ones, sbk, sm);
+    if (kb + 64 < nk) qk_block<ACT1>(lp, kb + 64, qf, sa);
+    softmax_pv_block<ACT1, false>(lp, kb, nk - kb, scale_log2, ones, sbk, sm);
     if (kb + 64 >= nk) break;
-    if (kb + 128 < nk) qk_block<ACT1>(Ks, kb + 128, qf, sbk);
-    softmax_pv_block<ACT1, false>(Vs, kb + 64, nk - kb - 64, scale_log2, ones, sa, sm);
+    if (kb + 128 < nk) qk_block<ACT1>(lp, kb + 128, qf, sbk);
+    softmax_pv_block<ACT1, false>(lp, kb + 64, nk - kb - 64, scale_log2, ones, sa, sm);
   }
 }
 
@@ -534,135 +551,189 @@ __device__ __forceinline__ void store_out(char* obase, int nq, uint32_t row_byte
   }
 }
 
+// Workgroup-uniform scheduling state of the execute loop.
+struct Sched {
+  Item cur, nx;    // item being computed, next item
+  bool nx_valid;
+  bool shift;      // the previous stage finished `cur`
+  int sb;          // stage (256-key block) of `cur`
+  int t_nn;        // thread 0: ticket of the item after `nx`
+};
+
+struct KernelCtx {
+  const AttnParams& p;
+  int n_items, G;
+  long long row_elems;
+  uint32_t row_bytes;
+  LdsOffsets lo;
+  bf16x8 ones;
+};
+
+// One stage: compute `cur`'s keys [sb*256, sb*256 + 256) from buffer Kc/Vc
+// while the DMA of the next stage fills Kn/Vn.  Returns false after the last
+// stage of the workgroup.
+template <int B>
+__device__ __forceinline__ bool attn_stage(const KernelCtx& c, Sched& s, const char* Kc, const char* Vc,
+                                           uint16_t* Kn, uint16_t* Vn, int2* s_raw, bf16x8 (&qn)[2][2],
+                                           bf16x8 (&qf)[2][2], SoftmaxState& sm) {
+  const AttnParams& p = c.p;
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6;
+  // This stage's DMA (issued one stage ago) has landed for every wave, every
+  // wave is done with the other buffer, and the descriptor thread 0 published
+  // at the end of the previous stage is visible.  Only LDS needs ordering
+  // here, so the barrier does not wait for this wave's output stores.
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+  if (s.shift) {
+    const int2 raw = uniform_raw(s_raw[1 - B]);
+    const bool nn_valid = raw.x != -1;
+    const Item nn = nn_valid ? decode_item(p, raw) : Item{0, 0, 0, 0};
+    s.cur = s.nx;
+    s.nx = nn;
+    s.nx_valid = nn_valid;
+    s.sb = 0;
+  }
+  const Item cur = s.cur;
+  const int kb0 = s.sb * kKRes;
+  const int nk = min(kKRes, cur.len - kb0);
+  const int q0 = cur.chunk * kAttnQTile;
+  const int nq = min(kAttnQTile, cur.len - q0);
+  const bool act0 = tile_q(wave, 0) < nq;
+  const bool act1 = tile_q(wave, 1) < nq;
+  if (s.sb == 0) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      qf[j][0] = qn[j][0];
+      qf[j][1] = qn[j][1];
+    }
+  }
+
+  // Next stage: the rest of this item's keys, or the next item.
+  const bool more_keys = kb0 + kKRes < cur.len;
+  const bool have_next = more_keys || s.nx_valid;
+  if (have_next) {
+    const Item kv_item = more_keys ? cur : s.nx;
+    const int kv_first = more_keys ? kb0 + kKRes : 0;
+    const int kv_n = min(kKRes, kv_item.len - kv_first);
+    if (kv_n > 0)
+      kv_dma(head_base(p.k, static_cast<long long>(kv_item.seq0) + kv_first, c.row_elems, kv_item.h),
+             head_base(p.v, static_cast<long long>(kv_item.seq0) + kv_first, c.row_elems, kv_item.h), kv_n,
+             c.row_bytes, Kn, Vn);
+  }
+  // The next item's queries (harmlessly early, and again, while `cur` still
+  // has stages left: `qf` holds its copy).
+  q_chunk_load(p, s.nx_valid ? s.nx : Item{0, 0, 0, 0}, c.row_elems, c.row_bytes, qn);
+  // Queue traffic goes out after the prefetch; its results are only
+  // consumed at the end of the stage (no wait in between).
+  int2 raw_next;
+  raw_next.x = -1;
+  raw_next.y = 0;
+  int t_got = 0;
+  if (tid == 0 && !more_keys) {
+    if (s.t_nn < c.n_items) raw_next = p.items[s.t_nn];
+    t_got = atomicAdd(&p.hdr->counter, 1);
+  }
+
+  if (act0) {
+    char* obase = const_cast<char*>(head_base(p.out, static_cast<long long>(cur.seq0) + q0, c.row_elems, cur.h));
+    const LanePtrs lp = lane_ptrs(Kc, Vc, c.lo);
+    if (act1) {
+      attend_stage<true>(lp, nk, s.sb == 0, p.scale_log2, c.ones, qf, sm);
+      if (!more_keys) store_out<true>(obase, nq, c.row_bytes, sm);
+    } else {
+      attend_stage<false>(lp, nk, s.sb == 0, p.scale_log2, c.ones, qf, sm);
+      if (!more_keys) store_out<false>(obase, nq, c.row_bytes, sm);
+    }
+  }
+
+  if (tid == 0 && !more_keys) {
+    s_raw[B] = raw_next;
+    s.t_nn = t_got + 3 * c.G;
+  }
+  s.shift = !more_keys;
+  if (more_keys) ++s.sb;
+  return have_next;
+}
+
 __global__ __launch_bounds__(kThreads) void attn_fwd_bf16_kernel(AttnParams p) {
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[kKRes * kKStride];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[kKRes * kKStride];
-  __shared__ int2 s_raw[2];   // item descriptors handed from thread 0 to the workgroup
+  // Two K/V buffer pairs in one object, V first: the V buffers take the low
+  // 64 KB of LDS, where the constant parts of the transposing V reads' addresses
+  // (16 per key block) fit the instruction's offset field; the 8 K reads per
+  // block pay the extra adds instead.
+  struct StageLds {
+    uint16_t v0[kStageElems], v1[kStageElems], k0[kStageElems], k1[kStageElems];
+  };
+  __shared__ __attribute__((aligned(1024))) StageLds lds;
+  uint16_t* const V0 = lds.v0;
+  uint16_t* const V1 = lds.v1;
+  uint16_t* const K0 = lds.k0;
+  uint16_t* const K1 = lds.k1;
+  __shared__ int2 s_init[2];  // the first two item descriptors
+  __shared__ int2 s_raw[2];   // descriptor handed from thread 0 to the workgroup, by stage parity
   __shared__ int s_first;
 
   if (!plan_matches(p)) {
     if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(p.status, DORA_DEV_PLAN);
     return;
   }
-  const int n_items = min(p.hdr->n_items, p.max_items);
   const int tid = threadIdx.x;
-  const int wave = tid >> 6;
-  const int G = static_cast<int>(gridDim.x);
-  const long long row_elems = static_cast<long long>(p.H) * kD;
-  const uint32_t row_bytes = static_cast<uint32_t>(row_elems) * 2u;
+  KernelCtx c{p, min(p.hdr->n_items, p.max_items), static_cast<int>(gridDim.x), static_cast<long long>(p.H) * kD,
+              static_cast<uint32_t>(p.H) * kD * 2u, lds_offsets(), {}};
+#pragma unroll
+  for (int e = 0; e < 8; ++e) c.ones[e] = static_cast<__bf16>(1.0f);
 
   // Queue.  Tickets 0 .. 3G-1 are dealt statically (workgroup w takes w, w+G
   // and w+2G, the longest items), the rest come from the atomic counter, so
   // the start of the kernel is not a burst of atomics on one address.
-  // `cur` computes while the K/V/Q of the next stage load.  Thread 0 alone
-  // talks to the queue: it holds the ticket of the item after `nx` (t_nn),
-  // loads that item's descriptor during the stage and publishes it in LDS at
-  // the end of the stage, so no wave waits on the queue mid-stage.
-  int t_nn = 0;
+  // Thread 0 alone talks to the queue: it holds the ticket of the item after
+  // `nx`, loads that item's descriptor during a stage and publishes it in LDS
+  // at the end of the stage, so no wave waits on the queue mid-stage.
+  Sched s;
+  s.t_nn = 0;
   if (tid == 0) {
-    const int t0 = blockIdx.x, t1 = blockIdx.x + G;
-    t_nn = blockIdx.x + 2 * G;
+    const int t0 = blockIdx.x, t1 = blockIdx.x + c.G;
+    s.t_nn = blockIdx.x + 2 * c.G;
     s_first = t0;
     int2 r0, r1;
     r0.x = -1;
     r0.y = 0;
     r1 = r0;
-    if (t0 < n_items) r0 = p.items[t0];
-    if (t1 < n_items) r1 = p.items[t1];
-    s_raw[0] = r0;
-    s_raw[1] = r1;
+    if (t0 < c.n_items) r0 = p.items[t0];
+    if (t1 < c.n_items) r1 = p.items[t1];
+    s_init[0] = r0;
+    s_init[1] = r1;
   }
   __syncthreads();
-  if (s_first >= n_items) {
+  if (s_first >= c.n_items) {
     leave_queue(p.hdr);
     return;
   }
-  Item cur = decode_item(p, uniform_raw(s_raw[0]));
-  const int2 raw1 = uniform_raw(s_raw[1]);
-  bool nx_valid = raw1.x != -1;
-  Item nx = nx_valid ? decode_item(p, raw1) : Item{0, 0, 0, 0};
-  __syncthreads();
+  s.cur = decode_item(p, uniform_raw(s_init[0]));
+  const int2 raw1 = uniform_raw(s_init[1]);
+  s.nx_valid = raw1.x != -1;
+  s.nx = s.nx_valid ? decode_item(p, raw1) : Item{0, 0, 0, 0};
+  s.shift = false;
+  s.sb = 0;
 
   bf16x8 qn[2][2], qf[2][2];
-  // Loads are issued unconditionally (a stage with nothing to load re-reads
-  // row 0, which exists whenever there is an item), so the staging registers
-  // are never live across a branch.
-  KVStage stage = kv_stage_load(p, cur, 0, min(cur.len, kKRes), row_elems, row_bytes);
-  q_chunk_load(p, cur, row_elems, row_bytes, qn);
-
+  {
+    const int nk = min(s.cur.len, kKRes);
+    if (nk > 0)
+      kv_dma(head_base(p.k, s.cur.seq0, c.row_elems, s.cur.h), head_base(p.v, s.cur.seq0, c.row_elems, s.cur.h), nk,
+             c.row_bytes, K0, V0);
+    q_chunk_load(p, s.cur, c.row_elems, c.row_bytes, qn);
+  }
   SoftmaxState sm;
-  bf16x8 ones;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) ones[e] = static_cast<__bf16>(1.0f);
-  int sb = 0;
-  bool shift = false;  // the previous stage finished an item
   for (;;) {
-    __syncthreads();  // every wave is done with the previous stage; s_raw[0] is published
-    kv_store(stage, Ks, Vs);
-    if (shift) {
-      const int2 raw = uniform_raw(s_raw[0]);
-      const bool nn_valid = raw.x != -1;
-      const Item nn = nn_valid ? decode_item(p, raw) : Item{0, 0, 0, 0};
-      cur = nx;
-      nx = nn;
-      nx_valid = nn_valid;
-      sb = 0;
-    }
-    __syncthreads();
-
-    const int kb0 = sb * kKRes;
-    const int nk = min(kKRes, cur.len - kb0);
-    const int q0 = cur.chunk * kAttnQTile;
-    const int nq = min(kAttnQTile, cur.len - q0);
-    const bool act0 = tile_q(wave, 0) < nq;
-    const bool act1 = tile_q(wave, 1) < nq;
-    if (sb == 0) {
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        qf[j][0] = qn[j][0];
-        qf[j][1] = qn[j][1];
-      }
-    }
-
-    // Next stage: the rest of this item's keys, or the next item.
-    const bool more_keys = kb0 + kKRes < cur.len;
-    const bool have_next = more_keys || nx_valid;
-    {
-      const Item kv_item = more_keys ? cur : nx;
-      const int kv_first = more_keys ? kb0 + kKRes : 0;
-      const int kv_n = have_next ? min(kKRes, kv_item.len - kv_first) : 0;
-      stage = kv_stage_load(p, kv_item, kv_first, kv_n, row_elems, row_bytes);
-      if (!more_keys) q_chunk_load(p, nx_valid ? nx : Item{0, 0, 0, 0}, row_elems, row_bytes, qn);
-    }
-    // Queue traffic goes out after the prefetch; its results are only
-    // consumed at the end of the stage (no wait in between).
-    int2 raw_next;
-    raw_next.x = -1;
-    raw_next.y = 0;
-    int t_got = 0;
-    if (tid == 0 && !more_keys) {
-      if (t_nn < n_items) raw_next = p.items[t_nn];
-      t_got = atomicAdd(&p.hdr->counter, 1);
-    }
-
-    if (act0) {
-      char* obase = const_cast<char*>(head_base(p.out, static_cast<long long>(cur.seq0) + q0, row_elems, cur.h));
-      if (act1) {
-        attend_stage<true>(Ks, Vs, nk, sb == 0, p.scale_log2, ones, qf, sm);
-        if (!more_keys) store_out<true>(obase, nq, row_bytes, sm);
-      } else {
-        attend_stage<false>(Ks, Vs, nk, sb == 0, p.scale_log2, ones, qf, sm);
-        if (!more_keys) store_out<false>(obase, nq, row_bytes, sm);
-      }
-    }
-
-    if (tid == 0 && !more_keys) {
-      s_raw[0] = raw_next;
-      t_nn = t_got + 3 * G;
-    }
-    shift = !more_keys;
-    if (!have_next) break;
-    if (more_keys) ++sb;
+    if (!attn_stage<0>(c, s, reinterpret_cast<const char*>(K0), reinterpret_cast<const char*>(V0), K1, V1, s_raw,
+                       qn, qf, sm))
+      break;
+    if (!attn_stage<1>(c, s, reinterpret_cast<const char*>(K1), reinterpret_cast<const char*>(V1), K0, V0, s_raw,
+                       qn, qf, sm))
+      break;
   }
   leave_queue(p.hdr);
 }
