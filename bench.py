@@ -254,25 +254,33 @@ def main() -> int:
     torch.cuda.synchronize()
     assert int(st.item()) == 0, f"device status {int(st.item())}"
 
+    # Each repeat times K steps twice: once bare (the step time: events only at
+    # the two ends) and once with events around every kernel (per-kernel
+    # durations; an event between two kernels adds a few microseconds of
+    # dispatch latency to the interval, so these are upper bounds).
     reps = []
     for rep in range(args.repeats):
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
         t_start = torch.cuda.Event(enable_timing=True)
         t_end = torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         t_start.record(stream)
         for i in range(args.steps):
-            step(evs[i])
+            step()
         t_end.record(stream)
         torch.cuda.synchronize()
         total_ms = t_start.elapsed_time(t_end)
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        for i in range(args.steps):
+            step(evs[i])
+        torch.cuda.synchronize()
         sel = np.mean([e[0].elapsed_time(e[1]) for e in evs])
         plan = np.mean([e[1].elapsed_time(e[2]) for e in evs])
         attn = np.mean([e[2].elapsed_time(e[3]) for e in evs])
         reps.append((total_ms / args.steps, sel, plan, attn))
         print(f"[bench] repeat {rep}: {total_ms / args.steps * 1e3:.1f} us/step "
-              f"(select_pack {sel * 1e3:.1f}, plan {plan * 1e3:.1f}, attention {attn * 1e3:.1f})",
-              file=sys.stderr, flush=True)
+              f"(per kernel with events: select_pack {sel * 1e3:.1f}, plan {plan * 1e3:.1f}, "
+              f"attention {attn * 1e3:.1f})", file=sys.stderr, flush=True)
     assert int(st.item()) == 0, f"device status {int(st.item())}"
     med = sorted(reps, key=lambda x: x[0])[len(reps) // 2]
     ms_step, ms_sel, ms_plan, ms_attn = med

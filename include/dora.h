@@ -7,7 +7,7 @@
  * (Sec. 3.1, Eq. (1); Sec. 3.2 "Sampling and deployment"; App. A.3).  The
  * survivors of all images are compacted into one packed buffer with
  * explicit sequence boundaries and processed by variable-length attention
- * that never attends across images (Sec. 3.5 "Inference"; App. E.4).
+ * that never attends across images (Sec. 3.5 "Inference"; App. E.5).
  *
  * This library implements that path as two calls:
  *   dora_select_pack  -- per-image top-k selection with CLS pinned, the
@@ -77,7 +77,7 @@ typedef enum {
  *
  * For every image b with input segment of n_b tokens (position 0 is CLS):
  *   keep CLS and the keep[b]-1 visual positions with the highest score,
- *   comparing scores as FP32 values (App. E.4); equal scores go to the lower
+ *   comparing scores as FP32 values (App. E.5); equal scores go to the lower
  *   position, NaN ranks below every number, -0 equals +0.  The kept
  *   positions are written in ascending order, so CLS and the survivors'
  *   relative order are preserved.
@@ -134,7 +134,8 @@ size_t dora_varlen_attn_workspace_size(int32_t B, int32_t H, int32_t max_seqlen)
  *
  *   cu_seqlens int32 [B+1]: 0 = cu[0] <= cu[1] <= ... <= cu[B] <= total and
  *              cu[b+1]-cu[b] <= max_seqlen; empty sequences are allowed.
- *   B >= 1, 1 <= H <= 256, 1 <= max_seqlen <= DORA_MAX_SEQLEN, total >= 0.
+ *   1 <= B <= 8192, 1 <= H <= 256, 1 <= max_seqlen <= DORA_MAX_SEQLEN,
+ *              0 <= total <= 2^31-1.
  *   workspace  device, 256-byte aligned, >= dora_varlen_attn_workspace_size bytes.
  *   dev_status DORA_DEV_CU_SEQLENS when the offsets are invalid (the plan is
  *              then empty and _execute writes nothing).
@@ -145,7 +146,7 @@ int dora_varlen_attn_plan(const int32_t* cu_seqlens, int32_t B, int32_t H, int32
 
 /*
  * dora_varlen_attn_execute -- exact softmax attention inside each packed
- * sequence (Sec. 3.5 "Inference"; App. E.4): for every sequence b and head h
+ * sequence (Sec. 3.5 "Inference"; App. E.5): for every sequence b and head h
  *   O_b,h = softmax(softmax_scale * Q_b,h K_b,h^T) V_b,h
  * with no causal mask, no bias and no attention across sequence boundaries.
  *

@@ -13,7 +13,7 @@ The arithmetic lives in ``dora_oracle.c`` (plain C, fp64 for attention):
   buffer with explicit boundaries (Sec. 3.5 "Inference").  Implemented as a
   full sort of (score, position) per image.
 * ``varlen_attn`` is exact softmax attention inside each boundary
-  (Sec. 3.5; App. E.4), computed as a dense fp64 score matrix per
+  (Sec. 3.5; App. E.5), computed as a dense fp64 score matrix per
   (image, head) from the exact values of the bf16 / fp32 inputs.
 
 Pins (tests/test_oracle_*.py): brute-force counting definition of the keep

@@ -11,10 +11,10 @@
  *     removed; deletion preserves CLS and the relative order of survivors
  *     (Sec. 3.1, pruning operator, Eq. (1)).  Here scores are keep-scores
  *     (higher = keep), so an image keeps CLS plus its keep-1 highest-scoring
- *     visual tokens.  Score comparisons are FP32 values (App. E.4).
+ *     visual tokens.  Score comparisons are FP32 values (App. E.5).
  *   - Packing (Sec. 3.5 "Inference"): survivors of all images are compacted
  *     into one buffer with explicit sequence boundaries.
- *   - Attention (Sec. 3.5, App. E.4): exact softmax attention inside each
+ *   - Attention (Sec. 3.5, App. E.5): exact softmax attention inside each
  *     sequence boundary, with no attention between images, no bias term and
  *     no token-size correction.
  *

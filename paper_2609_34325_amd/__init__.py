@@ -9,7 +9,7 @@ DORA (arXiv 2609.34325): hard deletion keeps CLS and the survivors' order
 (Sec. 3.1, Eq. (1)); deployment removes the highest-scoring visual tokens
 (Sec. 3.2 "Sampling and deployment"; App. A.3); survivors are packed with
 explicit sequence boundaries and run through variable-length attention that
-never attends across images (Sec. 3.5 "Inference"; App. E.4).
+never attends across images (Sec. 3.5 "Inference"; App. E.5).
 
 There is no fallback: if the library is missing, every call raises.
 """

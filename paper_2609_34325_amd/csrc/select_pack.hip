@@ -3,7 +3,7 @@
 // DORA (arXiv 2609.34325): Sec. 3.1 Eq. (1) (delete rows, keep CLS and the
 // survivors' order), Sec. 3.2 "Sampling and deployment" and App. A.3 (remove
 // the highest-scoring visual tokens), Sec. 3.5 "Inference" (packed buffer with
-// explicit sequence boundaries), App. E.4 (FP32 score comparisons).
+// explicit sequence boundaries), App. E.5 (FP32 score comparisons).
 //
 // One launch.  Workgroup (b, s) handles image b; the `split` workgroups of an
 // image each repeat the (cheap) selection and then copy a disjoint share of

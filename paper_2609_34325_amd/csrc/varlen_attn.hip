@@ -1,5 +1,5 @@
 // Variable-length multi-head attention over the packed buffer.
-// DORA (arXiv 2609.34325), Sec. 3.5 "Inference" and App. E.4: survivors of
+// DORA (arXiv 2609.34325), Sec. 3.5 "Inference" and App. E.5: survivors of
 // all images are packed with explicit sequence boundaries and processed by
 // exact softmax attention that never crosses a boundary (no mask beyond the
 // boundaries, no bias, no token-size term).

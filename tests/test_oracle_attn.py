@@ -2,7 +2,7 @@
 
 The paper fixes exact softmax attention inside each packed sequence with no
 attention across images and no bias or token-size term (Sec. 3.5
-"Inference"; App. E.4).  Each check computes the expected answer a different
+"Inference"; App. E.5).  Each check computes the expected answer a different
 way: a pure-Python triple loop, torch's fp64 scaled_dot_product_attention on
 dense and padded+masked batches, hand-worked closed forms, and invariances.
 """
