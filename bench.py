@@ -53,8 +53,15 @@ KERNEL_NAMES = {"attn": ("attn_fwd_bf16_kernel", "attn_fwd_f32_kernel"), "select
 
 
 def source_digest(rel: str) -> str:
+    """Hash of a kernel source with comments and blank lines removed, so that
+    stored counter readings go stale when the code changes, not its comments."""
     import hashlib
-    return hashlib.sha256(open(os.path.join(ROOT, rel), "rb").read()).hexdigest()[:16]
+    import re
+    text = open(os.path.join(ROOT, rel)).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    code = "\n".join(l.rstrip() for l in text.splitlines() if l.strip())
+    return hashlib.sha256(code.encode()).hexdigest()[:16]
 
 
 def load_traffic(path: str, workload: str) -> dict:
