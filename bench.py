@@ -48,7 +48,8 @@ def attn_bytes(w: W.Workload, keep: np.ndarray) -> int:
 
 KERNEL_SOURCES = {"attn": "paper_2609_34325_amd/csrc/varlen_attn.hip",
                   "select_pack": "paper_2609_34325_amd/csrc/select_pack.hip"}
-KERNEL_NAMES = {"attn": ("attn_fwd_bf16_kernel", "attn_fwd_f32_kernel"), "select_pack": ("select_pack_kernel",),
+KERNEL_NAMES = {"attn": ("attn_fwd_bf16_kernel", "attn_fwd_f32_kernel"),
+                "select_pack": ("select_pack_kernel",),
                 "plan": ("attn_plan_kernel",)}
 
 
@@ -127,7 +128,9 @@ def summarize_profile(d: str, workload: str, traffic_json: str, calib_mib: int) 
             vals = [ds[i] for i in sorted(ds)]
             vals = vals[2:] if len(vals) > 3 else vals   # skip the first launches (cold caches)
             kib = sum(vals) / len(vals)
-            measured[k][counter] = (kib, kib * 1024.0 * factors[counter], len(vals))
+            # kernels of one entry point add up (one launch of each per call)
+            prev = measured[k].get(counter, (0.0, 0.0, 0))
+            measured[k][counter] = (prev[0] + kib, prev[1] + kib * 1024.0 * factors[counter], len(vals))
     lines.append("")
     if measured:
         lines += ["| Kernel | FETCH_SIZE KiB/launch | WRITE_SIZE KiB/launch | scaled HBM bytes/launch |",

@@ -13,7 +13,7 @@
 //                 step, counting with wave ballots (keys live in VGPRs);
 //                 ordered compaction of the keep flags with ballot + mbcnt.
 //   waves 1..3    sum keep[0..b) -> this image's output offset (cu_out[b]).
-//   all waves     16-byte row copies, 8 loads in flight per lane.
+//   all waves     16-byte row copies, 2 loads in flight per lane.
 #include <limits.h>
 #include <stdlib.h>
 
@@ -23,7 +23,7 @@ namespace dora {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kCopyUnroll = 8;
+constexpr int kCopyUnroll = 2;  // loads in flight per lane: few, so stores start early (measured best)
 
 struct SelectPackParams {
   const float* scores;
@@ -198,7 +198,7 @@ int pick_split(int B, int N) {
     const char* e = getenv("DORA_SELECT_SPLIT");
     override_split = e ? atoi(e) : 0;
   }
-  int split = override_split > 0 ? override_split : (2048 + B - 1) / B;
+  int split = override_split > 0 ? override_split : (1024 + B - 1) / B;  // ~4 workgroups per compute unit
   const int max_split = N / 16 > 1 ? N / 16 : 1;  // at least ~16 rows per workgroup
   if (split > max_split) split = max_split;
   if (split < 1) split = 1;
