@@ -117,6 +117,7 @@ __device__ __forceinline__ void write_header(const PlanParams& p, int n_items) {
 }
 
 __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanParams p) {
+  __shared__ int32_t s_cu[kPlanMaxB + 1];  // cu_seqlens, read from global memory once
   __shared__ int hist[kPlanBins];
   __shared__ uint32_t order[kPlanMaxB];  // sequence | len << 13, by decreasing length
   __shared__ int base[kPlanMaxB + 1];    // first item of each sorted position
@@ -127,12 +128,13 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanParams p) {
   while ((p.max_seqlen >> shift) >= kPlanBins) ++shift;
 
   for (int i = tid; i < kPlanBins; i += kPlanThreads) hist[i] = 0;
-  if (tid == 0) s_bad = (p.cu[0] != 0);
+  for (int i = tid; i <= p.B; i += kPlanThreads) s_cu[i] = p.cu[i];
+  if (tid == 0) s_bad = 0;
   __syncthreads();
   for (int b = tid; b < p.B; b += kPlanThreads) {
-    const long long a = p.cu[b], e = p.cu[b + 1];
+    const long long a = s_cu[b], e = s_cu[b + 1];
     const long long len = e - a;
-    if (a < 0 || e > p.total || len < 0 || len > p.max_seqlen) s_bad = 1;
+    if (a < 0 || e > p.total || len < 0 || len > p.max_seqlen || (b == 0 && a != 0)) s_bad = 1;
     else atomicAdd(&hist[static_cast<int>(len) >> shift], 1);
   }
   __syncthreads();
@@ -153,7 +155,7 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanParams p) {
   }
   __syncthreads();
   for (int b = tid; b < p.B; b += kPlanThreads) {
-    const int len = p.cu[b + 1] - p.cu[b];
+    const int len = s_cu[b + 1] - s_cu[b];
     const int pos = atomicAdd(&hist[len >> shift], 1);
     order[pos] = static_cast<uint32_t>(b) | (static_cast<uint32_t>(len) << 13);
   }
@@ -192,9 +194,9 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanParams p) {
     const int chunks = (len + kAttnQTile - 1) / kAttnQTile;
     const int li = t - base[lo];
     const int h = li / chunks, c = li - h * chunks;
-    p.items[t] = make_int2(p.cu[b], static_cast<int>((static_cast<uint32_t>(len) << 17) |
-                                                     (static_cast<uint32_t>(h) << 9) |
-                                                     static_cast<uint32_t>(c)));
+    p.items[t] = make_int2(s_cu[b], static_cast<int>((static_cast<uint32_t>(len) << 17) |
+                                                      (static_cast<uint32_t>(h) << 9) |
+                                                      static_cast<uint32_t>(c)));
   }
   if (tid == 0) write_header(p, n_items);
 }
@@ -675,11 +677,23 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16_kernel(AttnParams p) {
   __shared__ int2 s_raw[2];   // descriptor handed from thread 0 to the workgroup, by stage parity
   __shared__ int s_first;
 
+  const int tid = threadIdx.x;
+  // The first two descriptors are read before the plan header has arrived
+  // (any slot below the workspace's capacity is in bounds) and dropped below
+  // if they lie past the plan's item count.
+  const int t0 = blockIdx.x, t1 = blockIdx.x + static_cast<int>(gridDim.x);
+  int2 r0, r1;
+  r0.x = -1;
+  r0.y = 0;
+  r1 = r0;
+  if (tid == 0) {
+    if (t0 < p.max_items) r0 = p.items[t0];
+    if (t1 < p.max_items) r1 = p.items[t1];
+  }
   if (!plan_matches(p)) {
     if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(p.status, DORA_DEV_PLAN);
     return;
   }
-  const int tid = threadIdx.x;
   KernelCtx c{p, min(p.hdr->n_items, p.max_items), static_cast<int>(gridDim.x), static_cast<long long>(p.H) * kD,
               static_cast<uint32_t>(p.H) * kD * 2u, lds_offsets(), {}};
 #pragma unroll
@@ -694,15 +708,10 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16_kernel(AttnParams p) {
   Sched s;
   s.t_nn = 0;
   if (tid == 0) {
-    const int t0 = blockIdx.x, t1 = blockIdx.x + c.G;
     s.t_nn = blockIdx.x + 2 * c.G;
     s_first = t0;
-    int2 r0, r1;
-    r0.x = -1;
-    r0.y = 0;
-    r1 = r0;
-    if (t0 < c.n_items) r0 = p.items[t0];
-    if (t1 < c.n_items) r1 = p.items[t1];
+    if (t0 >= c.n_items) r0.x = -1;
+    if (t1 >= c.n_items) r1.x = -1;
     s_init[0] = r0;
     s_init[1] = r1;
   }
