@@ -32,7 +32,7 @@ __device__ __forceinline__ int lanes_below(uint64_t mask) {
 // ordered by decreasing sequence length.
 // ---------------------------------------------------------------------------
 constexpr int32_t kPlanMagic = 0x444F5241;  // "DORA"
-constexpr int kAttnQTile = 256;             // queries per work item (8 waves x 32)
+constexpr int kAttnQTile = 240;             // queries per work item (15 tiles of 16)
 constexpr int kPlanMaxB = 8192;             // sequences one plan can order
 
 struct AttnPlanHeader {

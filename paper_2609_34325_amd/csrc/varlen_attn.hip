@@ -43,7 +43,7 @@ constexpr int kD = 64;
 constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * 64;
 constexpr int kQPerWave = 32;
-static_assert(kWaves * kQPerWave == kAttnQTile, "tile size");
+static_assert(kWaves * kQPerWave >= kAttnQTile && kWaves * 2 * 16 >= kAttnQTile, "tile size");
 constexpr int kKRes = 256;             // keys resident in LDS per stage (bf16)
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanBins = 1024;
@@ -365,29 +365,46 @@ __device__ __forceinline__ bf16x4 v_column4(const char* p) {
 // the busy waves of a short sequence spread over all four SIMDs.
 __device__ __forceinline__ int tile_q(int wave, int j) { return (wave + kWaves * j) * 16; }
 
-// Queries of one chunk (qbase = its first row, nq >= 1 of them).  Lanes past
-// the end re-read the last query; their scores are computed and never stored.
-__device__ __forceinline__ void q_load(const char* qbase, int nq, uint32_t row_bytes, bf16x8 (&qn)[2][2]) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+// DMA of the queries of an item's chunk (rows [0, nq) from qbase, 1 <= nq <=
+// kAttnQTile) into the query buffer, swizzled like K.  Rows up to the end of
+// the last 64-row round are filled with copies of row nq-1 (never past the
+// buffer), so every query row a tile reads is finite.
+__device__ __forceinline__ void q_dma(const char* qbase, int nq, uint32_t row_bytes, uint16_t* Qd) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
   const uint32_t last = static_cast<uint32_t>(nq - 1);
+  const uint32_t chunk = static_cast<uint32_t>(((lane & 7) ^ (lane >> 3)) * 16);
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const uint32_t qi = min(static_cast<uint32_t>(tile_q(wave, j) + (lane & 15)), last);
-    const char* row = qbase + qi * row_bytes + (lane >> 4) * 16;
-    qn[j][0] = *reinterpret_cast<const bf16x8*>(row);
-    qn[j][1] = *reinterpret_cast<const bf16x8*>(row + 64);
+  for (int i = 0; i < (kAttnQTile + 63) / 64; ++i) {
+    const int row0 = i * 64 + wave * 8;
+    if (i * 64 < nq && row0 < kAttnQTile) {
+      const uint32_t off = min(static_cast<uint32_t>(row0 + (lane >> 3)), last) * row_bytes + chunk;
+      __builtin_amdgcn_global_load_lds(qbase + off, (lds_void*)(Qd + row0 * kD), 16, 0, 0);
+    }
   }
 }
 
-// The queries of an item's chunk; an empty item re-reads row 0 of head 0
-// (which exists whenever there is an item), so the load is unconditional.
-__device__ __forceinline__ void q_chunk_load(const AttnParams& p, const Item& it, long long row_elems,
-                                             uint32_t row_bytes, bf16x8 (&qn)[2][2]) {
+// The queries of an item's chunk into the query buffer (nothing for an empty item).
+__device__ __forceinline__ void q_chunk_dma(const AttnParams& p, const Item& it, long long row_elems,
+                                            uint32_t row_bytes, uint16_t* Qd) {
   const int q0 = it.chunk * kAttnQTile;
   const int nq = min(kAttnQTile, it.len - q0);
-  const long long row0 = nq > 0 ? static_cast<long long>(it.seq0) + q0 : 0;
-  const int h = nq > 0 ? it.h : 0;
-  q_load(head_base(p.q, row0, row_elems, h), max(nq, 1), row_bytes, qn);
+  if (nq > 0) q_dma(head_base(p.q, static_cast<long long>(it.seq0) + q0, row_elems, it.h), nq, row_bytes, Qd);
+}
+
+// B operands of the wave's query tiles from the query buffer: lane (c16, g)
+// holds query tile_q + c16, dims 8g..8g+7 (ks = 0) and 32+8g..32+8g+7 (ks = 1).
+__device__ __forceinline__ void q_read(const uint16_t* Qs, const LdsOffsets& lo, int nq, bf16x8 (&qf)[2][2]) {
+  const int wave = threadIdx.x >> 6;
+  const char* base = reinterpret_cast<const char*>(Qs);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    if (tile_q(wave, j) < nq) {
+      const char* t = base + tile_q(wave, j) * kRowBytes;
+      qf[j][0] = *reinterpret_cast<const bf16x8*>(t + lo.k0);
+      qf[j][1] = *reinterpret_cast<const bf16x8*>(t + lo.k1);
+    }
+  }
 }
 
 // S^T[key][query] for keys kb .. kb+63 of the staged block: 4 key tiles of 16
@@ -532,25 +549,49 @@ __device__ __forceinline__ void attend_stage(const LanePtrs& lp, int nk, bool fi
   }
 }
 
-// O = O^T / l for the wave's active query tiles (obase = first row of the chunk).
+// Output of a finished item, O = O^T / l rounded to bf16, in staging
+// registers that stay reserved until the wave's next output: a register an
+// in-flight store still reads must not be rewritten before the store
+// completes, so the stores never hold up the next stage's work.
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+struct OutStage {
+  u32x2 v[2][4];  // [tile][dt]: dims dt*16 + 4g .. +3 of the lane's query
+};
+
+__device__ __forceinline__ void keep_staged(const OutStage& st) {
+  asm volatile("" ::"v"(st.v[0][0]), "v"(st.v[0][1]), "v"(st.v[0][2]), "v"(st.v[0][3]), "v"(st.v[1][0]),
+               "v"(st.v[1][1]), "v"(st.v[1][2]), "v"(st.v[1][3]));
+}
+
+// Returns the number of store instructions issued (4 per tile): they are the
+// last vector-memory instructions of the stage, which the next stage-start
+// wait relies on.
 template <bool ACT1>
-__device__ __forceinline__ void store_out(char* obase, int nq, uint32_t row_bytes, const SoftmaxState& sm) {
+__device__ __forceinline__ int store_out(char* obase, int nq, uint32_t row_bytes, const SoftmaxState& sm,
+                                         OutStage& st) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  keep_staged(st);  // the previous output's stores have long completed
 #pragma unroll
   for (int j = 0; j < (ACT1 ? 2 : 1); ++j) {
     const float inv = __builtin_amdgcn_rcpf(sm.l[j][0]);
-    const int qi = tile_q(wave, j) + (lane & 15);
-    if (qi < nq) {
-      char* dst = obase + static_cast<uint32_t>(qi) * row_bytes + (lane >> 4) * 8;
 #pragma unroll
-      for (int dt = 0; dt < 4; ++dt) {
-        bf16x4 r;
+    for (int dt = 0; dt < 4; ++dt) {
+      bf16x4 r;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) r[i] = static_cast<__bf16>(sm.o[j][dt][i] * inv);
-        *reinterpret_cast<bf16x4*>(dst + dt * 32) = r;
-      }
+      for (int i = 0; i < 4; ++i) r[i] = static_cast<__bf16>(sm.o[j][dt][i] * inv);
+      st.v[j][dt] = __builtin_bit_cast(u32x2, r);
     }
   }
+#pragma unroll
+  for (int j = 0; j < (ACT1 ? 2 : 1); ++j) {
+    const int qi = tile_q(wave, j) + (lane & 15);
+    if (qi < nq) {  // lane c16 = 0 is always inside, so all 4 stores issue
+      char* dst = obase + static_cast<uint32_t>(qi) * row_bytes + (lane >> 4) * 8;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) *reinterpret_cast<u32x2*>(dst + dt * 32) = st.v[j][dt];
+    }
+  }
+  return ACT1 ? 8 : 4;
 }
 
 // Workgroup-uniform scheduling state of the execute loop.
@@ -560,6 +601,7 @@ struct Sched {
   bool shift;      // the previous stage finished `cur`
   int sb;          // stage (256-key block) of `cur`
   int t_nn;        // thread 0: ticket of the item after `nx`
+  int nst;         // output stores this wave issued at the end of the last stage
 };
 
 struct KernelCtx {
@@ -576,19 +618,22 @@ struct KernelCtx {
 // stage of the workgroup.
 template <int B>
 __device__ __forceinline__ bool attn_stage(const KernelCtx& c, Sched& s, const char* Kc, const char* Vc,
-                                           uint16_t* Kn, uint16_t* Vn, int2* s_raw, bf16x8 (&qn)[2][2],
-                                           bf16x8 (&qf)[2][2], SoftmaxState& sm) {
+                                           uint16_t* Kn, uint16_t* Vn, uint16_t* Qs, int2* s_raw,
+                                           bf16x8 (&qf)[2][2], SoftmaxState& sm, OutStage& ost) {
   const AttnParams& p = c.p;
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
-  // This stage's DMA (issued one stage ago) has landed for every wave, every
-  // wave is done with the other buffer, and the descriptor thread 0 published
-  // at the end of the previous stage is visible.  Only LDS needs ordering
-  // here, so the barrier does not wait for this wave's output stores.
-  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+  // Stage start.  vmcnt counts in issue order and the previous stage's output
+  // stores were this wave's last vector-memory instructions, so waiting until
+  // only those remain outstanding waits for this wave's DMA (K/V of this
+  // stage, queries of this item) without waiting for the stores.  After the
+  // barrier every wave's DMA has landed, every wave is done with the other
+  // buffer and thread 0's descriptor write is visible.  (The barrier is
+  // written out so that no LDS fence makes it wait for the DMA in flight.)
+  const int nst = __builtin_amdgcn_readfirstlane(s.nst);
+  if (nst == 8) asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  else if (nst == 4) asm volatile("s_waitcnt vmcnt(4) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   if (s.shift) {
     const int2 raw = uniform_raw(s_raw[1 - B]);
     const bool nn_valid = raw.x != -1;
@@ -606,11 +651,11 @@ __device__ __forceinline__ bool attn_stage(const KernelCtx& c, Sched& s, const c
   const bool act0 = tile_q(wave, 0) < nq;
   const bool act1 = tile_q(wave, 1) < nq;
   if (s.sb == 0) {
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      qf[j][0] = qn[j][0];
-      qf[j][1] = qn[j][1];
-    }
+    // The item's queries, then a barrier so the buffer can take the next
+    // item's queries.
+    q_read(Qs, c.lo, nq, qf);
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    if (s.nx_valid) q_chunk_dma(p, s.nx, c.row_elems, c.row_bytes, Qs);
   }
 
   // Next stage: the rest of this item's keys, or the next item.
@@ -625,11 +670,8 @@ __device__ __forceinline__ bool attn_stage(const KernelCtx& c, Sched& s, const c
              head_base(p.v, static_cast<long long>(kv_item.seq0) + kv_first, c.row_elems, kv_item.h), kv_n,
              c.row_bytes, Kn, Vn);
   }
-  // The next item's queries (harmlessly early, and again, while `cur` still
-  // has stages left: `qf` holds its copy).
-  q_chunk_load(p, s.nx_valid ? s.nx : Item{0, 0, 0, 0}, c.row_elems, c.row_bytes, qn);
-  // Queue traffic goes out after the prefetch; its results are only
-  // consumed at the end of the stage (no wait in between).
+  // Queue traffic goes out after the DMA; its results are consumed before
+  // the output stores.
   int2 raw_next;
   raw_next.x = -1;
   raw_next.y = 0;
@@ -640,20 +682,24 @@ __device__ __forceinline__ bool attn_stage(const KernelCtx& c, Sched& s, const c
   }
 
   if (act0) {
-    char* obase = const_cast<char*>(head_base(p.out, static_cast<long long>(cur.seq0) + q0, c.row_elems, cur.h));
     const LanePtrs lp = lane_ptrs(Kc, Vc, c.lo);
-    if (act1) {
-      attend_stage<true>(lp, nk, s.sb == 0, p.scale_log2, c.ones, qf, sm);
-      if (!more_keys) store_out<true>(obase, nq, c.row_bytes, sm);
-    } else {
-      attend_stage<false>(lp, nk, s.sb == 0, p.scale_log2, c.ones, qf, sm);
-      if (!more_keys) store_out<false>(obase, nq, c.row_bytes, sm);
-    }
+    if (act1) attend_stage<true>(lp, nk, s.sb == 0, p.scale_log2, c.ones, qf, sm);
+    else attend_stage<false>(lp, nk, s.sb == 0, p.scale_log2, c.ones, qf, sm);
   }
-
+  // Everything this stage loaded has arrived by now (the DMA went out before
+  // the compute); an explicit wait says so, so that no later instruction
+  // waits for it behind the output stores or the next DMA.
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
   if (tid == 0 && !more_keys) {
     s_raw[B] = raw_next;
     s.t_nn = t_got + 3 * c.G;
+  }
+  // The output goes last (nothing vector-memory may be issued after it).
+  asm volatile("" ::: "memory");
+  s.nst = 0;
+  if (act0 && !more_keys) {
+    char* obase = const_cast<char*>(head_base(p.out, static_cast<long long>(cur.seq0) + q0, c.row_elems, cur.h));
+    s.nst = act1 ? store_out<true>(obase, nq, c.row_bytes, sm, ost) : store_out<false>(obase, nq, c.row_bytes, sm, ost);
   }
   s.shift = !more_keys;
   if (more_keys) ++s.sb;
@@ -667,6 +713,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16_kernel(AttnParams p) {
   // block pay the extra adds instead.
   struct StageLds {
     uint16_t v0[kStageElems], v1[kStageElems], k0[kStageElems], k1[kStageElems];
+    uint16_t q[kAttnQTile * kD];  // queries of the current item, then of the next
   };
   __shared__ __attribute__((aligned(1024))) StageLds lds;
   uint16_t* const V0 = lds.v0;
@@ -726,22 +773,24 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16_kernel(AttnParams p) {
   s.nx = s.nx_valid ? decode_item(p, raw1) : Item{0, 0, 0, 0};
   s.shift = false;
   s.sb = 0;
+  s.nst = 0;
 
-  bf16x8 qn[2][2], qf[2][2];
+  bf16x8 qf[2][2];
   {
     const int nk = min(s.cur.len, kKRes);
     if (nk > 0)
       kv_dma(head_base(p.k, s.cur.seq0, c.row_elems, s.cur.h), head_base(p.v, s.cur.seq0, c.row_elems, s.cur.h), nk,
              c.row_bytes, K0, V0);
-    q_chunk_load(p, s.cur, c.row_elems, c.row_bytes, qn);
+    q_chunk_dma(p, s.cur, c.row_elems, c.row_bytes, lds.q);
   }
   SoftmaxState sm;
+  OutStage ost;
   for (;;) {
-    if (!attn_stage<0>(c, s, reinterpret_cast<const char*>(K0), reinterpret_cast<const char*>(V0), K1, V1, s_raw,
-                       qn, qf, sm))
+    if (!attn_stage<0>(c, s, reinterpret_cast<const char*>(K0), reinterpret_cast<const char*>(V0), K1, V1, lds.q,
+                       s_raw, qf, sm, ost))
       break;
-    if (!attn_stage<1>(c, s, reinterpret_cast<const char*>(K1), reinterpret_cast<const char*>(V1), K0, V0, s_raw,
-                       qn, qf, sm))
+    if (!attn_stage<1>(c, s, reinterpret_cast<const char*>(K1), reinterpret_cast<const char*>(V1), K0, V0, lds.q,
+                       s_raw, qf, sm, ost))
       break;
   }
   leave_queue(p.hdr);
@@ -789,7 +838,8 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_f32_kernel(AttnParams p) {
     const long long seq0 = it.seq0;
     const int len = it.len;
     const int q0 = it.chunk * kAttnQTile + wave * kQPerWave;
-    const bool active = q0 < len;
+    const int qend = min(len, (it.chunk + 1) * kAttnQTile);  // this item's queries end here
+    const bool active = q0 < qend;
 
     float qf[2][16];
 #pragma unroll
@@ -797,7 +847,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_f32_kernel(AttnParams p) {
       const int qi = q0 + 16 * j + c16;
 #pragma unroll
       for (int ks = 0; ks < 16; ++ks)
-        qf[j][ks] = qi < len ? Q[(seq0 + qi) * row_elems + it.h * kD + 4 * ks + g] : 0.f;
+        qf[j][ks] = qi < qend ? Q[(seq0 + qi) * row_elems + it.h * kD + 4 * ks + g] : 0.f;
     }
     floatx4 o[2][4];
 #pragma unroll
@@ -892,7 +942,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_f32_kernel(AttnParams p) {
         l += __shfl_xor(l, 32, 64);
         const float inv = 1.0f / l;
         const int qi = q0 + 16 * j + c16;
-        if (qi < len) {
+        if (qi < qend) {
           float* dst = O + (seq0 + qi) * row_elems + it.h * kD + 4 * g;
 #pragma unroll
           for (int dt = 0; dt < 4; ++dt)
