@@ -549,49 +549,50 @@ __device__ __forceinline__ void attend_stage(const LanePtrs& lp, int nk, bool fi
   }
 }
 
-// Output of a finished item, O = O^T / l rounded to bf16, in staging
-// registers that stay reserved until the wave's next output: a register an
-// in-flight store still reads must not be rewritten before the store
-// completes, so the stores never hold up the next stage's work.
+// O = O^T / l rounded to bf16 for the wave's active query tiles (tile 1 when
+// `act1`), obase = first row of the chunk.  Returns the number of store
+// instructions issued (2 per tile): they are the last vector-memory
+// instructions of the stage, which the next stage-start wait relies on.
+//
+// Lane (c16, g) holds dims 16 dt + 4g .. +3 of query c16.  One swap between
+// 16-lane rows g and g^1 (v_permlane16_swap) per pair (dt, dt+1) leaves each
+// lane with 8 consecutive dims, 8 * [0, 2, 1, 3][g] + 32 * pair .. +7, so a
+// store instruction writes 64 contiguous bytes of each of 16 rows rather than
+// 32 (half as many instructions, each touching half as many pieces of lines).
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-struct OutStage {
-  u32x2 v[2][4];  // [tile][dt]: dims dt*16 + 4g .. +3 of the lane's query
-};
-
-__device__ __forceinline__ void keep_staged(const OutStage& st) {
-  asm volatile("" ::"v"(st.v[0][0]), "v"(st.v[0][1]), "v"(st.v[0][2]), "v"(st.v[0][3]), "v"(st.v[1][0]),
-               "v"(st.v[1][1]), "v"(st.v[1][2]), "v"(st.v[1][3]));
-}
-
-// Returns the number of store instructions issued (4 per tile): they are the
-// last vector-memory instructions of the stage, which the next stage-start
-// wait relies on.
-template <bool ACT1>
 __device__ __forceinline__ int store_out(char* obase, int nq, uint32_t row_bytes, const SoftmaxState& sm,
-                                         OutStage& st) {
+                                         bool act1) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  keep_staged(st);  // the previous output's stores have long completed
+  const int g = lane >> 4;
+  const uint32_t chunk = static_cast<uint32_t>((((g & 1) << 1) | (g >> 1)) * 16);
 #pragma unroll
-  for (int j = 0; j < (ACT1 ? 2 : 1); ++j) {
+  for (int j = 0; j < 2; ++j) {
+    if (j == 1 && !act1) break;
     const float inv = __builtin_amdgcn_rcpf(sm.l[j][0]);
+    uint32_t r[4][2];
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) {
-      bf16x4 r;
+      bf16x4 x;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) r[i] = static_cast<__bf16>(sm.o[j][dt][i] * inv);
-      st.v[j][dt] = __builtin_bit_cast(u32x2, r);
+      for (int i = 0; i < 4; ++i) x[i] = static_cast<__bf16>(sm.o[j][dt][i] * inv);
+      r[dt][0] = __builtin_bit_cast(u32x2, x)[0];
+      r[dt][1] = __builtin_bit_cast(u32x2, x)[1];
     }
-  }
+    uint4 v[2];
 #pragma unroll
-  for (int j = 0; j < (ACT1 ? 2 : 1); ++j) {
+    for (int pr = 0; pr < 2; ++pr) {
+      const auto s0 = __builtin_amdgcn_permlane16_swap(r[2 * pr][0], r[2 * pr + 1][0], false, false);
+      const auto s1 = __builtin_amdgcn_permlane16_swap(r[2 * pr][1], r[2 * pr + 1][1], false, false);
+      v[pr] = make_uint4(s0[0], s1[0], s0[1], s1[1]);
+    }
     const int qi = tile_q(wave, j) + (lane & 15);
-    if (qi < nq) {  // lane c16 = 0 is always inside, so all 4 stores issue
-      char* dst = obase + static_cast<uint32_t>(qi) * row_bytes + (lane >> 4) * 8;
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt) *reinterpret_cast<u32x2*>(dst + dt * 32) = st.v[j][dt];
+    if (qi < nq) {  // lane c16 = 0 is always inside, so both stores issue
+      char* dst = obase + static_cast<uint32_t>(qi) * row_bytes + chunk;
+      *reinterpret_cast<uint4*>(dst) = v[0];
+      *reinterpret_cast<uint4*>(dst + 64) = v[1];
     }
   }
-  return ACT1 ? 8 : 4;
+  return act1 ? 4 : 2;
 }
 
 // Workgroup-uniform scheduling state of the execute loop.
@@ -619,7 +620,7 @@ struct KernelCtx {
 template <int B>
 __device__ __forceinline__ bool attn_stage(const KernelCtx& c, Sched& s, const char* Kc, const char* Vc,
                                            uint16_t* Kn, uint16_t* Vn, uint16_t* Qs, int2* s_raw,
-                                           bf16x8 (&qf)[2][2], SoftmaxState& sm, OutStage& ost) {
+                                           bf16x8 (&qf)[2][2], SoftmaxState& sm) {
   const AttnParams& p = c.p;
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
@@ -631,8 +632,8 @@ __device__ __forceinline__ bool attn_stage(const KernelCtx& c, Sched& s, const c
   // buffer and thread 0's descriptor write is visible.  (The barrier is
   // written out so that no LDS fence makes it wait for the DMA in flight.)
   const int nst = __builtin_amdgcn_readfirstlane(s.nst);
-  if (nst == 8) asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  else if (nst == 4) asm volatile("s_waitcnt vmcnt(4) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  if (nst == 4) asm volatile("s_waitcnt vmcnt(4) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  else if (nst == 2) asm volatile("s_waitcnt vmcnt(2) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   if (s.shift) {
     const int2 raw = uniform_raw(s_raw[1 - B]);
@@ -699,7 +700,7 @@ __device__ __forceinline__ bool attn_stage(const KernelCtx& c, Sched& s, const c
   s.nst = 0;
   if (act0 && !more_keys) {
     char* obase = const_cast<char*>(head_base(p.out, static_cast<long long>(cur.seq0) + q0, c.row_elems, cur.h));
-    s.nst = act1 ? store_out<true>(obase, nq, c.row_bytes, sm, ost) : store_out<false>(obase, nq, c.row_bytes, sm, ost);
+    s.nst = store_out(obase, nq, c.row_bytes, sm, act1);
   }
   s.shift = !more_keys;
   if (more_keys) ++s.sb;
@@ -784,13 +785,12 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16_kernel(AttnParams p) {
     q_chunk_dma(p, s.cur, c.row_elems, c.row_bytes, lds.q);
   }
   SoftmaxState sm;
-  OutStage ost;
   for (;;) {
     if (!attn_stage<0>(c, s, reinterpret_cast<const char*>(K0), reinterpret_cast<const char*>(V0), K1, V1, lds.q,
-                       s_raw, qf, sm, ost))
+                       s_raw, qf, sm))
       break;
     if (!attn_stage<1>(c, s, reinterpret_cast<const char*>(K1), reinterpret_cast<const char*>(V1), K0, V0, lds.q,
-                       s_raw, qf, sm, ost))
+                       s_raw, qf, sm))
       break;
   }
   leave_queue(p.hdr);
