@@ -24,7 +24,7 @@ __device__ __forceinline__ int lanes_below(uint64_t mask) {
 // ---------------------------------------------------------------------------
 // Attention work-queue workspace layout (device memory owned by the caller).
 //
-//   [0, 256)      AttnPlanHeader
+//   [0, 256)      AttnPlanHeader (queue counters, plan sizes, a row of zeros)
 //   [256, ...)    items[max_items]: int2 {x = first row of the sequence,
 //                 y = len << 17 | head << 9 | query chunk}
 //
@@ -42,9 +42,11 @@ struct AttnPlanHeader {
   int32_t magic;       // kPlanMagic once planned
   int32_t B, H, max_seqlen, q_tile;
   int64_t total;
-  int32_t reserved[6];
+  int32_t reserved[22];
+  uint32_t zero_row[32];  // one 128-byte row of zeros (bf16 V rows past a sequence's end)
 };
-static_assert(sizeof(AttnPlanHeader) <= 256, "header must fit its slot");
+static_assert(sizeof(AttnPlanHeader) == 256, "header must fill its slot");
+static_assert(__builtin_offsetof(AttnPlanHeader, zero_row) == 128, "zero row is the header's second half");
 
 struct AttnWorkspaceLayout {
   size_t items_off, bytes;

@@ -7,20 +7,20 @@
 // Work decomposition (persistent, queue-driven):
 //   plan     one workgroup validates cu_seqlens, orders the sequences by
 //            decreasing length (counting sort) and writes the item list
-//            (sequence, head, chunk of 256 queries), each item carrying its
-//            first row and length so the executing kernel needs no other
-//            lookup; it also resets the queue counters.
-//   execute  one 512-thread workgroup per compute unit takes item tickets from
-//            an atomic counter until the list is drained; the last workgroup
-//            to leave resets the counters so the plan can run again (e.g. for
-//            every layer between two pruning steps).
+//            (sequence, head, chunk of kAttnQTile queries), each item
+//            carrying its first row and length so the executing kernel needs
+//            no other lookup; it also resets the queue counters.
+//   execute  persistent workgroups, as many as fit on the device, take item
+//            tickets from an atomic counter until the list is drained; the
+//            last workgroup to leave resets the counters so the plan can run
+//            again (e.g. for every layer between two pruning steps).
 //
-// bf16 kernel, per work item: 8 waves x 2 tiles of 16 queries.  Up to 256
-// keys of K and V (both row-major) are resident in LDS per stage, so a
-// ViT-sized sequence is staged once.  While a stage computes, the next stage's K/V and
-// Q are already in flight into registers (register-staged double buffering),
-// and the queue ticket / item descriptor two items ahead are fetched too, so
-// the HBM traffic of item i+1 overlaps the MFMA work of item i.
+// bf16 kernel, per work item: each wave owns up to two 16-query tiles of the
+// chunk.  K and V (row-major) stream through LDS in stages of kKRes keys by
+// LDS DMA, double-buffered, so the transfer of the next stage (the rest of
+// this item, or the next item) overlaps the MFMA work of the current one; the
+// next item's queries also arrive in LDS by DMA, and the queue ticket and
+// descriptor of the item after it are fetched one stage ahead.
 //
 // V^T operands come from the transposing LDS read (ds_read_b64_tr_b16), so V
 // needs no transpose on its way into LDS.
@@ -45,6 +45,9 @@ constexpr int kThreads = kWaves * 64;
 constexpr int kQPerWave = 32;
 static_assert(kWaves * kQPerWave >= kAttnQTile && kWaves * 2 * 16 >= kAttnQTile, "tile size");
 constexpr int kKRes = 256;             // keys resident in LDS per stage (bf16)
+// Lane 0 of the last wave talks to the queue: the last wave holds the fewest
+// query tiles of an item, so the queue's latency lands where there is slack.
+constexpr int kQueueThread = kThreads - 64;
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanBins = 1024;
 constexpr float kLog2e = 1.4426950408889634f;
@@ -198,6 +201,7 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanParams p) {
                                                       (static_cast<uint32_t>(h) << 9) |
                                                       static_cast<uint32_t>(c)));
   }
+  if (tid < 32) p.hdr->zero_row[tid] = 0u;
   if (tid == 0) write_header(p, n_items);
 }
 
@@ -287,11 +291,13 @@ __device__ __forceinline__ const char* head_base(const void* X, long long row0, 
 }
 
 // Issues the DMA of rows [0, n) of one head's K and V (1 <= n <= 256) into
-// Kd / Vd.  Rows up to the next multiple of 64 are filled as well, with
-// copies of row n-1, so every row a key block reads holds finite data (those
-// keys are masked out of the softmax).
-__device__ __forceinline__ void kv_dma(const char* kbase, const char* vbase, int n, uint32_t row_bytes,
-                                       uint16_t* Kd, uint16_t* Vd) {
+// Kd / Vd.  Rows up to the next multiple of 64 are filled as well: K with
+// copies of row n-1 (their scores repeat a real score, so a block maximum
+// taken over them is still a maximum over real keys) and V with zeros read
+// from `zrow`, so those keys add nothing to the output; the denominators
+// leave them out separately.
+__device__ __forceinline__ void kv_dma(const char* kbase, const char* vbase, const char* zrow, int n,
+                                       uint32_t row_bytes, uint16_t* Kd, uint16_t* Vd) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
   const uint32_t last = static_cast<uint32_t>(n - 1);
@@ -300,9 +306,11 @@ __device__ __forceinline__ void kv_dma(const char* kbase, const char* vbase, int
   for (int i = 0; i < kKRes / 64; ++i) {
     if (i * 64 < n) {
       const int row0 = i * 64 + wave * 8;
-      const uint32_t off = min(static_cast<uint32_t>(row0 + (lane >> 3)), last) * row_bytes + chunk;
+      const uint32_t row = static_cast<uint32_t>(row0 + (lane >> 3));
+      const uint32_t off = min(row, last) * row_bytes + chunk;
       __builtin_amdgcn_global_load_lds(kbase + off, (lds_void*)(Kd + row0 * kD), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(vbase + off, (lds_void*)(Vd + row0 * kD), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(row <= last ? vbase + off : zrow + chunk, (lds_void*)(Vd + row0 * kD), 16,
+                                       0, 0);
     }
   }
 }
@@ -432,9 +440,22 @@ struct SoftmaxState {
   float m[2];       // running max, log2 units
 };
 
+// Maximum over the four 16-lane rows of the wave: lanes c, c+16, c+32 and
+// c+48 hold different keys of the same query column.  Two row swaps
+// (v_permlane16_swap, then v_permlane32_swap), no LDS round trip.
+__device__ __forceinline__ float row_group_max(float m) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+  m = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
 // Online softmax of one 64-key block followed by O^T += V^T P^T.  FIRST marks
 // an item's first block: the running max starts at the block max and the
-// accumulators start from zero.
+// accumulators start from zero.  In a partial block (kvalid < 64) the keys
+// past the end are copies of the last key, with zero V rows: they leave every
+// block maximum unchanged and add nothing to O, and the denominators skip
+// them (their row of the ones operand is zero).
 template <bool ACT1, bool FIRST>
 __device__ __forceinline__ void softmax_pv_block(const LanePtrs& lp, int kb, int kvalid, float scale_log2,
                                                  const bf16x8& ones, floatx4 (&s)[2][4],
@@ -442,18 +463,8 @@ __device__ __forceinline__ void softmax_pv_block(const LanePtrs& lp, int kb, int
   constexpr int kTiles = ACT1 ? 2 : 1;
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4;
-  if (kvalid < 64) {  // last, partial block: keys past the end get zero weight
-    const int lim = kvalid - 4 * g;
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const bool dead = kt * 16 + i >= lim;
-#pragma unroll
-        for (int j = 0; j < kTiles; ++j) s[j][kt][i] = dead ? -INFINITY : s[j][kt][i];
-      }
-  }
-  float mx[2];
+  // The lane's maximum over its 16 scores (raw units; the scale is positive).
+  float lm[2];
 #pragma unroll
   for (int j = 0; j < kTiles; ++j) {
     float m = fmaxf(fmaxf(s[j][0][0], s[j][0][1]), s[j][0][2]);
@@ -464,23 +475,23 @@ __device__ __forceinline__ void softmax_pv_block(const LanePtrs& lp, int kb, int
 #pragma unroll
       for (int i = i0; i < 4; ++i) m = fmaxf(m, s[j][kt][i]);
     }
-    m = fmaxf(m, __shfl_xor(m, 16, 64));
-    m = fmaxf(m, __shfl_xor(m, 32, 64));
-    mx[j] = m * scale_log2;
+    lm[j] = m;
   }
   if (FIRST) {
 #pragma unroll
-    for (int j = 0; j < kTiles; ++j) st.m[j] = mx[j];
+    for (int j = 0; j < kTiles; ++j) st.m[j] = row_group_max(lm[j]) * scale_log2;
   } else {
     // Lazy rescaling: the running max only moves when a block exceeds it by
     // more than 2^8, so most blocks skip the rescale and the unnormalised
-    // weights stay below 256.
-    bool grow = mx[0] > st.m[0] + 8.0f;
-    if (ACT1) grow = grow || mx[1] > st.m[1] + 8.0f;
+    // weights stay below 256.  Some lane's partial maximum exceeds the bound
+    // exactly when some query's block maximum does, so the cross-lane
+    // maximum is only taken on a rescale.
+    bool grow = lm[0] * scale_log2 > st.m[0] + 8.0f;
+    if (ACT1) grow = grow || lm[1] * scale_log2 > st.m[1] + 8.0f;
     if (__ballot(grow) != 0ull) {
 #pragma unroll
       for (int j = 0; j < kTiles; ++j) {
-        const float m_new = fmaxf(st.m[j], mx[j]);
+        const float m_new = fmaxf(st.m[j], row_group_max(lm[j]) * scale_log2);
         const float alpha = __builtin_amdgcn_exp2f(st.m[j] - m_new);
         st.m[j] = m_new;
 #pragma unroll
@@ -507,14 +518,13 @@ __device__ __forceinline__ void softmax_pv_block(const LanePtrs& lp, int kb, int
       }
   }
   // O^T[dim][query] += V^T[dim][key] P^T[key][query]; a block of ones times
-  // P^T accumulates the denominators (row sums of the bf16 weights).
+  // P^T accumulates the denominators (row sums of the bf16 weights).  In a
+  // partial block the ones stop at the last key: element e of step ks in
+  // lane group g stands for the key of P^T's element e.
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) {
     const bool init = FIRST && ks == 0;
-#pragma unroll
-    for (int j = 0; j < kTiles; ++j)
-      st.l[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[j][ks], init ? zero : st.l[j], 0, 0, 0);
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) {
       // A operand V^T: lane (c16, g) holds dim dt*16 + c16 at keys ks*32 + 4g + 0..3
@@ -526,6 +536,26 @@ __device__ __forceinline__ void softmax_pv_block(const LanePtrs& lp, int kb, int
       for (int j = 0; j < kTiles; ++j)
         st.o[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[j][ks], init ? zero : st.o[j][dt], 0, 0, 0);
     }
+  }
+  if (kvalid < 64) {
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      bf16x8 on;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int key = ks * 32 + (e < 4 ? 4 * g + e : 12 + 4 * g + e);
+        on[e] = key < kvalid ? ones[e] : static_cast<__bf16>(0.0f);
+      }
+#pragma unroll
+      for (int j = 0; j < kTiles; ++j)
+        st.l[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(on, pb[j][ks], FIRST && ks == 0 ? zero : st.l[j], 0, 0, 0);
+    }
+  } else {
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int j = 0; j < kTiles; ++j)
+        st.l[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[j][ks], FIRST && ks == 0 ? zero : st.l[j], 0, 0, 0);
   }
 }
 
@@ -601,7 +631,7 @@ struct Sched {
   bool nx_valid;
   bool shift;      // the previous stage finished `cur`
   int sb;          // stage (256-key block) of `cur`
-  int t_nn;        // thread 0: ticket of the item after `nx`
+  int t_nn;        // queue thread: ticket of the item after `nx`
   int nst;         // output stores this wave issued at the end of the last stage
 };
 
@@ -612,6 +642,7 @@ struct KernelCtx {
   uint32_t row_bytes;
   LdsOffsets lo;
   bf16x8 ones;
+  const char* zrow;  // 128 zero bytes in the workspace header
 };
 
 // One stage: compute `cur`'s keys [sb*256, sb*256 + 256) from buffer Kc/Vc
@@ -629,7 +660,7 @@ __device__ __forceinline__ bool attn_stage(const KernelCtx& c, Sched& s, const c
   // only those remain outstanding waits for this wave's DMA (K/V of this
   // stage, queries of this item) without waiting for the stores.  After the
   // barrier every wave's DMA has landed, every wave is done with the other
-  // buffer and thread 0's descriptor write is visible.  (The barrier is
+  // buffer and the queue thread's descriptor write is visible.  (The barrier is
   // written out so that no LDS fence makes it wait for the DMA in flight.)
   const int nst = __builtin_amdgcn_readfirstlane(s.nst);
   if (nst == 4) asm volatile("s_waitcnt vmcnt(4) lgkmcnt(0)\n\ts_barrier" ::: "memory");
@@ -668,7 +699,7 @@ __device__ __forceinline__ bool attn_stage(const KernelCtx& c, Sched& s, const c
     const int kv_n = min(kKRes, kv_item.len - kv_first);
     if (kv_n > 0)
       kv_dma(head_base(p.k, static_cast<long long>(kv_item.seq0) + kv_first, c.row_elems, kv_item.h),
-             head_base(p.v, static_cast<long long>(kv_item.seq0) + kv_first, c.row_elems, kv_item.h), kv_n,
+             head_base(p.v, static_cast<long long>(kv_item.seq0) + kv_first, c.row_elems, kv_item.h), c.zrow, kv_n,
              c.row_bytes, Kn, Vn);
   }
   // Queue traffic goes out after the DMA; its results are consumed before
@@ -677,7 +708,7 @@ __device__ __forceinline__ bool attn_stage(const KernelCtx& c, Sched& s, const c
   raw_next.x = -1;
   raw_next.y = 0;
   int t_got = 0;
-  if (tid == 0 && !more_keys) {
+  if (tid == kQueueThread && !more_keys) {
     if (s.t_nn < c.n_items) raw_next = p.items[s.t_nn];
     t_got = atomicAdd(&p.hdr->counter, 1);
   }
@@ -691,7 +722,7 @@ __device__ __forceinline__ bool attn_stage(const KernelCtx& c, Sched& s, const c
   // the compute); an explicit wait says so, so that no later instruction
   // waits for it behind the output stores or the next DMA.
   __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
-  if (tid == 0 && !more_keys) {
+  if (tid == kQueueThread && !more_keys) {
     s_raw[B] = raw_next;
     s.t_nn = t_got + 3 * c.G;
   }
@@ -722,7 +753,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16_kernel(AttnParams p) {
   uint16_t* const K0 = lds.k0;
   uint16_t* const K1 = lds.k1;
   __shared__ int2 s_init[2];  // the first two item descriptors
-  __shared__ int2 s_raw[2];   // descriptor handed from thread 0 to the workgroup, by stage parity
+  __shared__ int2 s_raw[2];   // descriptor handed from the queue thread to the workgroup, by stage parity
   __shared__ int s_first;
 
   const int tid = threadIdx.x;
@@ -743,20 +774,22 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16_kernel(AttnParams p) {
     return;
   }
   KernelCtx c{p, min(p.hdr->n_items, p.max_items), static_cast<int>(gridDim.x), static_cast<long long>(p.H) * kD,
-              static_cast<uint32_t>(p.H) * kD * 2u, lds_offsets(), {}};
+              static_cast<uint32_t>(p.H) * kD * 2u, lds_offsets(), {},
+              reinterpret_cast<const char*>(p.hdr->zero_row)};
 #pragma unroll
   for (int e = 0; e < 8; ++e) c.ones[e] = static_cast<__bf16>(1.0f);
 
   // Queue.  Tickets 0 .. 3G-1 are dealt statically (workgroup w takes w, w+G
   // and w+2G, the longest items), the rest come from the atomic counter, so
   // the start of the kernel is not a burst of atomics on one address.
-  // Thread 0 alone talks to the queue: it holds the ticket of the item after
-  // `nx`, loads that item's descriptor during a stage and publishes it in LDS
-  // at the end of the stage, so no wave waits on the queue mid-stage.
+  // One thread (kQueueThread) talks to the queue: it holds the ticket of the
+  // item after `nx`, loads that item's descriptor during a stage and
+  // publishes it in LDS at the end of the stage, so no wave waits on the
+  // queue mid-stage.
   Sched s;
   s.t_nn = 0;
+  if (tid == kQueueThread) s.t_nn = blockIdx.x + 2 * c.G;
   if (tid == 0) {
-    s.t_nn = blockIdx.x + 2 * c.G;
     s_first = t0;
     if (t0 >= c.n_items) r0.x = -1;
     if (t1 >= c.n_items) r1.x = -1;
@@ -780,8 +813,8 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16_kernel(AttnParams p) {
   {
     const int nk = min(s.cur.len, kKRes);
     if (nk > 0)
-      kv_dma(head_base(p.k, s.cur.seq0, c.row_elems, s.cur.h), head_base(p.v, s.cur.seq0, c.row_elems, s.cur.h), nk,
-             c.row_bytes, K0, V0);
+      kv_dma(head_base(p.k, s.cur.seq0, c.row_elems, s.cur.h), head_base(p.v, s.cur.seq0, c.row_elems, s.cur.h),
+             c.zrow, nk, c.row_bytes, K0, V0);
     q_chunk_dma(p, s.cur, c.row_elems, c.row_bytes, lds.q);
   }
   SoftmaxState sm;
