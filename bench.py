@@ -1,8 +1,9 @@
 """Benchmark of the DORA deployment hot path on one MI355X.
 
 One step = one pass of the whole path over one batch:
-    dora_select_pack  (top-k with CLS pinned + cu_seqlens + packed gather)
-    dora_varlen_attn_plan     (work queue for the packed layout)
+    dora_select_pack_plan     (top-k with CLS pinned + cu_seqlens + packed
+                               gather, and the attention work queue of the
+                               packed layout, in one launch)
     dora_varlen_attn_execute  (varlen attention, bf16 MFMA)
 on synthetic inputs already resident in HBM.  Prints one JSON line.
 
@@ -30,11 +31,17 @@ MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # dense matrix peaks, TFLOP/
 METRIC = "packed tokens/s + varlen-attn TFLOP/s (% MFMA peak), DeiT-B shape, B=256"
 
 
+def plan_items(w: W.Workload, keep: np.ndarray) -> int:
+    """Attention work items: one per (image, head, chunk of 240 queries)."""
+    return w.H * int(np.sum((keep.astype(np.int64) + 239) // 240))
+
+
 def select_pack_bytes(w: W.Workload, keep: np.ndarray, n_in: np.ndarray) -> int:
-    """Algorithmic HBM bytes of select/pack: read scores and keep, read and write
-    each kept row once, write the kept indices and cu_seqlens."""
+    """Algorithmic HBM bytes of select/pack with its attention plan: read scores
+    and keep, read and write each kept row once, write the kept indices,
+    cu_seqlens, the plan's items (8 bytes each) and its 256-byte header."""
     sk = int(keep.sum())
-    return 2 * sk * w.C * w.elt + 4 * (int(n_in.sum()) + sk + 2 * w.B + 1)
+    return 2 * sk * w.C * w.elt + 4 * (int(n_in.sum()) + sk + 2 * w.B + 1) + 8 * plan_items(w, keep) + 256
 
 
 def attn_flops(w: W.Workload, keep: np.ndarray) -> float:
@@ -240,16 +247,13 @@ def main() -> int:
     def step(ev=None):
         if ev is not None:
             ev[0].record(stream)
-        dora.dora_select_pack(scores, keep, tokens, idx_out=idx, cu_out=cu, packed_out=packed,
-                              cap_rows=sk, dev_status=st, stream=stream)
+        dora.dora_select_pack_plan(scores, keep, tokens, w.H, max_seqlen, sk, ws, idx_out=idx, cu_out=cu,
+                                   packed_out=packed, cap_rows=sk, dev_status=st, stream=stream)
         if ev is not None:
             ev[1].record(stream)
-        dora.dora_varlen_attn_plan(cu, w.H, max_seqlen, sk, ws, st, stream=stream)
-        if ev is not None:
-            ev[2].record(stream)
         dora.dora_varlen_attn_execute(q, k, v, cu, max_seqlen, ws, out=out, dev_status=st, stream=stream)
         if ev is not None:
-            ev[3].record(stream)
+            ev[2].record(stream)
 
     if args.calibrate_copy > 0:
         src = torch.ones(args.calibrate_copy * 2 ** 20, dtype=torch.uint8, device="cuda")
@@ -279,21 +283,20 @@ def main() -> int:
         t_end.record(stream)
         torch.cuda.synchronize()
         total_ms = t_start.elapsed_time(t_end)
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
         torch.cuda.synchronize()
         for i in range(args.steps):
             step(evs[i])
         torch.cuda.synchronize()
         sel = np.mean([e[0].elapsed_time(e[1]) for e in evs])
-        plan = np.mean([e[1].elapsed_time(e[2]) for e in evs])
-        attn = np.mean([e[2].elapsed_time(e[3]) for e in evs])
-        reps.append((total_ms / args.steps, sel, plan, attn))
+        attn = np.mean([e[1].elapsed_time(e[2]) for e in evs])
+        reps.append((total_ms / args.steps, sel, attn))
         print(f"[bench] repeat {rep}: {total_ms / args.steps * 1e3:.1f} us/step "
-              f"(per kernel with events: select_pack {sel * 1e3:.1f}, plan {plan * 1e3:.1f}, "
+              f"(per kernel with events: select_pack+plan {sel * 1e3:.1f}, "
               f"attention {attn * 1e3:.1f})", file=sys.stderr, flush=True)
     assert int(st.item()) == 0, f"device status {int(st.item())}"
     med = sorted(reps, key=lambda x: x[0])[len(reps) // 2]
-    ms_step, ms_sel, ms_plan, ms_attn = med
+    ms_step, ms_sel, ms_attn = med
 
     flops = attn_flops(w, r.keep)
     sp_bytes = select_pack_bytes(w, r.keep, r.n_in)
@@ -329,8 +332,7 @@ def main() -> int:
                                  "traffic": traffic.get("select_pack"), "algorithmic_bytes": sp_bytes},
         "select_pack_tokens_per_s": sk / (ms_sel * 1e-3),
         "attn_tflops": attn_tflops,
-        "us": {"select_pack": ms_sel * 1e3, "plan": ms_plan * 1e3, "attention": ms_attn * 1e3,
-               "step": ms_step * 1e3},
+        "us": {"select_pack_plan": ms_sel * 1e3, "attention": ms_attn * 1e3, "step": ms_step * 1e3},
         "repeats": args.repeats,
     }
     if not args.no_cpu_baseline:

@@ -145,6 +145,35 @@ int dora_varlen_attn_plan(const int32_t* cu_seqlens, int32_t B, int32_t H, int32
                           int32_t* dev_status, void* stream);
 
 /*
+ * dora_select_pack_plan -- dora_select_pack and, in the same launch, the
+ * attention plan of its packed output (Sec. 3.5 "Inference": the packed
+ * sequences are the kept tokens of each image, so sequence b has keep[b]
+ * rows starting at cu_out[b]).
+ *
+ * The select/pack arguments and results are those of dora_select_pack.  The
+ * plan written into `workspace` serves dora_varlen_attn_execute with
+ * cu_seqlens = cu_out and the same B, H, max_seqlen and total, exactly as a
+ * dora_varlen_attn_plan call on cu_out would (its items are ordered by
+ * decreasing keep count, then by image); the plan depends on the keep
+ * counts only, so it is built while the rows are copied instead of after.
+ *
+ *   H, max_seqlen, total  as for dora_varlen_attn_plan; total is the row
+ *              count of the Q/K/V buffers that execute will read.
+ *   workspace  device, 256-byte aligned, >= dora_varlen_attn_workspace_size
+ *              (B, H, max_seqlen) bytes.
+ *   dev_status the select/pack bits, plus DORA_DEV_CU_SEQLENS when some
+ *              keep[b] is outside [1, max_seqlen] or sum(keep) > total (the
+ *              plan is then empty and execute writes nothing).
+ *
+ * Returns DORA_OK or a negative dora_status; enqueues one kernel.
+ */
+int dora_select_pack_plan(const float* scores, const int32_t* keep, const void* tokens,
+                          const int32_t* cu_in, int64_t total_in, int32_t B, int32_t N, int32_t C,
+                          dora_dtype dtype, int32_t* idx_out, int32_t* cu_out, void* packed_out,
+                          int64_t cap_rows, int32_t H, int32_t max_seqlen, int64_t total,
+                          void* workspace, size_t workspace_bytes, int32_t* dev_status, void* stream);
+
+/*
  * dora_varlen_attn_execute -- exact softmax attention inside each packed
  * sequence (Sec. 3.5 "Inference"; App. E.5): for every sequence b and head h
  *   O_b,h = softmax(softmax_scale * Q_b,h K_b,h^T) V_b,h
@@ -157,9 +186,9 @@ int dora_varlen_attn_plan(const int32_t* cu_seqlens, int32_t B, int32_t H, int32
  *   dtype      DORA_BF16: bf16 inputs, fp32 accumulation and softmax, P rounded
  *              to bf16 for the P.V product, output rounded once to bf16.
  *              DORA_F32: fp32 throughout.
- *   workspace  as filled by dora_varlen_attn_plan with the same cu_seqlens,
- *              B, H, max_seqlen and total; otherwise DORA_DEV_PLAN is set and
- *              nothing is written.
+ *   workspace  as filled by dora_varlen_attn_plan (or dora_select_pack_plan)
+ *              with the same cu_seqlens, B, H, max_seqlen and total; otherwise
+ *              DORA_DEV_PLAN is set and nothing is written.
  * Execute calls that share one workspace must not overlap in time.
  */
 int dora_varlen_attn_execute(const void* q, const void* k, const void* v,

@@ -49,6 +49,7 @@ DORA_HEAD_DIM = 64
 
 EXPORTS = (
     "dora_select_pack",
+    "dora_select_pack_plan",
     "dora_varlen_attn_workspace_size",
     "dora_varlen_attn_plan",
     "dora_varlen_attn_execute",
@@ -79,6 +80,9 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.dora_select_pack.restype = ctypes.c_int
     lib.dora_select_pack.argtypes = [vp, vp, vp, vp, i64, i32, i32, i32, ctypes.c_int,
                                      vp, vp, vp, i64, vp, vp]
+    lib.dora_select_pack_plan.restype = ctypes.c_int
+    lib.dora_select_pack_plan.argtypes = lib.dora_select_pack.argtypes[:13] + [i32, i32, i64, vp, sz,
+                                                                               vp, vp]
     lib.dora_varlen_attn_workspace_size.restype = sz
     lib.dora_varlen_attn_workspace_size.argtypes = [i32, i32, i32]
     lib.dora_varlen_attn_plan.restype = ctypes.c_int
@@ -137,24 +141,7 @@ def new_status(device=None) -> torch.Tensor:
     return torch.zeros(1, dtype=torch.int32, device=device or "cuda")
 
 
-def dora_select_pack(scores: torch.Tensor, keep: torch.Tensor, tokens: torch.Tensor,
-                     cu_in: Optional[torch.Tensor] = None, N: Optional[int] = None,
-                     idx_out: Optional[torch.Tensor] = None,
-                     cu_out: Optional[torch.Tensor] = None,
-                     packed_out: Optional[torch.Tensor] = None,
-                     cap_rows: Optional[int] = None,
-                     dev_status: Optional[torch.Tensor] = None,
-                     stream=None) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor, torch.Tensor]:
-    """Keep CLS + the keep-1 highest keep-scores per image, pack the kept rows.
-
-    Dense input: scores [B,N] fp32, tokens [B,N,C].  Packed input (a cascaded
-    round): scores [total_in], tokens [total_in,C], cu_in [B+1] and N = an
-    upper bound on the segment lengths.  keep: int32 [B] (counts CLS).
-    Outputs (allocated if not given; capacity defaults to B*N rows so no
-    host synchronisation is needed): idx [cap], cu [B+1], packed [cap,C],
-    dev_status [1].  Returns (idx_out, cu_out, packed_out, dev_status).
-    """
-    lib = load_library()
+def _select_pack_args(scores, keep, tokens, cu_in, N, idx_out, cu_out, packed_out, cap_rows, dev_status):
     B = int(keep.shape[0])
     if cu_in is None:
         if tokens.dim() != 3:
@@ -190,15 +177,60 @@ def dora_select_pack(scores: torch.Tensor, keep: torch.Tensor, tokens: torch.Ten
         raise ValueError("packed_out must match the tokens' dtype and C")
     if int(idx_out.numel()) < cap_rows or int(packed_out.shape[0]) < cap_rows:
         raise ValueError("outputs smaller than cap_rows")
-    rc = lib.dora_select_pack(
-        _dev(scores, "scores", torch.float32), _dev(keep, "keep", torch.int32),
-        _dev(tokens, "tokens"), None if cu_in is None else _dev(cu_in, "cu_in", torch.int32),
-        total_in, B, int(N), C, _dtype_code(tokens),
-        _dev(idx_out, "idx_out", torch.int32), _dev(cu_out, "cu_out", torch.int32),
-        _dev(packed_out, "packed_out"), int(cap_rows), _dev(dev_status, "dev_status", torch.int32),
-        _stream(stream))
+    args = [_dev(scores, "scores", torch.float32), _dev(keep, "keep", torch.int32),
+            _dev(tokens, "tokens"), None if cu_in is None else _dev(cu_in, "cu_in", torch.int32),
+            total_in, B, int(N), C, _dtype_code(tokens),
+            _dev(idx_out, "idx_out", torch.int32), _dev(cu_out, "cu_out", torch.int32),
+            _dev(packed_out, "packed_out"), int(cap_rows)]
+    return args, (idx_out, cu_out, packed_out, dev_status)
+
+
+def dora_select_pack(scores: torch.Tensor, keep: torch.Tensor, tokens: torch.Tensor,
+                     cu_in: Optional[torch.Tensor] = None, N: Optional[int] = None,
+                     idx_out: Optional[torch.Tensor] = None,
+                     cu_out: Optional[torch.Tensor] = None,
+                     packed_out: Optional[torch.Tensor] = None,
+                     cap_rows: Optional[int] = None,
+                     dev_status: Optional[torch.Tensor] = None,
+                     stream=None) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor, torch.Tensor]:
+    """Keep CLS + the keep-1 highest keep-scores per image, pack the kept rows.
+
+    Dense input: scores [B,N] fp32, tokens [B,N,C].  Packed input (a cascaded
+    round): scores [total_in], tokens [total_in,C], cu_in [B+1] and N = an
+    upper bound on the segment lengths.  keep: int32 [B] (counts CLS).
+    Outputs (allocated if not given; capacity defaults to B*N rows so no
+    host synchronisation is needed): idx [cap], cu [B+1], packed [cap,C],
+    dev_status [1].  Returns (idx_out, cu_out, packed_out, dev_status).
+    """
+    lib = load_library()
+    args, outs = _select_pack_args(scores, keep, tokens, cu_in, N, idx_out, cu_out, packed_out,
+                                   cap_rows, dev_status)
+    rc = lib.dora_select_pack(*args, _dev(outs[3], "dev_status", torch.int32), _stream(stream))
     _check("dora_select_pack", rc)
-    return idx_out, cu_out, packed_out, dev_status
+    return outs
+
+
+def dora_select_pack_plan(scores: torch.Tensor, keep: torch.Tensor, tokens: torch.Tensor,
+                          H: int, max_seqlen: int, total: int, workspace: torch.Tensor,
+                          cu_in: Optional[torch.Tensor] = None, N: Optional[int] = None,
+                          idx_out: Optional[torch.Tensor] = None,
+                          cu_out: Optional[torch.Tensor] = None,
+                          packed_out: Optional[torch.Tensor] = None,
+                          cap_rows: Optional[int] = None,
+                          dev_status: Optional[torch.Tensor] = None,
+                          stream=None) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor, torch.Tensor]:
+    """dora_select_pack plus the attention plan of the packed output in `workspace`
+    (for dora_varlen_attn_execute with cu_seqlens = cu_out, H heads, max_seqlen
+    and total Q/K/V rows)."""
+    lib = load_library()
+    args, outs = _select_pack_args(scores, keep, tokens, cu_in, N, idx_out, cu_out, packed_out,
+                                   cap_rows, dev_status)
+    rc = lib.dora_select_pack_plan(*args, int(H), int(max_seqlen), int(total),
+                                   _dev(workspace, "workspace"),
+                                   workspace.numel() * workspace.element_size(),
+                                   _dev(outs[3], "dev_status", torch.int32), _stream(stream))
+    _check("dora_select_pack_plan", rc)
+    return outs
 
 
 def dora_varlen_attn_workspace_size(B: int, H: int, max_seqlen: int) -> int:

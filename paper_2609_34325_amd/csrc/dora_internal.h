@@ -63,4 +63,37 @@ inline AttnWorkspaceLayout attn_workspace_layout(int32_t B, int32_t H, int32_t m
   return L;
 }
 
+// Host-side range checks of the sizes a plan is made for.
+inline int check_attn_sizes(int32_t B, int32_t H, int32_t max_seqlen, int64_t total) {
+  if (B < 1 || B > kPlanMaxB || H < 1 || H > 256 || max_seqlen < 1 || max_seqlen > DORA_MAX_SEQLEN ||
+      total < 0 || total > 0x7FFFFFFF)
+    return DORA_ERR_SHAPE;
+  if (attn_workspace_layout(B, H, max_seqlen).max_items > 0x7FFFFFFF) return DORA_ERR_UNSUPPORTED;
+  return DORA_OK;
+}
+
+// Query chunks of a sequence of `len` tokens (len >= 0).
+__host__ __device__ __forceinline__ int attn_chunks(int len) { return (len + kAttnQTile - 1) / kAttnQTile; }
+
+// Item descriptor of chunk c of head h of the sequence at rows [seq0, seq0 + len).
+__device__ __forceinline__ int2 encode_item(int seq0, int len, int h, int c) {
+  return make_int2(seq0, static_cast<int>((static_cast<uint32_t>(len) << 17) | (static_cast<uint32_t>(h) << 9) |
+                                          static_cast<uint32_t>(c)));
+}
+
+// Header of a plan with n_items items (one thread); the zero row is written
+// separately.
+__device__ __forceinline__ void write_plan_header(AttnPlanHeader* hdr, int n_items, int32_t B, int32_t H,
+                                                  int32_t max_seqlen, int64_t total) {
+  hdr->n_items = n_items;
+  hdr->counter = 0;
+  hdr->exit_count = 0;
+  hdr->B = B;
+  hdr->H = H;
+  hdr->max_seqlen = max_seqlen;
+  hdr->q_tile = kAttnQTile;
+  hdr->total = total;
+  hdr->magic = kPlanMagic;
+}
+
 }  // namespace dora

@@ -14,6 +14,13 @@
 //                 ordered compaction of the keep flags with ballot + mbcnt.
 //   waves 1..3    sum keep[0..b) -> this image's output offset (cu_out[b]).
 //   all waves     16-byte row copies, 2 loads in flight per lane.
+//
+// dora_select_pack_plan also writes the attention work queue of the packed
+// output (Sec. 3.5 "Inference": one sequence per image, keep[b] rows): it
+// depends on the keep counts only, so workgroup (b, 0) places image b's
+// items while it sums the keep counts for its output offset (queue order:
+// longer sequences first, then lower image index), and workgroup (0, 0)
+// writes the plan header.
 #include <limits.h>
 #include <stdlib.h>
 
@@ -37,6 +44,11 @@ struct SelectPackParams {
   uint4* packed;
   int64_t cap_rows;
   int32_t* status;
+  // Attention plan of the packed output (plan_hdr == nullptr: none).
+  AttnPlanHeader* plan_hdr;
+  int2* plan_items;
+  int32_t H, max_seqlen, max_items;
+  int64_t plan_total;
 };
 
 // Order-preserving key: larger key = preferred for keeping.  -0 and +0 map
@@ -58,6 +70,10 @@ template <int SLOTS>
 __global__ __launch_bounds__(kThreads) void select_pack_kernel(SelectPackParams p) {
   __shared__ int32_t s_idx[SLOTS * 64];
   __shared__ long long s_part[kThreads / 64];
+  __shared__ long long s_before[kThreads / 64];  // plan items of the sequences ordered before b
+  __shared__ long long s_items[kThreads / 64];   // plan items of all sequences
+  __shared__ long long s_kept[kThreads / 64];    // sum of all keep counts
+  __shared__ int s_bad[kThreads / 64];           // some keep count outside [1, max_seqlen]
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -78,18 +94,50 @@ __global__ __launch_bounds__(kThreads) void select_pack_kernel(SelectPackParams 
     n = p.N;
   }
   const int kb = p.keep[b];
-  if (!seg_ok || kb < 1 || kb > n) {
-    if (s == 0 && tid == 0) atomicOr(p.status, seg_ok ? DORA_DEV_KEEP_RANGE : DORA_DEV_CU_IN);
-    return;
-  }
+  const bool img_ok = seg_ok && kb >= 1 && kb <= n;
+  // With a plan, workgroup (b, 0) writes image b's attention items and
+  // workgroup (0, 0) the plan header.
+  const bool plan_img = p.plan_hdr != nullptr && s == 0;
+  const bool plan_head = p.plan_hdr != nullptr && blockIdx.x == 0;
 
   if (wave != 0) {
-    // Output offset of image b: keep[0] + ... + keep[b-1].
-    long long part = 0;
-    for (int j = tid - 64; j < b; j += kThreads - 64) part += p.keep[j];
+    // Output offset of image b: keep[0] + ... + keep[b-1].  For the plan, the
+    // items of the sequences that precede b in the queue order (longer
+    // first, then lower index) give the position of b's first item.
+    long long part = 0, before = 0, items = 0, kept = 0;
+    int bad = 0;
+    const int jend = plan_img ? p.B : b;
+    for (int j = tid - 64; j < jend; j += kThreads - 64) {
+      const int kj = p.keep[j];
+      if (j < b) part += kj;
+      if (plan_img) {
+        const bool fits = kj >= 1 && kj <= p.max_seqlen;
+        const int cj = fits ? p.H * attn_chunks(kj) : 0;
+        if (kj > kb || (kj == kb && j < b)) before += cj;
+        if (plan_head) {
+          items += cj;
+          kept += kj;
+          bad |= !fits;
+        }
+      }
+    }
     part = wave_sum(part);
     if (lane == 0) s_part[wave] = part;
-  } else {
+    if (plan_img) {
+      before = wave_sum(before);
+      if (lane == 0) s_before[wave] = before;
+    }
+    if (plan_head) {
+      items = wave_sum(items);
+      kept = wave_sum(kept);
+      bad = __ballot(bad != 0) != 0ull;
+      if (lane == 0) {
+        s_items[wave] = items;
+        s_kept[wave] = kept;
+        s_bad[wave] = bad;
+      }
+    }
+  } else if (img_ok) {
     // Candidates are positions 1..n-1 (CLS, position 0, is not a candidate).
     // Position pos = r*64 + lane lives in key[r] of that lane.
     uint32_t key[SLOTS];
@@ -138,6 +186,29 @@ __global__ __launch_bounds__(kThreads) void select_pack_kernel(SelectPackParams 
   }
   __syncthreads();
   const long long off_out = s_part[1] + s_part[2] + s_part[3];
+
+  if (plan_img && kb >= 1 && kb <= p.max_seqlen) {
+    // Items (b, h, c) for head h and query chunk c, head-major.
+    const long long first = s_before[1] + s_before[2] + s_before[3];
+    const int ch = attn_chunks(kb);
+    for (int i = tid; i < p.H * ch; i += kThreads) {
+      const int h = i / ch;
+      if (first + i < p.max_items) p.plan_items[first + i] = encode_item(static_cast<int>(off_out), kb, h, i - h * ch);
+    }
+  }
+  if (plan_head) {
+    if (tid < 32) p.plan_hdr->zero_row[tid] = 0u;
+    if (tid == 0) {
+      const bool bad = s_bad[1] | s_bad[2] | s_bad[3] || s_kept[1] + s_kept[2] + s_kept[3] > p.plan_total;
+      if (bad) atomicOr(p.status, DORA_DEV_CU_SEQLENS);
+      write_plan_header(p.plan_hdr, bad ? 0 : static_cast<int>(s_items[1] + s_items[2] + s_items[3]), p.B, p.H,
+                        p.max_seqlen, p.plan_total);
+    }
+  }
+  if (!img_ok) {
+    if (s == 0 && tid == 0) atomicOr(p.status, seg_ok ? DORA_DEV_KEEP_RANGE : DORA_DEV_CU_IN);
+    return;
+  }
 
   if (s == 0) {
     if (tid == 0) {
@@ -206,6 +277,53 @@ int pick_split(int B, int N) {
   return split;
 }
 
+// Checks the arguments of a select/pack call and fills `p` (no plan).
+int prepare(const float* scores, const int32_t* keep, const void* tokens, const int32_t* cu_in, int64_t total_in,
+            int32_t B, int32_t N, int32_t C, dora_dtype dtype, int32_t* idx_out, int32_t* cu_out, void* packed_out,
+            int64_t cap_rows, int32_t* dev_status, SelectPackParams* p) {
+  if (!scores || !keep || !tokens || !idx_out || !cu_out || !packed_out || !dev_status) return DORA_ERR_NULL;
+  if (dtype != DORA_F32 && dtype != DORA_BF16) return DORA_ERR_DTYPE;
+  if (B < 1 || N < 1 || N > DORA_MAX_ROW_TOKENS || C < 1) return DORA_ERR_SHAPE;
+  if (cu_in != nullptr && total_in < 0) return DORA_ERR_SHAPE;
+  const int64_t row_bytes = static_cast<int64_t>(C) * (dtype == DORA_F32 ? 4 : 2);
+  if (row_bytes % 16 != 0) return DORA_ERR_ALIGN;
+  if (row_bytes > (int64_t(1) << 20)) return DORA_ERR_UNSUPPORTED;
+  if ((reinterpret_cast<uintptr_t>(tokens) | reinterpret_cast<uintptr_t>(packed_out)) & 15u) return DORA_ERR_ALIGN;
+  if (cap_rows < 1 || cap_rows > INT_MAX) return DORA_ERR_CAPACITY;
+
+  p->scores = scores;
+  p->keep = keep;
+  p->tokens = static_cast<const uint4*>(tokens);
+  p->cu_in = cu_in;
+  p->total_in = total_in;
+  p->B = B;
+  p->N = N;
+  p->row_vecs = static_cast<int32_t>(row_bytes / 16);
+  p->split = pick_split(B, N);
+  p->idx_out = idx_out;
+  p->cu_out = cu_out;
+  p->packed = static_cast<uint4*>(packed_out);
+  p->cap_rows = cap_rows;
+  p->status = dev_status;
+  p->plan_hdr = nullptr;
+  p->plan_items = nullptr;
+  p->H = p->max_seqlen = p->max_items = 0;
+  p->plan_total = 0;
+  return DORA_OK;
+}
+
+int launch_select_pack(const SelectPackParams& p, void* stream) {
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t err;
+  if (p.N <= 64) err = launch<1>(p, st);
+  else if (p.N <= 128) err = launch<2>(p, st);
+  else if (p.N <= 256) err = launch<4>(p, st);
+  else if (p.N <= 512) err = launch<8>(p, st);
+  else if (p.N <= 1024) err = launch<16>(p, st);
+  else err = launch<32>(p, st);
+  return err == hipSuccess ? DORA_OK : DORA_ERR_HIP;
+}
+
 }  // namespace
 }  // namespace dora
 
@@ -215,41 +333,34 @@ extern "C" int dora_select_pack(const float* scores, const int32_t* keep, const 
                                 void* packed_out, int64_t cap_rows, int32_t* dev_status,
                                 void* stream) {
   using namespace dora;
-  if (!scores || !keep || !tokens || !idx_out || !cu_out || !packed_out || !dev_status)
-    return DORA_ERR_NULL;
-  if (dtype != DORA_F32 && dtype != DORA_BF16) return DORA_ERR_DTYPE;
-  if (B < 1 || N < 1 || N > DORA_MAX_ROW_TOKENS || C < 1) return DORA_ERR_SHAPE;
-  if (cu_in != nullptr && total_in < 0) return DORA_ERR_SHAPE;
-  const int64_t row_bytes = static_cast<int64_t>(C) * (dtype == DORA_F32 ? 4 : 2);
-  if (row_bytes % 16 != 0) return DORA_ERR_ALIGN;
-  if (row_bytes > (int64_t(1) << 20)) return DORA_ERR_UNSUPPORTED;
-  if ((reinterpret_cast<uintptr_t>(tokens) | reinterpret_cast<uintptr_t>(packed_out)) & 15u)
-    return DORA_ERR_ALIGN;
-  if (cap_rows < 1 || cap_rows > INT_MAX) return DORA_ERR_CAPACITY;
-
   SelectPackParams p;
-  p.scores = scores;
-  p.keep = keep;
-  p.tokens = static_cast<const uint4*>(tokens);
-  p.cu_in = cu_in;
-  p.total_in = total_in;
-  p.B = B;
-  p.N = N;
-  p.row_vecs = static_cast<int32_t>(row_bytes / 16);
-  p.split = pick_split(B, N);
-  p.idx_out = idx_out;
-  p.cu_out = cu_out;
-  p.packed = static_cast<uint4*>(packed_out);
-  p.cap_rows = cap_rows;
-  p.status = dev_status;
+  const int rc = prepare(scores, keep, tokens, cu_in, total_in, B, N, C, dtype, idx_out, cu_out, packed_out,
+                         cap_rows, dev_status, &p);
+  if (rc != DORA_OK) return rc;
+  return launch_select_pack(p, stream);
+}
 
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  hipError_t err;
-  if (N <= 64) err = launch<1>(p, st);
-  else if (N <= 128) err = launch<2>(p, st);
-  else if (N <= 256) err = launch<4>(p, st);
-  else if (N <= 512) err = launch<8>(p, st);
-  else if (N <= 1024) err = launch<16>(p, st);
-  else err = launch<32>(p, st);
-  return err == hipSuccess ? DORA_OK : DORA_ERR_HIP;
+extern "C" int dora_select_pack_plan(const float* scores, const int32_t* keep, const void* tokens,
+                                     const int32_t* cu_in, int64_t total_in, int32_t B, int32_t N,
+                                     int32_t C, dora_dtype dtype, int32_t* idx_out, int32_t* cu_out,
+                                     void* packed_out, int64_t cap_rows, int32_t H, int32_t max_seqlen,
+                                     int64_t total, void* workspace, size_t workspace_bytes,
+                                     int32_t* dev_status, void* stream) {
+  using namespace dora;
+  SelectPackParams p;
+  int rc = prepare(scores, keep, tokens, cu_in, total_in, B, N, C, dtype, idx_out, cu_out, packed_out, cap_rows,
+                   dev_status, &p);
+  if (rc != DORA_OK) return rc;
+  rc = check_attn_sizes(B, H, max_seqlen, total);
+  if (rc != DORA_OK) return rc;
+  const AttnWorkspaceLayout L = attn_workspace_layout(B, H, max_seqlen);
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) || workspace_bytes < L.bytes)
+    return DORA_ERR_WORKSPACE;
+  p.plan_hdr = static_cast<AttnPlanHeader*>(workspace);
+  p.plan_items = reinterpret_cast<int2*>(static_cast<char*>(workspace) + L.items_off);
+  p.H = H;
+  p.max_seqlen = max_seqlen;
+  p.max_items = static_cast<int32_t>(L.max_items);
+  p.plan_total = total;
+  return launch_select_pack(p, stream);
 }

@@ -107,18 +107,6 @@ __device__ int block_exclusive_scan(int v, int* wave_sums, int* total) {
   return r;
 }
 
-__device__ __forceinline__ void write_header(const PlanParams& p, int n_items) {
-  p.hdr->n_items = n_items;
-  p.hdr->counter = 0;
-  p.hdr->exit_count = 0;
-  p.hdr->B = p.B;
-  p.hdr->H = p.H;
-  p.hdr->max_seqlen = p.max_seqlen;
-  p.hdr->q_tile = kAttnQTile;
-  p.hdr->total = p.total;
-  p.hdr->magic = kPlanMagic;
-}
-
 __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanParams p) {
   __shared__ int32_t s_cu[kPlanMaxB + 1];  // cu_seqlens, read from global memory once
   __shared__ int hist[kPlanBins];
@@ -144,7 +132,7 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanParams p) {
   if (s_bad) {
     if (tid == 0) {
       atomicOr(p.status, DORA_DEV_CU_SEQLENS);
-      write_header(p, 0);
+      write_plan_header(p.hdr, 0, p.B, p.H, p.max_seqlen, p.total);
     }
     return;
   }
@@ -169,7 +157,7 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanParams p) {
   int local = 0;
   for (int i = 0; i < per; ++i) {
     const int pos = tid * per + i;
-    if (pos < p.B) local += p.H * static_cast<int>(((order[pos] >> 13) + kAttnQTile - 1) / kAttnQTile);
+    if (pos < p.B) local += p.H * attn_chunks(static_cast<int>(order[pos] >> 13));
   }
   int n_items;
   int run = block_exclusive_scan(local, wave_sums, &n_items);
@@ -177,7 +165,7 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanParams p) {
     const int pos = tid * per + i;
     if (pos < p.B) {
       base[pos] = run;
-      run += p.H * static_cast<int>(((order[pos] >> 13) + kAttnQTile - 1) / kAttnQTile);
+      run += p.H * attn_chunks(static_cast<int>(order[pos] >> 13));
     }
   }
   if (tid == 0) base[p.B] = n_items;
@@ -194,15 +182,13 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanParams p) {
     const uint32_t o = order[lo];
     const int b = static_cast<int>(o & 0x1FFFu);
     const int len = static_cast<int>(o >> 13);
-    const int chunks = (len + kAttnQTile - 1) / kAttnQTile;
+    const int chunks = attn_chunks(len);
     const int li = t - base[lo];
     const int h = li / chunks, c = li - h * chunks;
-    p.items[t] = make_int2(s_cu[b], static_cast<int>((static_cast<uint32_t>(len) << 17) |
-                                                      (static_cast<uint32_t>(h) << 9) |
-                                                      static_cast<uint32_t>(c)));
+    p.items[t] = encode_item(s_cu[b], len, h, c);
   }
   if (tid < 32) p.hdr->zero_row[tid] = 0u;
-  if (tid == 0) write_header(p, n_items);
+  if (tid == 0) write_plan_header(p.hdr, n_items, p.B, p.H, p.max_seqlen, p.total);
 }
 
 // ------------------------------ execute -----------------------------------
@@ -1003,15 +989,6 @@ int persistent_grid(KernelT kernel, int slot, int* grid) {
     per_cu_cache[dev][slot] = per_cu;
   }
   *grid = cus * per_cu_cache[dev][slot];
-  return DORA_OK;
-}
-
-int check_attn_sizes(int32_t B, int32_t H, int32_t max_seqlen, int64_t total) {
-  if (B < 1 || B > kPlanMaxB || H < 1 || H > 256 || max_seqlen < 1 || max_seqlen > DORA_MAX_SEQLEN ||
-      total < 0 || total > INT_MAX)
-    return DORA_ERR_SHAPE;
-  const AttnWorkspaceLayout L = attn_workspace_layout(B, H, max_seqlen);
-  if (L.max_items > INT_MAX) return DORA_ERR_UNSUPPORTED;
   return DORA_OK;
 }
 

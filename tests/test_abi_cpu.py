@@ -72,6 +72,36 @@ def test_select_pack_host_validation():
     assert call_select(lib, cu_in=FAKE, total_in=-1) == dora.DORA_ERR_SHAPE
 
 
+def call_select_plan(lib, **kw):
+    ws = dora.dora_varlen_attn_workspace_size(4, 3, 197)
+    a = dict(scores=FAKE, keep=FAKE, tokens=FAKE, cu_in=None, total_in=0, B=4, N=197, C=768, dtype=1,
+             idx=FAKE, cu=FAKE, packed=FAKE, cap=100, H=3, max_seqlen=197, total=100, ws=FAKE, ws_bytes=ws,
+             status=FAKE, stream=None)
+    a.update(kw)
+    return lib.dora_select_pack_plan(a["scores"], a["keep"], a["tokens"], a["cu_in"], a["total_in"], a["B"],
+                                     a["N"], a["C"], a["dtype"], a["idx"], a["cu"], a["packed"], a["cap"],
+                                     a["H"], a["max_seqlen"], a["total"], a["ws"], a["ws_bytes"],
+                                     a["status"], a["stream"])
+
+
+def test_select_pack_plan_host_validation():
+    """The fused call checks both argument sets before anything is enqueued."""
+    lib = dora.load_library()
+    assert call_select_plan(lib, scores=None) == dora.DORA_ERR_NULL
+    assert call_select_plan(lib, C=3) == dora.DORA_ERR_ALIGN
+    assert call_select_plan(lib, cap=0) == dora.DORA_ERR_CAPACITY
+    assert call_select_plan(lib, H=0) == dora.DORA_ERR_SHAPE
+    assert call_select_plan(lib, H=257) == dora.DORA_ERR_SHAPE
+    assert call_select_plan(lib, max_seqlen=0) == dora.DORA_ERR_SHAPE
+    assert call_select_plan(lib, max_seqlen=dora.DORA_MAX_SEQLEN + 1) == dora.DORA_ERR_SHAPE
+    assert call_select_plan(lib, total=-1) == dora.DORA_ERR_SHAPE
+    assert call_select_plan(lib, B=8193, cap=100) == dora.DORA_ERR_SHAPE
+    assert call_select_plan(lib, ws=None) == dora.DORA_ERR_WORKSPACE
+    assert call_select_plan(lib, ws=FAKE + 16) == dora.DORA_ERR_WORKSPACE
+    ws = dora.dora_varlen_attn_workspace_size(4, 3, 197)
+    assert call_select_plan(lib, ws_bytes=ws - 1) == dora.DORA_ERR_WORKSPACE
+
+
 def test_workspace_size():
     assert dora.dora_varlen_attn_workspace_size(256, 12, 197) > 0
     assert dora.dora_varlen_attn_workspace_size(0, 12, 197) == 0
