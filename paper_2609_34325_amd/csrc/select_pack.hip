@@ -251,9 +251,12 @@ __global__ __launch_bounds__(kThreads) void select_pack_kernel(SelectPackParams 
         ++row;
       }
     }
+    // One wait for both loads, so no store waits behind another store's
+    // write-through (the compiler does not see the stores; see store_through).
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
 #pragma unroll
     for (int u = 0; u < kCopyUnroll; ++u)
-      if (dst[u] >= 0) p.packed[dst[u]] = buf[u];
+      if (dst[u] >= 0) store_through(p.packed + dst[u], u32x4{buf[u].x, buf[u].y, buf[u].z, buf[u].w});
   }
 }
 

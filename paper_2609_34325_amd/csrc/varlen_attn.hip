@@ -594,18 +594,18 @@ __device__ __forceinline__ int store_out(char* obase, int nq, uint32_t row_bytes
       r[dt][0] = __builtin_bit_cast(u32x2, x)[0];
       r[dt][1] = __builtin_bit_cast(u32x2, x)[1];
     }
-    uint4 v[2];
+    u32x4 v[2];
 #pragma unroll
     for (int pr = 0; pr < 2; ++pr) {
       const auto s0 = __builtin_amdgcn_permlane16_swap(r[2 * pr][0], r[2 * pr + 1][0], false, false);
       const auto s1 = __builtin_amdgcn_permlane16_swap(r[2 * pr][1], r[2 * pr + 1][1], false, false);
-      v[pr] = make_uint4(s0[0], s1[0], s0[1], s1[1]);
+      v[pr] = u32x4{s0[0], s1[0], s0[1], s1[1]};
     }
     const int qi = tile_q(wave, j) + (lane & 15);
     if (qi < nq) {  // lane c16 = 0 is always inside, so both stores issue
       char* dst = obase + static_cast<uint32_t>(qi) * row_bytes + chunk;
-      *reinterpret_cast<uint4*>(dst) = v[0];
-      *reinterpret_cast<uint4*>(dst + 64) = v[1];
+      store_through(dst, v[0]);
+      store_through(dst + 64, v[1]);
     }
   }
   return act1 ? 4 : 2;
