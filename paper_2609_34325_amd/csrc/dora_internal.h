@@ -15,17 +15,18 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 // Number of compute units of the current device (cached per device id).
 int device_cu_count(int* device_out);
 
-// 16-byte global store at system scope (sc1): it is written through the L2,
-// so the line is not left dirty there and the end of the kernel does not wait
-// for the L2 to write its output back (a bulk output written with plain
-// stores leaves up to the L2's capacity dirty, several microseconds of
-// write-back after the last workgroup ends).  No builtin sets this bit on a
-// global store, hence the assembly.  The compiler does not count the store in
-// its vmcnt bookkeeping; vmcnt still counts it, so a compiler wait for a
-// later load may also wait for this store (never the reverse).
+// 16-byte global store at system scope (sc1), non-temporal (nt): it is
+// written through the L2 and does not stay there, so the line is not left
+// dirty (a bulk output written with plain stores leaves up to the L2's
+// capacity dirty: several microseconds of write-back after the last
+// workgroup ends) and the output does not push the inputs still to be read
+// out of the caches.  No builtin sets these bits on a global store, hence the
+// assembly.  The compiler does not count the store in its vmcnt bookkeeping;
+// vmcnt still counts it, so a compiler wait for a later load may also wait
+// for this store (never the reverse).
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ void store_through(void* p, u32x4 v) {
-  asm volatile("global_store_dwordx4 %0, %1, off sc1" ::"v"(p), "v"(v) : "memory");
+  asm volatile("global_store_dwordx4 %0, %1, off sc1 nt" ::"v"(p), "v"(v) : "memory");
 }
 
 // Wave64 helpers.
