@@ -307,6 +307,22 @@ def main() -> int:
 
     traffic = load_traffic(args.traffic_json, w.name)
 
+    # The attention roofline is the lower of the two ceilings at its
+    # arithmetic intensity (flops per algorithmic byte): below the ridge point
+    # (peak flops / peak bandwidth) the kernel is bound by HBM.
+    intensity = flops / a_bytes
+    attn_gbs = a_bytes / (ms_attn * 1e-3) / 1e9
+    kname = "attn_fwd_bf16_kernel" if w.dtype == "bf16" else "attn_fwd_f32_kernel"
+    common = {"kernel": kname, "traffic": traffic.get("attn"), "algorithmic_bytes": a_bytes, "flops": flops,
+              "intensity_flop_per_byte": intensity, "ridge_flop_per_byte": peak * 1e3 / HBM_PEAK_GBS,
+              "tflops": attn_tflops, "mfma_peak_tflops": peak, "mfma_frac": attn_tflops / peak}
+    if intensity < peak * 1e3 / HBM_PEAK_GBS:
+        attn_roofline = {"bound": "hbm", "achieved": attn_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": attn_gbs / HBM_PEAK_GBS, **common}
+    else:
+        attn_roofline = {"bound": "mfma", "achieved": attn_tflops, "peak": peak, "unit": "TFLOP/s",
+                         "frac": attn_tflops / peak, **common}
+
     result = {
         "metric": METRIC,
         "value": sk / (ms_step * 1e-3),
@@ -323,10 +339,7 @@ def main() -> int:
         "config": {"workload": w.name, "B": w.B, "N": w.N, "H": w.H, "head_dim": W.HEAD_DIM, "C": w.C,
                    "sum_keep": sk, "sum_keep_sq": int(np.sum(r.keep.astype(np.int64) ** 2)),
                    "max_seqlen": max_seqlen},
-        "roofline": {"bound": "mfma", "kernel": "attn_fwd_bf16_kernel" if w.dtype == "bf16" else "attn_fwd_f32_kernel",
-                     "achieved": attn_tflops, "peak": peak, "unit": "TFLOP/s", "frac": attn_tflops / peak,
-                     "traffic": traffic.get("attn"), "algorithmic_bytes": a_bytes,
-                     "hbm_bound_tflops": flops / (a_bytes / (HBM_PEAK_GBS * 1e9)) / 1e12},
+        "roofline": attn_roofline,
         "roofline_select_pack": {"bound": "hbm", "kernel": "select_pack_kernel", "achieved": sp_gbs,
                                  "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": sp_gbs / HBM_PEAK_GBS,
                                  "traffic": traffic.get("select_pack"), "algorithmic_bytes": sp_bytes},
