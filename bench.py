@@ -39,9 +39,9 @@ def plan_items(w: W.Workload, keep: np.ndarray) -> int:
 def select_pack_bytes(w: W.Workload, keep: np.ndarray, n_in: np.ndarray) -> int:
     """Algorithmic HBM bytes of select/pack with its attention plan: read scores
     and keep, read and write each kept row once, write the kept indices,
-    cu_seqlens, the plan's items (8 bytes each) and its 256-byte header."""
+    cu_seqlens, the plan's items (8 bytes each) and its 2 KB header."""
     sk = int(keep.sum())
-    return 2 * sk * w.C * w.elt + 4 * (int(n_in.sum()) + sk + 2 * w.B + 1) + 8 * plan_items(w, keep) + 256
+    return 2 * sk * w.C * w.elt + 4 * (int(n_in.sum()) + sk + 2 * w.B + 1) + 8 * plan_items(w, keep) + 2048
 
 
 def attn_flops(w: W.Workload, keep: np.ndarray) -> float:

@@ -38,19 +38,29 @@ __device__ __forceinline__ int lanes_below(uint64_t mask) {
 // ---------------------------------------------------------------------------
 // Attention work-queue workspace layout (device memory owned by the caller).
 //
-//   [0, 256)      AttnPlanHeader (queue counters, plan sizes, a row of zeros)
-//   [256, ...)    items[max_items]: int2 {x = first row of the sequence,
+//   [0, 2048)     AttnPlanHeader (plan sizes, exit counter, a row of zeros,
+//                 one ticket counter per sub-queue, each on its own 128-byte
+//                 line)
+//   [2048, ...)   items[max_items]: int2 {x = first row of the sequence,
 //                 y = len << 17 | head << 9 | query chunk}
 //
 // A work item is one (sequence, head, chunk of kAttnQTile queries); items are
-// ordered by decreasing sequence length.
+// ordered by decreasing sequence length.  Item i belongs to sub-queue
+// i % kSubQueues, so each sub-queue is itself longest-first and the
+// sub-queues carry near-equal work.
 // ---------------------------------------------------------------------------
 constexpr int32_t kPlanMagic = 0x444F5241;  // "DORA"
 constexpr int kAttnQTile = 240;             // queries per work item (15 tiles of 16)
 constexpr int kPlanMaxB = 8192;             // sequences one plan can order
+constexpr int kSubQueues = 8;               // ticket counters (one per XCD of an MI355X)
+
+struct AttnQueueLine {
+  int32_t ticket;  // next dynamic ticket of the sub-queue
+  int32_t pad[31];
+};
 
 struct AttnPlanHeader {
-  int32_t counter;     // next ticket of the dynamic queue
+  int32_t unused;
   int32_t exit_count;  // workgroups that have left the current execute
   int32_t n_items;     // items in this plan
   int32_t magic;       // kPlanMagic once planned
@@ -58,9 +68,12 @@ struct AttnPlanHeader {
   int64_t total;
   int32_t reserved[22];
   uint32_t zero_row[32];  // one 128-byte row of zeros (bf16 V rows past a sequence's end)
+  AttnQueueLine queue[kSubQueues];
+  int32_t reserved2[192];
 };
-static_assert(sizeof(AttnPlanHeader) == 256, "header must fill its slot");
-static_assert(__builtin_offsetof(AttnPlanHeader, zero_row) == 128, "zero row is the header's second half");
+static_assert(sizeof(AttnPlanHeader) == 2048, "header must fill its slot");
+static_assert(__builtin_offsetof(AttnPlanHeader, zero_row) == 128, "zero row is the header's second line");
+static_assert(__builtin_offsetof(AttnPlanHeader, queue) == 256, "queue counters start on a line of their own");
 
 struct AttnWorkspaceLayout {
   size_t items_off, bytes;
@@ -71,7 +84,7 @@ inline AttnWorkspaceLayout attn_workspace_layout(int32_t B, int32_t H, int32_t m
   AttnWorkspaceLayout L;
   const int64_t chunks = (static_cast<int64_t>(max_seqlen) + kAttnQTile - 1) / kAttnQTile;
   L.max_items = static_cast<int64_t>(B) * H * chunks;
-  L.items_off = 256;
+  L.items_off = sizeof(AttnPlanHeader);
   L.bytes = L.items_off + static_cast<size_t>(L.max_items) * 8;
   L.bytes = (L.bytes + 255) & ~size_t(255);
   return L;
@@ -100,7 +113,7 @@ __device__ __forceinline__ int2 encode_item(int seq0, int len, int h, int c) {
 __device__ __forceinline__ void write_plan_header(AttnPlanHeader* hdr, int n_items, int32_t B, int32_t H,
                                                   int32_t max_seqlen, int64_t total) {
   hdr->n_items = n_items;
-  hdr->counter = 0;
+  for (int q = 0; q < kSubQueues; ++q) hdr->queue[q].ticket = 0;
   hdr->exit_count = 0;
   hdr->B = B;
   hdr->H = H;

@@ -42,8 +42,12 @@ namespace {
 constexpr int kD = 64;
 constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * 64;
-constexpr int kQPerWave = 32;
-static_assert(kWaves * kQPerWave >= kAttnQTile && kWaves * 2 * 16 >= kAttnQTile, "tile size");
+constexpr int kTilesPerWave = 2;  // 16-query tiles per wave (1 or 2)
+static_assert(kTilesPerWave == 1 || kTilesPerWave == 2, "tiles per wave");
+static_assert(kWaves * kTilesPerWave * 16 >= kAttnQTile && kAttnQTile % 16 == 0, "tile size");
+constexpr int kF32Waves = 8;  // fp32 kernel: 8 waves x 32 queries
+constexpr int kF32Threads = kF32Waves * 64;
+static_assert(kF32Waves * 32 >= kAttnQTile, "fp32 tile size");
 constexpr int kKRes = 256;             // keys resident in LDS per stage (bf16)
 // Lane 0 of the last wave talks to the queue: the last wave holds the fewest
 // query tiles of an item, so the queue's latency lands where there is slack.
@@ -242,7 +246,7 @@ __device__ __forceinline__ void leave_queue(AttnPlanHeader* hdr) {
     __threadfence();
     const int done = atomicAdd(&hdr->exit_count, 1);
     if (done == static_cast<int>(gridDim.x) - 1) {
-      atomicExch(&hdr->counter, 0);
+      for (int q = 0; q < kSubQueues; ++q) atomicExch(&hdr->queue[q].ticket, 0);
       atomicExch(&hdr->exit_count, 0);
     }
   }
@@ -288,10 +292,12 @@ __device__ __forceinline__ void kv_dma(const char* kbase, const char* vbase, con
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
   const uint32_t last = static_cast<uint32_t>(n - 1);
   const uint32_t chunk = static_cast<uint32_t>(((lane & 7) ^ (lane >> 3)) * 16);
+  const int n64 = (n + 63) & ~63;
+  // Instruction i (8 rows) goes to wave i % kWaves.
 #pragma unroll
-  for (int i = 0; i < kKRes / 64; ++i) {
-    if (i * 64 < n) {
-      const int row0 = i * 64 + wave * 8;
+  for (int r = 0; r < (kKRes / 8 + kWaves - 1) / kWaves; ++r) {
+    const int row0 = (r * kWaves + wave) * 8;
+    if (row0 < n64) {
       const uint32_t row = static_cast<uint32_t>(row0 + (lane >> 3));
       const uint32_t off = min(row, last) * row_bytes + chunk;
       __builtin_amdgcn_global_load_lds(kbase + off, (lds_void*)(Kd + row0 * kD), 16, 0, 0);
@@ -361,17 +367,18 @@ __device__ __forceinline__ int tile_q(int wave, int j) { return (wave + kWaves *
 
 // DMA of the queries of an item's chunk (rows [0, nq) from qbase, 1 <= nq <=
 // kAttnQTile) into the query buffer, swizzled like K.  Rows up to the end of
-// the last 64-row round are filled with copies of row nq-1 (never past the
-// buffer), so every query row a tile reads is finite.
+// the last 16-row tile are filled with copies of row nq-1, so every query row
+// a tile reads is finite.
 __device__ __forceinline__ void q_dma(const char* qbase, int nq, uint32_t row_bytes, uint16_t* Qd) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
   const uint32_t last = static_cast<uint32_t>(nq - 1);
   const uint32_t chunk = static_cast<uint32_t>(((lane & 7) ^ (lane >> 3)) * 16);
+  const int nrow = (nq + 15) & ~15;  // <= kAttnQTile
 #pragma unroll
-  for (int i = 0; i < (kAttnQTile + 63) / 64; ++i) {
-    const int row0 = i * 64 + wave * 8;
-    if (i * 64 < nq && row0 < kAttnQTile) {
+  for (int r = 0; r < (kAttnQTile / 8 + kWaves - 1) / kWaves; ++r) {
+    const int row0 = (r * kWaves + wave) * 8;
+    if (row0 < nrow) {
       const uint32_t off = min(static_cast<uint32_t>(row0 + (lane >> 3)), last) * row_bytes + chunk;
       __builtin_amdgcn_global_load_lds(qbase + off, (lds_void*)(Qd + row0 * kD), 16, 0, 0);
     }
@@ -392,7 +399,7 @@ __device__ __forceinline__ void q_read(const uint16_t* Qs, const LdsOffsets& lo,
   const int wave = threadIdx.x >> 6;
   const char* base = reinterpret_cast<const char*>(Qs);
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+  for (int j = 0; j < kTilesPerWave; ++j) {
     if (tile_q(wave, j) < nq) {
       const char* t = base + tile_q(wave, j) * kRowBytes;
       qf[j][0] = *reinterpret_cast<const bf16x8*>(t + lo.k0);
@@ -582,7 +589,7 @@ __device__ __forceinline__ int store_out(char* obase, int nq, uint32_t row_bytes
   const int g = lane >> 4;
   const uint32_t chunk = static_cast<uint32_t>((((g & 1) << 1) | (g >> 1)) * 16);
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+  for (int j = 0; j < kTilesPerWave; ++j) {
     if (j == 1 && !act1) break;
     const float inv = __builtin_amdgcn_rcpf(sm.l[j][0]);
     uint32_t r[4][2];
@@ -623,7 +630,8 @@ struct Sched {
 
 struct KernelCtx {
   const AttnParams& p;
-  int n_items, G;
+  int n_items;
+  int S, q, Gq;  // sub-queues, this workgroup's sub-queue, workgroups sharing it
   long long row_elems;
   uint32_t row_bytes;
   LdsOffsets lo;
@@ -667,7 +675,7 @@ __device__ __forceinline__ bool attn_stage(const KernelCtx& c, Sched& s, const c
   const int q0 = cur.chunk * kAttnQTile;
   const int nq = min(kAttnQTile, cur.len - q0);
   const bool act0 = tile_q(wave, 0) < nq;
-  const bool act1 = tile_q(wave, 1) < nq;
+  const bool act1 = kTilesPerWave > 1 && tile_q(wave, 1) < nq;
   if (s.sb == 0) {
     // The item's queries, then a barrier so the buffer can take the next
     // item's queries.
@@ -695,14 +703,19 @@ __device__ __forceinline__ bool attn_stage(const KernelCtx& c, Sched& s, const c
   raw_next.y = 0;
   int t_got = 0;
   if (tid == kQueueThread && !more_keys) {
-    if (s.t_nn < c.n_items) raw_next = p.items[s.t_nn];
-    t_got = atomicAdd(&p.hdr->counter, 1);
+    const int t = s.t_nn * c.S + c.q;
+    if (t < c.n_items) raw_next = p.items[t];
+    t_got = atomicAdd(&p.hdr->queue[c.q].ticket, 1);
   }
 
   if (act0) {
     const LanePtrs lp = lane_ptrs(Kc, Vc, c.lo);
-    if (act1) attend_stage<true>(lp, nk, s.sb == 0, p.scale_log2, c.ones, qf, sm);
-    else attend_stage<false>(lp, nk, s.sb == 0, p.scale_log2, c.ones, qf, sm);
+    if constexpr (kTilesPerWave > 1) {
+      if (act1) attend_stage<true>(lp, nk, s.sb == 0, p.scale_log2, c.ones, qf, sm);
+      else attend_stage<false>(lp, nk, s.sb == 0, p.scale_log2, c.ones, qf, sm);
+    } else {
+      attend_stage<false>(lp, nk, s.sb == 0, p.scale_log2, c.ones, qf, sm);
+    }
   }
   // Everything this stage loaded has arrived by now (the DMA went out before
   // the compute); an explicit wait says so, so that no later instruction
@@ -710,7 +723,7 @@ __device__ __forceinline__ bool attn_stage(const KernelCtx& c, Sched& s, const c
   __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
   if (tid == kQueueThread && !more_keys) {
     s_raw[B] = raw_next;
-    s.t_nn = t_got + 3 * c.G;
+    s.t_nn = t_got + 3 * c.Gq;
   }
   // The output goes last (nothing vector-memory may be issued after it).
   asm volatile("" ::: "memory");
@@ -746,7 +759,13 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16_kernel(AttnParams p) {
   // The first two descriptors are read before the plan header has arrived
   // (any slot below the workspace's capacity is in bounds) and dropped below
   // if they lie past the plan's item count.
-  const int t0 = blockIdx.x, t1 = blockIdx.x + static_cast<int>(gridDim.x);
+  // Sub-queue q = w % S of workgroup w; its local tickets r, r + Gq, ...
+  // (r = w / S, Gq workgroups share the sub-queue) name items lt * S + q.
+  const int G = static_cast<int>(gridDim.x);
+  const int S = min(kSubQueues, G);
+  const int q = static_cast<int>(blockIdx.x) % S, r = static_cast<int>(blockIdx.x) / S;
+  const int Gq = (G - q + S - 1) / S;
+  const int t0 = r * S + q, t1 = (r + Gq) * S + q;
   int2 r0, r1;
   r0.x = -1;
   r0.y = 0;
@@ -759,22 +778,25 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16_kernel(AttnParams p) {
     if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(p.status, DORA_DEV_PLAN);
     return;
   }
-  KernelCtx c{p, min(p.hdr->n_items, p.max_items), static_cast<int>(gridDim.x), static_cast<long long>(p.H) * kD,
+  KernelCtx c{p, min(p.hdr->n_items, p.max_items), S, q, Gq, static_cast<long long>(p.H) * kD,
               static_cast<uint32_t>(p.H) * kD * 2u, lds_offsets(), {},
               reinterpret_cast<const char*>(p.hdr->zero_row)};
 #pragma unroll
   for (int e = 0; e < 8; ++e) c.ones[e] = static_cast<__bf16>(1.0f);
 
-  // Queue.  Tickets 0 .. 3G-1 are dealt statically (workgroup w takes w, w+G
-  // and w+2G, the longest items), the rest come from the atomic counter, so
-  // the start of the kernel is not a burst of atomics on one address.
-  // One thread (kQueueThread) talks to the queue: it holds the ticket of the
-  // item after `nx`, loads that item's descriptor during a stage and
+  // Queue.  Local tickets 0 .. 3Gq-1 of a sub-queue are dealt statically
+  // (workgroup rank r takes r, r+Gq and r+2Gq, the longest items), the rest
+  // come from the sub-queue's atomic counter, so the start of the kernel is
+  // not a burst of atomics.  Eight counters on separate lines take eight
+  // times the atomic rate of one: with one counter, the atomics alone bound
+  // a DeiT-B execute to about 45 us.
+  // One thread (kQueueThread) talks to the queue: it holds the local ticket
+  // of the item after `nx`, loads that item's descriptor during a stage and
   // publishes it in LDS at the end of the stage, so no wave waits on the
   // queue mid-stage.
   Sched s;
   s.t_nn = 0;
-  if (tid == kQueueThread) s.t_nn = blockIdx.x + 2 * c.G;
+  if (tid == kQueueThread) s.t_nn = r + 2 * Gq;
   if (tid == 0) {
     s_first = t0;
     if (t0 >= c.n_items) r0.x = -1;
@@ -826,7 +848,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16_kernel(AttnParams p) {
 constexpr int kBlockKeys = 64;
 constexpr int kFStride = kD + 4;  // floats per K / V row in LDS
 
-__global__ __launch_bounds__(kThreads) void attn_fwd_f32_kernel(AttnParams p) {
+__global__ __launch_bounds__(kF32Threads) void attn_fwd_f32_kernel(AttnParams p) {
   __shared__ __attribute__((aligned(16))) float Ks[kBlockKeys * kFStride];
   __shared__ __attribute__((aligned(16))) float Vs[kBlockKeys * kFStride];
   __shared__ int s_ticket;
@@ -848,7 +870,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_f32_kernel(AttnParams p) {
   const long long row_elems = static_cast<long long>(p.H) * kD;
 
   for (;;) {
-    if (tid == 0) s_ticket = atomicAdd(&p.hdr->counter, 1);
+    if (tid == 0) s_ticket = atomicAdd(&p.hdr->queue[0].ticket, 1);
     __syncthreads();
     const int ticket = s_ticket;
     __syncthreads();
@@ -856,7 +878,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_f32_kernel(AttnParams p) {
     const Item it = decode_item(p, p.items[ticket]);
     const long long seq0 = it.seq0;
     const int len = it.len;
-    const int q0 = it.chunk * kAttnQTile + wave * kQPerWave;
+    const int q0 = it.chunk * kAttnQTile + wave * 32;
     const int qend = min(len, (it.chunk + 1) * kAttnQTile);  // this item's queries end here
     const bool active = q0 < qend;
 
@@ -879,8 +901,8 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_f32_kernel(AttnParams p) {
     for (int kb0 = 0; kb0 < len; kb0 += kBlockKeys) {
       __syncthreads();
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int e = tid + u * kThreads;  // 64 keys x 16 float4
+      for (int u = 0; u < kBlockKeys * 16 / kF32Threads; ++u) {
+        const int e = tid + u * kF32Threads;  // 64 keys x 16 float4
         const int key = e >> 4, dv = e & 15;
         float4 kv = make_float4(0.f, 0.f, 0.f, 0.f), vv = kv;
         if (kb0 + key < len) {
@@ -976,14 +998,14 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_f32_kernel(AttnParams p) {
 
 // Persistent grid: every compute unit filled to the kernel's occupancy.
 template <typename KernelT>
-int persistent_grid(KernelT kernel, int slot, int* grid) {
+int persistent_grid(KernelT kernel, int threads, int slot, int* grid) {
   static int per_cu_cache[64][2];
   int dev = 0;
   const int cus = device_cu_count(&dev);
   if (cus <= 0 || dev >= 64) return DORA_ERR_HIP;
   if (per_cu_cache[dev][slot] == 0) {
     int per_cu = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, 0) != hipSuccess ||
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess ||
         per_cu < 1)
       per_cu = 1;
     per_cu_cache[dev][slot] = per_cu;
@@ -1073,14 +1095,14 @@ extern "C" int dora_varlen_attn_execute(const void* q, const void* k, const void
   p.status = dev_status;
 
   int grid = 0;
-  const int rc = dtype == DORA_BF16 ? persistent_grid(attn_fwd_bf16_kernel, 0, &grid)
-                                    : persistent_grid(attn_fwd_f32_kernel, 1, &grid);
+  const int rc = dtype == DORA_BF16 ? persistent_grid(attn_fwd_bf16_kernel, kThreads, 0, &grid)
+                                    : persistent_grid(attn_fwd_f32_kernel, kF32Threads, 1, &grid);
   if (rc != DORA_OK) return rc;
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (dtype == DORA_BF16)
     hipLaunchKernelGGL(attn_fwd_bf16_kernel, dim3(grid), dim3(kThreads), 0, st, p);
   else
-    hipLaunchKernelGGL(attn_fwd_f32_kernel, dim3(grid), dim3(kThreads), 0, st, p);
+    hipLaunchKernelGGL(attn_fwd_f32_kernel, dim3(grid), dim3(kF32Threads), 0, st, p);
   return hipGetLastError() == hipSuccess ? DORA_OK : DORA_ERR_HIP;
 }
 

@@ -21,8 +21,9 @@ from gpu_util import assert_attn_close, to_dev, to_host_bits, widen
 pytestmark = pytest.mark.gpu
 
 Q_TILE = 240       # queries per item, as the library's workspace layout defines
-HDR_INTS = 64      # 256-byte header as int32 words
-ITEMS_OFF = 256
+HDR_BYTES = 2048   # plan header: sizes, a row of zeros, eight queue counters
+ITEMS_OFF = HDR_BYTES
+QUEUE_INTS = [64 + 32 * q for q in range(8)]   # one counter per 128-byte line
 
 
 def expected_items(keep, H, max_seqlen):
@@ -41,7 +42,7 @@ def expected_items(keep, H, max_seqlen):
 
 
 def read_plan(ws):
-    hdr = ws[:256].view(torch.int32).cpu().numpy()
+    hdr = ws[:HDR_BYTES].view(torch.int32).cpu().numpy()
     n = int(hdr[2])
     items = ws[ITEMS_OFF:ITEMS_OFF + 8 * n].view(torch.int32).cpu().numpy().astype(np.int64).reshape(-1, 2)
     return hdr, n, items
@@ -127,7 +128,7 @@ def test_fused_plan_replaces_a_stale_plan(gpu):
         hdr, n, items = read_plan(ws)
         assert n == len(expected_items(r.keep, w.H, w.N))
         assert np.array_equal(items, expected_items(r.keep, w.H, w.N))
-        assert int(hdr[0]) == 0 and int(hdr[1]) == 0          # queue counters reset
+        assert int(hdr[1]) == 0 and all(int(hdr[i]) == 0 for i in QUEUE_INTS)   # counters reset
         assert np.all(hdr[32:64] == 0)                         # the row of zeros
 
 
