@@ -365,22 +365,26 @@ __device__ __forceinline__ bf16x4 v_column4(const char* p) {
 // the busy waves of a short sequence spread over all four SIMDs.
 __device__ __forceinline__ int tile_q(int wave, int j) { return (wave + kWaves * j) * 16; }
 
-// DMA of the queries of an item's chunk (rows [0, nq) from qbase, 1 <= nq <=
-// kAttnQTile) into the query buffer, swizzled like K.  Rows up to the end of
-// the last 16-row tile are filled with copies of row nq-1, so every query row
-// a tile reads is finite.
+// DMA of this wave's query tiles of an item's chunk (chunk rows [0, nq) at
+// qbase, 1 <= nq <= kAttnQTile) into the query buffer, swizzled like K: the
+// 16 rows of each tile the wave owns, rows past nq-1 filled with copies of row
+// nq-1 so every row a tile reads is finite.  Each wave loads and reads only
+// its own rows, so no barrier guards the buffer between items.
 __device__ __forceinline__ void q_dma(const char* qbase, int nq, uint32_t row_bytes, uint16_t* Qd) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
   const uint32_t last = static_cast<uint32_t>(nq - 1);
   const uint32_t chunk = static_cast<uint32_t>(((lane & 7) ^ (lane >> 3)) * 16);
-  const int nrow = (nq + 15) & ~15;  // <= kAttnQTile
 #pragma unroll
-  for (int r = 0; r < (kAttnQTile / 8 + kWaves - 1) / kWaves; ++r) {
-    const int row0 = (r * kWaves + wave) * 8;
-    if (row0 < nrow) {
-      const uint32_t off = min(static_cast<uint32_t>(row0 + (lane >> 3)), last) * row_bytes + chunk;
-      __builtin_amdgcn_global_load_lds(qbase + off, (lds_void*)(Qd + row0 * kD), 16, 0, 0);
+  for (int j = 0; j < kTilesPerWave; ++j) {
+    const int t0 = tile_q(wave, j);
+    if (t0 < nq) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int row0 = t0 + 8 * h;
+        const uint32_t off = min(static_cast<uint32_t>(row0 + (lane >> 3)), last) * row_bytes + chunk;
+        __builtin_amdgcn_global_load_lds(qbase + off, (lds_void*)(Qd + row0 * kD), 16, 0, 0);
+      }
     }
   }
 }
@@ -677,11 +681,13 @@ __device__ __forceinline__ bool attn_stage(const KernelCtx& c, Sched& s, const c
   const bool act0 = tile_q(wave, 0) < nq;
   const bool act1 = kTilesPerWave > 1 && tile_q(wave, 1) < nq;
   if (s.sb == 0) {
-    // The item's queries, then a barrier so the buffer can take the next
-    // item's queries.
+    // The item's queries (this wave's rows), then, once they are in
+    // registers, the next item's queries into the same rows.
     q_read(Qs, c.lo, nq, qf);
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    if (s.nx_valid) q_chunk_dma(p, s.nx, c.row_elems, c.row_bytes, Qs);
+    if (s.nx_valid) {
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      q_chunk_dma(p, s.nx, c.row_elems, c.row_bytes, Qs);
+    }
   }
 
   // Next stage: the rest of this item's keys, or the next item.
