@@ -287,23 +287,21 @@ __device__ __forceinline__ const char* head_base(const void* X, long long row0, 
 // from `zrow`, so those keys add nothing to the output; the denominators
 // leave them out separately.
 __device__ __forceinline__ void kv_dma(const char* kbase, const char* vbase, const char* zrow, int n,
-                                       uint32_t row_bytes, uint16_t* Kd, uint16_t* Vd) {
+                                       uint32_t row_bytes, uint16_t* Kd, uint16_t* Vd, int w0, int nw) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
   const uint32_t last = static_cast<uint32_t>(n - 1);
   const uint32_t chunk = static_cast<uint32_t>(((lane & 7) ^ (lane >> 3)) * 16);
-  const int n64 = (n + 63) & ~63;
-  // Instruction i (8 rows) goes to wave i % kWaves.
-#pragma unroll
-  for (int r = 0; r < (kKRes / 8 + kWaves - 1) / kWaves; ++r) {
-    const int row0 = (r * kWaves + wave) * 8;
-    if (row0 < n64) {
-      const uint32_t row = static_cast<uint32_t>(row0 + (lane >> 3));
-      const uint32_t off = min(row, last) * row_bytes + chunk;
-      __builtin_amdgcn_global_load_lds(kbase + off, (lds_void*)(Kd + row0 * kD), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(row <= last ? vbase + off : zrow + chunk, (lds_void*)(Vd + row0 * kD), 16,
-                                       0, 0);
-    }
+  const int n8 = ((n + 63) & ~63) / 8;
+  // Instruction pair i (8 rows of K, 8 of V) goes to wave w0 + i % nw.
+  if (wave < w0) return;
+  for (int i = wave - w0; i < n8; i += nw) {
+    const int row0 = i * 8;
+    const uint32_t row = static_cast<uint32_t>(row0 + (lane >> 3));
+    const uint32_t off = min(row, last) * row_bytes + chunk;
+    __builtin_amdgcn_global_load_lds(kbase + off, (lds_void*)(Kd + row0 * kD), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(row <= last ? vbase + off : zrow + chunk, (lds_void*)(Vd + row0 * kD), 16,
+                                     0, 0);
   }
 }
 
@@ -690,7 +688,13 @@ __device__ __forceinline__ bool attn_stage(const KernelCtx& c, Sched& s, const c
     }
   }
 
-  // Next stage: the rest of this item's keys, or the next item.
+  // Next stage: the rest of this item's keys, or the next item.  Its DMA is
+  // issued by the waves with the fewest query tiles in this stage (waves
+  // w >= T % kWaves for T tiles: with T > kWaves the waves below hold two
+  // tiles, with T < kWaves the waves from T on hold none), so it stays off
+  // the busiest waves' path.
+  const int n_tiles = (nq + 15) / 16;
+  const int w_dma = kTilesPerWave > 1 ? n_tiles % kWaves : (n_tiles < kWaves ? n_tiles : 0);
   const bool more_keys = kb0 + kKRes < cur.len;
   const bool have_next = more_keys || s.nx_valid;
   if (have_next) {
@@ -700,7 +704,7 @@ __device__ __forceinline__ bool attn_stage(const KernelCtx& c, Sched& s, const c
     if (kv_n > 0)
       kv_dma(head_base(p.k, static_cast<long long>(kv_item.seq0) + kv_first, c.row_elems, kv_item.h),
              head_base(p.v, static_cast<long long>(kv_item.seq0) + kv_first, c.row_elems, kv_item.h), c.zrow, kv_n,
-             c.row_bytes, Kn, Vn);
+             c.row_bytes, Kn, Vn, w_dma, kWaves - w_dma);
   }
   // Queue traffic goes out after the DMA; its results are consumed before
   // the output stores.
@@ -828,7 +832,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16_kernel(AttnParams p) {
     const int nk = min(s.cur.len, kKRes);
     if (nk > 0)
       kv_dma(head_base(p.k, s.cur.seq0, c.row_elems, s.cur.h), head_base(p.v, s.cur.seq0, c.row_elems, s.cur.h),
-             c.zrow, nk, c.row_bytes, K0, V0);
+             c.zrow, nk, c.row_bytes, K0, V0, 0, kWaves);
     q_chunk_dma(p, s.cur, c.row_elems, c.row_bytes, lds.q);
   }
   SoftmaxState sm;
