@@ -29,6 +29,11 @@ HIPCC_FLAGS = [
     # Queue tickets are taken by one lane; keep the atomic as written so its
     # result is not broadcast to scalar registers (and waited on) at issue.
     "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
+    # The machine scheduler's iterative ILP strategy interleaves the softmax
+    # VALU work with the matrix and LDS instructions better than the default
+    # occupancy-driven one (DeiT-B attention 51.8 -> 49.1 us, select/pack
+    # about 0.6 us faster; no VGPR spills).
+    "-mllvm", "-amdgpu-sched-strategy=iterative-ilp",
     "-I", INCLUDE,
 ]
 

@@ -15,18 +15,25 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 // Number of compute units of the current device (cached per device id).
 int device_cu_count(int* device_out);
 
-// 16-byte global store at system scope (sc1), non-temporal (nt): it is
-// written through the L2 and does not stay there, so the line is not left
-// dirty (a bulk output written with plain stores leaves up to the L2's
-// capacity dirty: several microseconds of write-back after the last
-// workgroup ends) and the output does not push the inputs still to be read
-// out of the caches.  No builtin sets these bits on a global store, hence the
-// assembly.  The compiler does not count the store in its vmcnt bookkeeping;
-// vmcnt still counts it, so a compiler wait for a later load may also wait
-// for this store (never the reverse).
+// 16-byte stores at system scope (sc1), non-temporal (nt): written through
+// the L2 and not kept there, so no line is left dirty (a bulk output written
+// with plain stores leaves up to the L2's capacity dirty: several
+// microseconds of write-back after the last workgroup ends) and the output
+// does not push the inputs still to be read out of the caches.  Issued as
+// buffer stores, the only global store form whose cache-policy bits a builtin
+// sets; the compiler sees them as stores, so its hazard and wait bookkeeping
+// covers them.  The resource spans [base, base + 2^31 - 1) with raw byte
+// offsets; a store at an offset past that range is dropped by the hardware.
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-__device__ __forceinline__ void store_through(void* p, u32x4 v) {
-  asm volatile("global_store_dwordx4 %0, %1, off sc1 nt" ::"v"(p), "v"(v) : "memory");
+constexpr int kStoreThrough = 16 | 2;  // cache policy: sc1 (system scope) | nt
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_buffer(void* base) {
+  // Word 3 of a raw gfx9-family buffer descriptor: 32-bit data format, no swizzle.
+  return __builtin_amdgcn_make_buffer_rsrc(base, 0, 0x7FFFFFFF, 0x00020000);
+}
+
+__device__ __forceinline__ void store_through(__amdgpu_buffer_rsrc_t r, uint32_t off, u32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, kStoreThrough);
 }
 
 // Wave64 helpers.

@@ -233,9 +233,13 @@ __global__ __launch_bounds__(kThreads) void select_pack_kernel(SelectPackParams 
   const int step_vecs = kThreads - step_rows * vpr;
   int row = tid / vpr;
   int vec = tid - row * vpr;
+  // Stores go through a buffer resource based at this workgroup's first
+  // output row (offsets below 2^31: at most N rows of at most 1 MB); a row at
+  // or past cap_rows gets an offset past the resource and is dropped.
+  const __amdgpu_buffer_rsrc_t out = raw_buffer(p.packed + (off_out + r0) * vpr);
   for (int base = tid; base < nvec; base += kThreads * kCopyUnroll) {
     uint4 buf[kCopyUnroll];
-    long long dst[kCopyUnroll];
+    uint32_t dst[kCopyUnroll];
 #pragma unroll
     for (int u = 0; u < kCopyUnroll; ++u) {
       const bool in_range = base + u * kThreads < nvec;
@@ -243,7 +247,8 @@ __global__ __launch_bounds__(kThreads) void select_pack_kernel(SelectPackParams 
       const long long src_row = off_in + min(max(pos, 0), static_cast<int>(n) - 1);  // always inside the segment
       const long long out_row = off_out + r0 + row;
       buf[u] = in_range ? p.tokens[src_row * vpr + vec] : make_uint4(0u, 0u, 0u, 0u);
-      dst[u] = (in_range && out_row >= 0 && out_row < p.cap_rows) ? out_row * vpr + vec : -1;
+      dst[u] = (in_range && out_row >= 0 && out_row < p.cap_rows) ? static_cast<uint32_t>(row * vpr + vec) * 16u
+                                                                   : 0xFFFFFFF0u;
       row += step_rows;
       vec += step_vecs;
       if (vec >= vpr) {
@@ -251,12 +256,8 @@ __global__ __launch_bounds__(kThreads) void select_pack_kernel(SelectPackParams 
         ++row;
       }
     }
-    // One wait for both loads, so no store waits behind another store's
-    // write-through (the compiler does not see the stores; see store_through).
-    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
 #pragma unroll
-    for (int u = 0; u < kCopyUnroll; ++u)
-      if (dst[u] >= 0) store_through(p.packed + dst[u], u32x4{buf[u].x, buf[u].y, buf[u].z, buf[u].w});
+    for (int u = 0; u < kCopyUnroll; ++u) store_through(out, dst[u], u32x4{buf[u].x, buf[u].y, buf[u].z, buf[u].w});
   }
 }
 

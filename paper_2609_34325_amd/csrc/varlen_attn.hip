@@ -590,6 +590,7 @@ __device__ __forceinline__ int store_out(char* obase, int nq, uint32_t row_bytes
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane >> 4;
   const uint32_t chunk = static_cast<uint32_t>((((g & 1) << 1) | (g >> 1)) * 16);
+  const __amdgpu_buffer_rsrc_t out = raw_buffer(obase);
 #pragma unroll
   for (int j = 0; j < kTilesPerWave; ++j) {
     if (j == 1 && !act1) break;
@@ -610,12 +611,11 @@ __device__ __forceinline__ int store_out(char* obase, int nq, uint32_t row_bytes
       const auto s1 = __builtin_amdgcn_permlane16_swap(r[2 * pr][1], r[2 * pr + 1][1], false, false);
       v[pr] = u32x4{s0[0], s1[0], s0[1], s1[1]};
     }
+    // Queries past the chunk's end get an offset past the resource: dropped.
     const int qi = tile_q(wave, j) + (lane & 15);
-    if (qi < nq) {  // lane c16 = 0 is always inside, so both stores issue
-      char* dst = obase + static_cast<uint32_t>(qi) * row_bytes + chunk;
-      store_through(dst, v[0]);
-      store_through(dst + 64, v[1]);
-    }
+    const uint32_t off = qi < nq ? static_cast<uint32_t>(qi) * row_bytes + chunk : 0xFFFFFF00u;
+    store_through(out, off, v[0]);
+    store_through(out, off + 64, v[1]);
   }
   return act1 ? 4 : 2;
 }

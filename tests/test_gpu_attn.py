@@ -53,6 +53,17 @@ def test_ragged_tile_edges(gpu, dtype):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_query_chunk_and_stage_edges(gpu, dtype):
+    """Lengths around the 240-query chunks and the 256-key stages, several
+    chunks and stages in one sequence, and heads that wrap a DMA round."""
+    lens = np.array([239, 240, 241, 255, 256, 257, 479, 480, 481, 511, 512, 513, 720, 721])
+    rng = np.random.default_rng(41)
+    q, k, v = qkv(rng, lens, 5, dtype)
+    print(f"[attn] chunk/stage edges {dtype}", flush=True)
+    full_compare(gpu, q, k, v, cu_of(lens), dtype, what="chunk edges")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_empty_sequences(gpu, dtype):
     lens = np.array([0, 5, 0, 0, 130, 0, 1, 0])
     rng = np.random.default_rng(32)
