@@ -240,10 +240,15 @@ __device__ __forceinline__ int2 uniform_raw(int2 r) {
   return make_int2(__builtin_amdgcn_readfirstlane(r.x), __builtin_amdgcn_readfirstlane(r.y));
 }
 
+// Called by every thread of the workgroup.  The last workgroup out resets the
+// counters for the next execute.  Each ticket atomic has returned before the
+// wave that took it goes on (its result is waited for), so after the barrier
+// no ticket of this workgroup is in flight and its exit may be counted; the
+// exit count orders nothing else, so there is no fence (the output stores
+// drain on their own before the kernel ends).
 __device__ __forceinline__ void leave_queue(AttnPlanHeader* hdr) {
-  // The last workgroup out resets the counters for the next execute.
+  asm volatile("s_barrier" ::: "memory");
   if (threadIdx.x == 0) {
-    __threadfence();
     const int done = atomicAdd(&hdr->exit_count, 1);
     if (done == static_cast<int>(gridDim.x) - 1) {
       for (int q = 0; q < kSubQueues; ++q) atomicExch(&hdr->queue[q].ticket, 0);
