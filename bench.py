@@ -163,6 +163,73 @@ def summarize_profile(d: str, workload: str, traffic_json: str, calib_mib: int) 
     return 0
 
 
+N_XCD = 8             # MI355X: GRBM_GUI_ACTIVE comes summed over its 8 accelerator complex dies
+N_SIMD = 256 * 4      # 256 CUs x 4 SIMDs
+
+
+def summarize_pmc(d: str, workload: str) -> int:
+    """Reads rocprofv3 --pmc CSV output of runs of this script under DIR/*/
+    and prints, per kernel, the matrix-unit and LDS counters the attention
+    design is judged by: MFMA busy share (SQ_VALU_MFMA_BUSY_CYCLES over
+    GRBM_GUI_ACTIVE x SIMDs, rocprofv3's MfmaUtil), bf16 MFMA flops executed
+    (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512) against the algorithmic flops, and
+    LDS bank conflicts per LDS access cycle.  Averages are per dispatch, over
+    the launches after the first two."""
+    import csv
+    import collections
+    w = W.WORKLOADS[workload]
+    keep = W.generate(w, parts=("keep",))[0].keep
+    alg = {"attn": attn_flops(w, keep)}
+    per = collections.defaultdict(lambda: collections.defaultdict(lambda: collections.defaultdict(float)))
+    dur = collections.defaultdict(dict)
+    for sub in sorted(os.listdir(d)):
+        f = os.path.join(d, sub, "run_counter_collection.csv")
+        if not os.path.exists(f):
+            continue
+        for r in csv.DictReader(open(f)):
+            k = _kernel_key(r["Kernel_Name"])
+            if k is None:
+                continue
+            disp = (sub, int(r["Dispatch_Id"]))
+            per[k][r["Counter_Name"]][disp] += float(r["Counter_Value"])
+            dur[k][disp] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9
+
+    def mean(vals):
+        vals = [vals[i] for i in sorted(vals)]
+        vals = vals[2:] if len(vals) > 3 else vals
+        return sum(vals) / len(vals) if vals else float("nan")
+
+    lines = ["| Kernel | Counter / derived | Per launch |", "|---|---|---|"]
+    for k in sorted(per):
+        c = {name: mean(v) for name, v in per[k].items()}
+        t = mean(dur[k])
+        for name in sorted(c):
+            lines.append(f"| {k} | {name} | {c[name]:,.0f} |")
+        lines.append(f"| {k} | duration under the counters (us) | {t * 1e6:,.1f} |")
+        grbm = c.get("GRBM_GUI_ACTIVE")
+        if grbm:
+            lines.append(f"| {k} | clock = GRBM_GUI_ACTIVE / {N_XCD} / duration (GHz) | {grbm / N_XCD / t / 1e9:.2f} |")
+        if grbm and "SQ_VALU_MFMA_BUSY_CYCLES" in c:
+            util = c["SQ_VALU_MFMA_BUSY_CYCLES"] / (grbm / N_XCD * N_SIMD)
+            lines.append(f"| {k} | MFMA busy = MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / {N_XCD} x {N_SIMD} SIMDs) | "
+                         f"{100 * util:.1f} % |")
+        if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in c and k in alg:
+            ex = c["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512
+            lines.append(f"| {k} | bf16 MFMA flops executed / algorithmic | {ex / 1e9:,.2f} G / {alg[k] / 1e9:,.2f} G "
+                         f"= {ex / alg[k]:.2f} |")
+            lines.append(f"| {k} | executed bf16 MFMA rate over the duration | {ex / t / 1e12:,.0f} TFLOP/s "
+                         f"({100 * ex / t / 1e12 / MFMA_PEAK_TFLOPS['bf16']:.1f} % of peak) |")
+        if "SQ_LDS_BANK_CONFLICT" in c and "SQ_LDS_IDX_ACTIVE" in c and c["SQ_LDS_IDX_ACTIVE"] > 0:
+            lines.append(f"| {k} | LDS bank conflict cycles / LDS active cycles | "
+                         f"{c['SQ_LDS_BANK_CONFLICT'] / c['SQ_LDS_IDX_ACTIVE']:.3f} |")
+        if "SQ_WAVE_CYCLES" in c:
+            for name in ("SQ_ACTIVE_INST_VALU", "SQ_ACTIVE_INST_LDS", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY"):
+                if name in c:
+                    lines.append(f"| {k} | {name} / SQ_WAVE_CYCLES | {100 * c[name] / c['SQ_WAVE_CYCLES']:.1f} % |")
+    print("\n".join(lines))
+    return 0
+
+
 def cpu_model() -> str:
     try:
         for line in open("/proc/cpuinfo"):
@@ -203,10 +270,14 @@ def main() -> int:
                          "for scaling hardware byte counters)")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM bytes per launch (from rocprofv3 counters), if present")
+    ap.add_argument("--summarize-pmc", metavar="DIR",
+                    help="print matrix-unit / LDS counter summaries from rocprofv3 --pmc runs under DIR/*/")
     ap.add_argument("--summarize-profile", metavar="DIR",
                     help="no benchmark: summarise rocprofv3 output under DIR/{stats,fetch,write} "
                          "for --workload and update --traffic-json")
     args = ap.parse_args()
+    if args.summarize_pmc:
+        return summarize_pmc(args.summarize_pmc, args.workload)
     if args.summarize_profile:
         return summarize_profile(args.summarize_profile, args.workload, args.traffic_json,
                                  args.calibrate_copy or 256)
