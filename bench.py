@@ -230,6 +230,46 @@ def summarize_pmc(d: str, workload: str) -> int:
     return 0
 
 
+def measure_peaks(torch, stream) -> dict:
+    """What this device sustains: a plain 256 MiB device-to-device copy
+    (read + write bytes over time) and a loop of independent bf16 MFMAs on
+    every SIMD (paper_2609_34325_amd/csrc/calibrate.hip)."""
+    import ctypes
+    peaks = {}
+    nbytes = 256 * 2 ** 20
+    src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(10):
+        dst.copy_(src)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    peaks["copy_GBs"] = 2 * nbytes * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, dst
+    from paper_2609_34325_amd import build as pkg_build
+    if os.path.exists(pkg_build.CALIB_LIB):
+        lib = ctypes.CDLL(pkg_build.CALIB_LIB)
+        lib.dora_calibrate_mfma_bf16.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+        lib.dora_calibrate_mfma_bf16_flops.restype = ctypes.c_double
+        lib.dora_calibrate_mfma_bf16_flops.argtypes = [ctypes.c_int, ctypes.c_int]
+        blocks = 2 * torch.cuda.get_device_properties(0).multi_processor_count
+        iters = 4096
+        out = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+        for _ in range(2):
+            assert lib.dora_calibrate_mfma_bf16(blocks, iters, out.data_ptr(), stream.cuda_stream) == 0
+        e0.record(stream)
+        for _ in range(5):
+            lib.dora_calibrate_mfma_bf16(blocks, iters, out.data_ptr(), stream.cuda_stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        flops = 5 * lib.dora_calibrate_mfma_bf16_flops(blocks, iters)
+        peaks["mfma_bf16_TFLOPs"] = flops / (e0.elapsed_time(e1) * 1e-3) / 1e12
+    return peaks
+
+
 def cpu_model() -> str:
     try:
         for line in open("/proc/cpuinfo"):
@@ -265,6 +305,9 @@ def main() -> int:
     ap.add_argument("--repeats", type=int, default=5)
     ap.add_argument("--workload", default=W.HEADLINE, choices=sorted(W.WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cold-sets", type=int, default=3,
+                    help="also time the step rotating through this many buffer sets (cold MALL); <= 1: off")
+    ap.add_argument("--no-peaks", action="store_true", help="skip measuring the copy and MFMA peaks")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="before timing, run one plain device copy of MIB MiB (a reference dispatch "
                          "for scaling hardware byte counters)")
@@ -303,29 +346,77 @@ def main() -> int:
             return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
         return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
-    scores, keep, tokens = dev(r.scores), dev(r.keep), dev(r.tokens)
-    q, k, v = dev(r.q), dev(r.k), dev(r.v)
     sk = r.total_keep
     max_seqlen = int(r.keep.max())
-    idx = torch.empty(sk, dtype=torch.int32, device="cuda")
-    cu = torch.empty(w.B + 1, dtype=torch.int32, device="cuda")
-    packed = torch.empty((sk, w.C), dtype=tokens.dtype, device="cuda")
-    out = torch.empty_like(q)
-    ws = dora.new_workspace(w.B, w.H, max_seqlen)
-    st = dora.new_status()
     stream = torch.cuda.current_stream()
 
-    def step(ev=None):
+    def buffer_set(src=None):
+        """Inputs (copied from `src`, or uploaded) and outputs of one step."""
+        b = {}
+        if src is None:
+            b["scores"], b["keep"], b["tokens"] = dev(r.scores), dev(r.keep), dev(r.tokens)
+            b["q"], b["k"], b["v"] = dev(r.q), dev(r.k), dev(r.v)
+        else:
+            for name in ("scores", "keep", "tokens", "q", "k", "v"):
+                b[name] = src[name].clone()
+        b["idx"] = torch.empty(sk, dtype=torch.int32, device="cuda")
+        b["cu"] = torch.empty(w.B + 1, dtype=torch.int32, device="cuda")
+        b["packed"] = torch.empty((sk, w.C), dtype=b["tokens"].dtype, device="cuda")
+        b["out"] = torch.empty_like(b["q"])
+        b["ws"] = dora.new_workspace(w.B, w.H, max_seqlen)
+        b["st"] = dora.new_status()
+        return b
+
+    def step(b, ev=None):
         if ev is not None:
             ev[0].record(stream)
-        dora.dora_select_pack_plan(scores, keep, tokens, w.H, max_seqlen, sk, ws, idx_out=idx, cu_out=cu,
-                                   packed_out=packed, cap_rows=sk, dev_status=st, stream=stream)
+        dora.dora_select_pack_plan(b["scores"], b["keep"], b["tokens"], w.H, max_seqlen, sk, b["ws"],
+                                   idx_out=b["idx"], cu_out=b["cu"], packed_out=b["packed"], cap_rows=sk,
+                                   dev_status=b["st"], stream=stream)
         if ev is not None:
             ev[1].record(stream)
-        dora.dora_varlen_attn_execute(q, k, v, cu, max_seqlen, ws, out=out, dev_status=st, stream=stream)
+        dora.dora_varlen_attn_execute(b["q"], b["k"], b["v"], b["cu"], max_seqlen, b["ws"], out=b["out"],
+                                      dev_status=b["st"], stream=stream)
         if ev is not None:
             ev[2].record(stream)
 
+    def timed(sets, tag):
+        """Median over repeats of (step time, select/pack+plan time, attention
+        time) in ms; step i uses sets[i % len(sets)].  Each repeat times K steps
+        twice: once bare (events only at the two ends) and once with events
+        around every kernel (per-kernel durations; an event between two kernels
+        adds a few microseconds of dispatch latency to the interval, so these
+        are upper bounds)."""
+        for i in range(args.warmup):
+            step(sets[i % len(sets)])
+        torch.cuda.synchronize()
+        reps = []
+        for rep in range(args.repeats):
+            t_start = torch.cuda.Event(enable_timing=True)
+            t_end = torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            t_start.record(stream)
+            for i in range(args.steps):
+                step(sets[i % len(sets)])
+            t_end.record(stream)
+            torch.cuda.synchronize()
+            total_ms = t_start.elapsed_time(t_end)
+            evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+            torch.cuda.synchronize()
+            for i in range(args.steps):
+                step(sets[i % len(sets)], evs[i])
+            torch.cuda.synchronize()
+            sel = np.mean([e[0].elapsed_time(e[1]) for e in evs])
+            attn = np.mean([e[1].elapsed_time(e[2]) for e in evs])
+            reps.append((total_ms / args.steps, sel, attn))
+            print(f"[bench] {tag} repeat {rep}: {total_ms / args.steps * 1e3:.1f} us/step "
+                  f"(per kernel with events: select_pack+plan {sel * 1e3:.1f}, "
+                  f"attention {attn * 1e3:.1f})", file=sys.stderr, flush=True)
+        for b in sets:
+            assert int(b["st"].item()) == 0, f"device status {int(b['st'].item())}"
+        return sorted(reps, key=lambda x: x[0])[len(reps) // 2]
+
+    main_set = buffer_set()
     if args.calibrate_copy > 0:
         src = torch.ones(args.calibrate_copy * 2 ** 20, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -334,40 +425,20 @@ def main() -> int:
         torch.cuda.synchronize()
         del src, dst
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    assert int(st.item()) == 0, f"device status {int(st.item())}"
-
-    # Each repeat times K steps twice: once bare (the step time: events only at
-    # the two ends) and once with events around every kernel (per-kernel
-    # durations; an event between two kernels adds a few microseconds of
-    # dispatch latency to the interval, so these are upper bounds).
-    reps = []
-    for rep in range(args.repeats):
-        t_start = torch.cuda.Event(enable_timing=True)
-        t_end = torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        t_start.record(stream)
-        for i in range(args.steps):
-            step()
-        t_end.record(stream)
-        torch.cuda.synchronize()
-        total_ms = t_start.elapsed_time(t_end)
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
-        torch.cuda.synchronize()
-        for i in range(args.steps):
-            step(evs[i])
-        torch.cuda.synchronize()
-        sel = np.mean([e[0].elapsed_time(e[1]) for e in evs])
-        attn = np.mean([e[1].elapsed_time(e[2]) for e in evs])
-        reps.append((total_ms / args.steps, sel, attn))
-        print(f"[bench] repeat {rep}: {total_ms / args.steps * 1e3:.1f} us/step "
-              f"(per kernel with events: select_pack+plan {sel * 1e3:.1f}, "
-              f"attention {attn * 1e3:.1f})", file=sys.stderr, flush=True)
-    assert int(st.item()) == 0, f"device status {int(st.item())}"
-    med = sorted(reps, key=lambda x: x[0])[len(reps) // 2]
-    ms_step, ms_sel, ms_attn = med
+    # Warm: the same buffers every step, as in deployment, where the producing
+    # kernel has just written the inputs.
+    ms_step, ms_sel, ms_attn = timed([main_set], "warm")
+    # Cold: rotate through enough buffer sets that one rotation exceeds twice
+    # the 256 MB MALL, so every step's inputs come from HBM.
+    cold = None
+    if args.cold_sets > 1:
+        set_bytes = sum(t.numel() * t.element_size() for t in main_set.values())
+        cold_sets = [main_set] + [buffer_set(main_set) for _ in range(args.cold_sets - 1)]
+        c_step, c_sel, c_attn = timed(cold_sets, "cold")
+        cold = {"sets": args.cold_sets, "bytes_per_set": set_bytes, "ms_per_step": c_step,
+                "value": sk / (c_step * 1e-3),
+                "us": {"select_pack_plan": c_sel * 1e3, "attention": c_attn * 1e3, "step": c_step * 1e3}}
+        del cold_sets
 
     flops = attn_flops(w, r.keep)
     sp_bytes = select_pack_bytes(w, r.keep, r.n_in)
@@ -394,6 +465,20 @@ def main() -> int:
         attn_roofline = {"bound": "mfma", "achieved": attn_tflops, "peak": peak, "unit": "TFLOP/s",
                          "frac": attn_tflops / peak, **common}
 
+    peaks = {} if args.no_peaks else measure_peaks(torch, stream)
+    attn_roofline["attainable_tflops"] = min(peak, intensity * HBM_PEAK_GBS / 1e3)
+    if "copy_GBs" in peaks:
+        attn_roofline["frac_of_measured_copy"] = attn_gbs / peaks["copy_GBs"]
+    if "mfma_bf16_TFLOPs" in peaks and w.dtype == "bf16":
+        attn_roofline["frac_of_measured_mfma"] = attn_tflops / peaks["mfma_bf16_TFLOPs"]
+    if cold is not None:
+        c_attn, c_sel = cold["us"]["attention"] * 1e-6, cold["us"]["select_pack_plan"] * 1e-6
+        cold["attn_GBs"] = a_bytes / c_attn / 1e9
+        cold["attn_hbm_frac"] = cold["attn_GBs"] / HBM_PEAK_GBS
+        cold["attn_tflops"] = flops / c_attn / 1e12
+        cold["select_pack_GBs"] = sp_bytes / c_sel / 1e9
+        cold["select_pack_hbm_frac"] = cold["select_pack_GBs"] / HBM_PEAK_GBS
+
     result = {
         "metric": METRIC,
         "value": sk / (ms_step * 1e-3),
@@ -418,7 +503,12 @@ def main() -> int:
         "attn_tflops": attn_tflops,
         "us": {"select_pack_plan": ms_sel * 1e3, "attention": ms_attn * 1e3, "step": ms_step * 1e3},
         "repeats": args.repeats,
+        "regime": "warm: the same input buffers every step",
+        "cold": cold,
+        "measured_peaks": peaks,
     }
+    if "copy_GBs" in peaks:
+        result["roofline_select_pack"]["frac_of_measured_copy"] = sp_gbs / peaks["copy_GBs"]
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         result["cpu_baseline"] = run_cpu_baseline(w, r)

@@ -13,6 +13,9 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libdora.so")
+# Measurement helper for bench.py (sustained MFMA rate); not part of the boundary.
+CALIB_LIB = os.path.join(PKG, "libdora_calibrate.so")
+CALIB_SOURCES = ["calibrate.hip"]
 SOURCES = ["select_pack.hip", "varlen_attn.hip"]
 ARCH = "gfx950"
 
@@ -45,8 +48,14 @@ def hipcc() -> str:
 
 
 def build(verbose: bool = False) -> str:
-    srcs = [os.path.join(CSRC, s) for s in SOURCES]
-    tmp = LIB + ".tmp%d" % os.getpid()
+    _build_one(SOURCES, LIB, verbose)
+    _build_one(CALIB_SOURCES, CALIB_LIB, verbose)
+    return LIB
+
+
+def _build_one(sources, lib: str, verbose: bool) -> None:
+    srcs = [os.path.join(CSRC, s) for s in sources]
+    tmp = lib + ".tmp%d" % os.getpid()
     cmd = [hipcc(), *HIPCC_FLAGS, *srcs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
@@ -58,8 +67,7 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError("hipcc failed:\n" + "\n".join(msgs))
     if verbose and msgs:
         print("\n".join(msgs))
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
 
 
 if __name__ == "__main__":
