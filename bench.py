@@ -292,9 +292,16 @@ def run_cpu_baseline(w: W.Workload, r: W.RoundInputs, repeats: int = 3) -> dict:
         times.append(time.perf_counter() - t0)
         assert st == 0
     t = statistics.median(times)
+    # One more pass on one thread.
+    t0 = time.perf_counter()
+    idx, cu, packed, st = oracle.select_pack(r.scores, r.keep, r.tokens)
+    oracle.varlen_attn(r.q, r.k, r.v, cu, w.dtype, threads=1)
+    t1 = time.perf_counter() - t0
     return {"value": r.total_keep / t, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "value_1_thread": r.total_keep / t1,
             "sample": f"full {w.name} batch (B={w.B}, sum keep={r.total_keep}), select+pack+attention, "
-                      f"median of {repeats}, {t:.3f} s per pass, CPU: {cpu_model()}"}
+                      f"median of {repeats}, {t:.3f} s per pass ({t1:.3f} s on one thread), "
+                      f"CPU: {cpu_model()}"}
 
 
 def main() -> int:
