@@ -5,7 +5,9 @@ One step = one pass of the whole path over one batch:
                                gather, and the attention work queue of the
                                packed layout, in one launch)
     dora_varlen_attn_execute  (varlen attention, bf16 MFMA)
-on synthetic inputs already resident in HBM.  Prints one JSON line.
+on synthetic inputs already resident in HBM.  Prints one JSON line.  Beside
+the step it also times dora_select_pack_residual (the kept rows of tokens +
+attention output) on the same batch.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 """
@@ -44,6 +46,14 @@ def select_pack_bytes(w: W.Workload, keep: np.ndarray, n_in: np.ndarray) -> int:
     return 2 * sk * w.C * w.elt + 4 * (int(n_in.sum()) + sk + 2 * w.B + 1) + 8 * plan_items(w, keep) + 2048
 
 
+def residual_bytes(w: W.Workload, keep: np.ndarray, n_in: np.ndarray) -> int:
+    """Algorithmic HBM bytes of select/pack after the attention residual: read
+    scores and keep, read the kept rows of the tokens and of the attention
+    output, write each packed row once, write the kept indices and cu_seqlens."""
+    sk = int(keep.sum())
+    return 3 * sk * w.C * w.elt + 4 * (int(n_in.sum()) + sk + 2 * w.B + 1)
+
+
 def attn_flops(w: W.Workload, keep: np.ndarray) -> float:
     k = keep.astype(np.float64)
     return 4.0 * w.H * W.HEAD_DIM * float(np.sum(k * k))
@@ -54,9 +64,11 @@ def attn_bytes(w: W.Workload, keep: np.ndarray) -> int:
 
 
 KERNEL_SOURCES = {"attn": "paper_2609_34325_amd/csrc/varlen_attn.hip",
-                  "select_pack": "paper_2609_34325_amd/csrc/select_pack.hip"}
+                  "select_pack": "paper_2609_34325_amd/csrc/select_pack.hip",
+                  "residual": "paper_2609_34325_amd/csrc/select_pack.hip"}
 KERNEL_NAMES = {"attn": ("attn_fwd_bf16_kernel", "attn_fwd_f32_kernel"),
                 "select_pack": ("select_pack_kernel",),
+                "residual": ("select_pack_residual_kernel",),
                 "plan": ("attn_plan_kernel",)}
 
 
@@ -315,6 +327,8 @@ def main() -> int:
     ap.add_argument("--cold-sets", type=int, default=3,
                     help="also time the step rotating through this many buffer sets (cold MALL); <= 1: off")
     ap.add_argument("--no-peaks", action="store_true", help="skip measuring the copy and MFMA peaks")
+    ap.add_argument("--no-residual", action="store_true",
+                    help="skip timing select/pack after the attention residual (outside the step)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="before timing, run one plain device copy of MIB MiB (a reference dispatch "
                          "for scaling hardware byte counters)")
@@ -445,6 +459,54 @@ def main() -> int:
         cold = {"sets": args.cold_sets, "bytes_per_set": set_bytes, "ms_per_step": c_step,
                 "value": sk / (c_step * 1e-3),
                 "us": {"select_pack_plan": c_sel * 1e3, "attention": c_attn * 1e3, "step": c_step * 1e3}}
+
+    # Beside the path: deletion after the attention residual (the kept rows of
+    # tokens + attention output) on the same batch, timed on its own, warm and,
+    # with a second attention-output buffer per set, cold.
+    residual = None
+    if not args.no_residual:
+        a_host = W.generate(w, parts=("keep", "attn_out"))[0].attn_out
+        a_main = dev(a_host)
+
+        def res_launch(b, a):
+            dora.dora_select_pack_residual(b["scores"], b["keep"], b["tokens"], a, idx_out=b["idx"],
+                                           cu_out=b["cu"], packed_out=b["packed"], cap_rows=sk,
+                                           dev_status=b["st"], stream=stream)
+
+        def res_timed(pairs, tag):
+            for i in range(args.warmup):
+                res_launch(*pairs[i % len(pairs)])
+            reps = []
+            for rep in range(args.repeats):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                torch.cuda.synchronize()
+                e0.record(stream)
+                for i in range(args.steps):
+                    res_launch(*pairs[i % len(pairs)])
+                e1.record(stream)
+                torch.cuda.synchronize()
+                reps.append(e0.elapsed_time(e1) / args.steps)
+                print(f"[bench] residual {tag} repeat {rep}: {reps[-1] * 1e3:.1f} us/launch",
+                      file=sys.stderr, flush=True)
+            for b, _ in pairs:
+                assert int(b["st"].item()) == 0, f"device status {int(b['st'].item())}"
+            return sorted(reps)[len(reps) // 2]
+
+        rb = residual_bytes(w, r.keep, r.n_in)
+        ms_res = res_timed([(main_set, a_main)], "warm")
+        residual = {"entry": "dora_select_pack_residual", "kernel": "select_pack_residual_kernel",
+                    "bound": "hbm", "us": ms_res * 1e3, "achieved": rb / (ms_res * 1e-3) / 1e9,
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "algorithmic_bytes": rb,
+                    "tokens_per_s": sk / (ms_res * 1e-3), "regime": "warm"}
+        residual["frac"] = residual["achieved"] / HBM_PEAK_GBS
+        if args.cold_sets > 1:
+            pairs = [(main_set, a_main)] + [(b, a_main.clone()) for b in cold_sets[1:]]
+            ms_c = res_timed(pairs, "cold")
+            residual["cold"] = {"us": ms_c * 1e3, "achieved": rb / (ms_c * 1e-3) / 1e9,
+                                "frac": rb / (ms_c * 1e-3) / 1e9 / HBM_PEAK_GBS}
+            del pairs
+        del a_main
+    if args.cold_sets > 1:
         del cold_sets
 
     flops = attn_flops(w, r.keep)
@@ -516,6 +578,11 @@ def main() -> int:
     }
     if "copy_GBs" in peaks:
         result["roofline_select_pack"]["frac_of_measured_copy"] = sp_gbs / peaks["copy_GBs"]
+    if residual is not None:
+        residual["traffic"] = traffic.get("residual")
+        if "copy_GBs" in peaks:
+            residual["frac_of_measured_copy"] = residual["achieved"] / peaks["copy_GBs"]
+        result["residual_select_pack"] = residual
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         result["cpu_baseline"] = run_cpu_baseline(w, r)

@@ -174,6 +174,33 @@ int dora_select_pack_plan(const float* scores, const int32_t* keep, const void* 
                           void* workspace, size_t workspace_bytes, int32_t* dev_status, void* stream);
 
 /*
+ * dora_select_pack_residual -- deletion after the attention residual
+ * (Sec. 3.1, Eq. (1): the removed rows still take part in the current
+ * attention, and they are dropped from H + Attention(LayerNorm(H)) before
+ * the MLP).  Equivalent to dora_select_pack on tokens = h + a, without
+ * writing the full sum to memory: only the kept rows of the sum are formed.
+ *
+ *   h          dtype, the residual stream, laid out as `tokens` of
+ *              dora_select_pack (dense [B, N, C] or packed [total_in, C]).
+ *   a          dtype, the attention branch's output in h's layout (after the
+ *              output projection); 16-byte aligned.
+ *   packed_out packed_out[cu_out[b] + r] = h + a of token row
+ *              idx_out[cu_out[b] + r] of image b, each element the exact sum
+ *              of the two values rounded once to dtype, to nearest with ties
+ *              to even (subnormals kept; a sum past the largest finite value
+ *              is infinity).
+ * Every other argument, result and dev_status bit is that of
+ * dora_select_pack.  packed_out must not overlap h or a.
+ *
+ * Returns DORA_OK or a negative dora_status (DORA_ERR_NULL for a NULL a,
+ * DORA_ERR_ALIGN for a misaligned one); enqueues one kernel.
+ */
+int dora_select_pack_residual(const float* scores, const int32_t* keep, const void* h, const void* a,
+                              const int32_t* cu_in, int64_t total_in, int32_t B, int32_t N, int32_t C,
+                              dora_dtype dtype, int32_t* idx_out, int32_t* cu_out, void* packed_out,
+                              int64_t cap_rows, int32_t* dev_status, void* stream);
+
+/*
  * dora_varlen_attn_execute -- exact softmax attention inside each packed
  * sequence (Sec. 3.5 "Inference"; App. E.5): for every sequence b and head h
  *   O_b,h = softmax(softmax_scale * Q_b,h K_b,h^T) V_b,h

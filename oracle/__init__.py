@@ -12,6 +12,10 @@ The arithmetic lives in ``dora_oracle.c`` (plain C, fp64 for attention):
   original order (Sec. 3.1, Eq. (1)); images are compacted into one packed
   buffer with explicit boundaries (Sec. 3.5 "Inference").  Implemented as a
   full sort of (score, position) per image.
+* ``select_pack_residual`` applies the same deletion to H + A, the
+  attention residual (Sec. 3.1, Eq. (1): rows are removed after the
+  residual add and before the MLP): each element is the exact sum rounded
+  once, to nearest even, into bf16 or fp32 (``round_to_format``).
 * ``varlen_attn`` is exact softmax attention inside each boundary
   (Sec. 3.5; App. E.5), computed as a dense fp64 score matrix per
   (image, head) from the exact values of the bf16 / fp32 inputs.
@@ -22,7 +26,10 @@ closed forms (keep-all, keep-one, constant scores, monotone scores), a
 hand-worked fixture; for attention a pure-Python triple loop, torch fp64
 ``scaled_dot_product_attention`` on keep-all and padded+masked batches,
 one-hot V (softmax rows sum to 1), segment-permutation and key-permutation
-invariance, keep-one (O = V) and identical keys (O = mean of V).
+invariance, keep-one (O = V) and identical keys (O = mean of V); for the
+residual, torch's fp32 -> bf16 conversion and bf16 addition, NumPy's fp64 ->
+fp32 cast and fp32 addition, hand-worked ties, overflow and subnormal cases,
+and the -0 addend reducing to ``select_pack``.
 """
 from __future__ import annotations
 
@@ -54,6 +61,11 @@ def load_library(path: str):
         ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_double,
         ctypes.c_void_p, ctypes.c_int32]
     lib.oracle_max_threads.restype = ctypes.c_int
+    lib.oracle_round_to_format.restype = None
+    lib.oracle_round_to_format.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p]
+    lib.oracle_residual_add.restype = None
+    lib.oracle_residual_add.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
+                                        ctypes.c_void_p]
     return lib
 
 
@@ -112,6 +124,37 @@ def select_pack(scores: np.ndarray, keep: np.ndarray, tokens: np.ndarray,
     if st:
         return (np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros((0, C), tok2.dtype), int(st))
     return idx[:cap], cu, packed[:cap], 0
+
+
+def round_to_format(x: np.ndarray, dtype: str, lib=None) -> np.ndarray:
+    """fp64 values rounded to nearest-even bf16 (uint16 bits) or fp32."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    out = np.empty(x.shape, dtype=np.uint16 if dtype == "bf16" else np.float32)
+    _load(lib).oracle_round_to_format(_ptr(x), x.size, int(dtype == "bf16"), _ptr(out))
+    return out
+
+
+def residual_add(h: np.ndarray, a: np.ndarray, dtype: str, lib=None) -> np.ndarray:
+    """h + a, correctly rounded to the storage type: bf16 bit patterns (uint16)
+    or fp32 values, any shape (Sec. 3.1, Eq. (1): H + Attention(LayerNorm(H)))."""
+    st = np.uint16 if dtype == "bf16" else np.float32
+    h = np.ascontiguousarray(h, dtype=st)
+    a = np.ascontiguousarray(a, dtype=st)
+    if h.shape != a.shape:
+        raise ValueError("h and a must have the same shape")
+    out = np.empty(h.shape, dtype=st)
+    _load(lib).oracle_residual_add(_ptr(h), _ptr(a), h.size, int(dtype == "bf16"), _ptr(out))
+    return out
+
+
+def select_pack_residual(scores: np.ndarray, keep: np.ndarray, h: np.ndarray, a: np.ndarray, dtype: str,
+                         cu_in: Optional[np.ndarray] = None, N: Optional[int] = None, lib=None
+                         ) -> Tuple[np.ndarray, np.ndarray, np.ndarray, int]:
+    """Deletion after the attention residual (Sec. 3.1, Eq. (1)): the kept
+    rows of H + A, where A is the attention branch's output in H's layout.
+    Computed as the definition reads: the whole sum first, then
+    ``select_pack`` of it."""
+    return select_pack(scores, keep, residual_add(h, a, dtype, lib=lib), cu_in=cu_in, N=N, lib=lib)
 
 
 def widen(x: np.ndarray, dtype: str) -> np.ndarray:

@@ -22,6 +22,11 @@
  *   - Ties: equal scores are broken by the lower position (a stable order).
  *   - NaN ranks below every number; NaNs tie with each other.  -0 == +0.
  *   - Softmax scale is a parameter (1/sqrt(64) for ViT heads of width 64).
+ *   - Residual before deletion (Sec. 3.1, Eq. (1): the rows are removed from
+ *     H + Attention(...), not from H): each element of the sum is the exact
+ *     sum of the two stored values rounded once, to nearest with ties to
+ *     even, into the storage format (bf16 or fp32); subnormals are kept and
+ *     a sum past the largest finite value becomes infinity.
  *
  * Everything is computed the slow, direct way: a full sort per image and a
  * dense fp64 score matrix per (image, head).
@@ -181,6 +186,57 @@ void oracle_varlen_attn(const double* q, const double* k, const double* v, const
       }
       free(logits);
     }
+  }
+}
+
+/* Round x to the nearest value of a binary floating-point format with p
+ * significand bits (hidden bit included), smallest normal exponent emin and
+ * largest exponent emax; a tie goes to the even significand.  A result at or
+ * past 2^(emax+1) is infinity.  NaN, infinities and zeros pass through. */
+static double round_nearest_even(double x, int p, int emin, int emax) {
+  if (!isfinite(x) || x == 0.0) return x;
+  int e;
+  frexp(fabs(x), &e);                           /* |x| = m 2^e, 1/2 <= m < 1 */
+  const int lead = (e - 1 < emin) ? emin : e - 1; /* exponent of the leading bit, subnormals at emin */
+  const double quantum = ldexp(1.0, lead - (p - 1));
+  const double k = fabs(x) / quantum;           /* exact: power-of-two scaling */
+  double n = floor(k);
+  const double frac = k - n;
+  if (frac > 0.5 || (frac == 0.5 && fmod(n, 2.0) != 0.0)) n += 1.0;
+  double r = n * quantum;
+  if (r >= ldexp(1.0, emax + 1)) r = INFINITY;
+  return copysign(r, x);
+}
+
+/* x rounded to bf16 (is_bf16 != 0) or fp32, written as its bit pattern
+ * (uint16 or uint32) into out[i]. */
+void oracle_round_to_format(const double* x, int64_t n, int32_t is_bf16, void* out) {
+  for (int64_t i = 0; i < n; ++i) {
+    const float f = (float)round_nearest_even(x[i], is_bf16 ? 8 : 24, -126, 127); /* exact */
+    uint32_t bits;
+    memcpy(&bits, &f, sizeof bits);
+    if (is_bf16) ((uint16_t*)out)[i] = (uint16_t)(bits >> 16);
+    else ((uint32_t*)out)[i] = bits;
+  }
+}
+
+static double stored_value(const void* v, int64_t i, int32_t is_bf16) {
+  uint32_t bits;
+  float f;
+  if (is_bf16) bits = (uint32_t)((const uint16_t*)v)[i] << 16;
+  else bits = ((const uint32_t*)v)[i];
+  memcpy(&f, &bits, sizeof f);
+  return (double)f;
+}
+
+/* out = h + a elementwise over n values of bf16 (is_bf16 != 0) or fp32 bit
+ * patterns.  The sum of two such values in fp64 is either exact or rounded
+ * with at least 2p+2 significand bits to spare, so rounding it once more to
+ * the storage format gives the correctly rounded sum. */
+void oracle_residual_add(const void* h, const void* a, int64_t n, int32_t is_bf16, void* out) {
+  for (int64_t i = 0; i < n; ++i) {
+    const double s = stored_value(h, i, is_bf16) + stored_value(a, i, is_bf16);
+    oracle_round_to_format(&s, 1, is_bf16, is_bf16 ? (void*)((uint16_t*)out + i) : (void*)((uint32_t*)out + i));
   }
 }
 

@@ -50,6 +50,7 @@ DORA_HEAD_DIM = 64
 EXPORTS = (
     "dora_select_pack",
     "dora_select_pack_plan",
+    "dora_select_pack_residual",
     "dora_varlen_attn_workspace_size",
     "dora_varlen_attn_plan",
     "dora_varlen_attn_execute",
@@ -83,6 +84,9 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.dora_select_pack_plan.restype = ctypes.c_int
     lib.dora_select_pack_plan.argtypes = lib.dora_select_pack.argtypes[:13] + [i32, i32, i64, vp, sz,
                                                                                vp, vp]
+    lib.dora_select_pack_residual.restype = ctypes.c_int
+    lib.dora_select_pack_residual.argtypes = lib.dora_select_pack.argtypes[:3] + [vp] + \
+        lib.dora_select_pack.argtypes[3:]
     lib.dora_varlen_attn_workspace_size.restype = sz
     lib.dora_varlen_attn_workspace_size.argtypes = [i32, i32, i32]
     lib.dora_varlen_attn_plan.restype = ctypes.c_int
@@ -230,6 +234,27 @@ def dora_select_pack_plan(scores: torch.Tensor, keep: torch.Tensor, tokens: torc
                                    workspace.numel() * workspace.element_size(),
                                    _dev(outs[3], "dev_status", torch.int32), _stream(stream))
     _check("dora_select_pack_plan", rc)
+    return outs
+
+
+def dora_select_pack_residual(scores: torch.Tensor, keep: torch.Tensor, h: torch.Tensor, a: torch.Tensor,
+                              cu_in: Optional[torch.Tensor] = None, N: Optional[int] = None,
+                              idx_out: Optional[torch.Tensor] = None,
+                              cu_out: Optional[torch.Tensor] = None,
+                              packed_out: Optional[torch.Tensor] = None,
+                              cap_rows: Optional[int] = None,
+                              dev_status: Optional[torch.Tensor] = None,
+                              stream=None) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor, torch.Tensor]:
+    """dora_select_pack of the attention residual h + a: the kept rows of the
+    sum, each element rounded once to h's dtype.  a has h's shape and dtype."""
+    if a.shape != h.shape or a.dtype != h.dtype:
+        raise ValueError("a must have h's shape and dtype")
+    lib = load_library()
+    args, outs = _select_pack_args(scores, keep, h, cu_in, N, idx_out, cu_out, packed_out,
+                                   cap_rows, dev_status)
+    args.insert(3, _dev(a, "a", h.dtype))
+    rc = lib.dora_select_pack_residual(*args, _dev(outs[3], "dev_status", torch.int32), _stream(stream))
+    _check("dora_select_pack_residual", rc)
     return outs
 
 

@@ -5,6 +5,11 @@
 // the highest-scoring visual tokens), Sec. 3.5 "Inference" (packed buffer with
 // explicit sequence boundaries), App. E.5 (FP32 score comparisons).
 //
+// dora_select_pack_residual packs the kept rows of h + a instead, the
+// attention residual (Sec. 3.1, Eq. (1): rows are deleted after the residual
+// add): the same kernel body reads the two rows, adds them in fp32 and rounds
+// once to the storage type, so the full sum is never written.
+//
 // One launch.  Workgroup (b, s) handles image b; the `split` workgroups of an
 // image each repeat the (cheap) selection and then copy a disjoint share of
 // the kept rows, so the HBM-bound copy is spread over many workgroups.
@@ -36,6 +41,7 @@ struct SelectPackParams {
   const float* scores;
   const int32_t* keep;
   const uint4* tokens;
+  const uint4* addend;  // residual-add variant: rows added to the token rows (same layout), else null
   const int32_t* cu_in;
   int64_t total_in;
   int32_t B, N, row_vecs, split;
@@ -66,8 +72,38 @@ __device__ __forceinline__ long long wave_sum(long long v) {
   return v;
 }
 
-template <int SLOTS>
-__global__ __launch_bounds__(kThreads) void select_pack_kernel(SelectPackParams p) {
+// What the copy writes for one 16-byte piece of a kept row.
+enum PackMode { kCopy = 0, kAddBf16 = 1, kAddF32 = 2 };
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// tokens + addend for 8 bf16 or 4 fp32 values: the sum is formed in fp32 and
+// rounded once to the token type (round to nearest even).
+template <int MODE>
+__device__ __forceinline__ u32x4 combine(uint4 x, uint4 y) {
+  if constexpr (MODE == kCopy) {
+    return u32x4{x.x, x.y, x.z, x.w};
+  } else if constexpr (MODE == kAddF32) {
+    return u32x4{__float_as_uint(__uint_as_float(x.x) + __uint_as_float(y.x)),
+                 __float_as_uint(__uint_as_float(x.y) + __uint_as_float(y.y)),
+                 __float_as_uint(__uint_as_float(x.z) + __uint_as_float(y.z)),
+                 __float_as_uint(__uint_as_float(x.w) + __uint_as_float(y.w))};
+  } else {
+    const uint32_t a[4] = {x.x, x.y, x.z, x.w}, b[4] = {y.x, y.y, y.z, y.w};
+    u32x4 r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float lo = __uint_as_float(a[i] << 16) + __uint_as_float(b[i] << 16);
+      const float hi = __uint_as_float(a[i] & 0xFFFF0000u) + __uint_as_float(b[i] & 0xFFFF0000u);
+      const bf16x2 v = {static_cast<__bf16>(lo), static_cast<__bf16>(hi)};
+      r[i] = __builtin_bit_cast(uint32_t, v);
+    }
+    return r;
+  }
+}
+
+template <int SLOTS, int MODE>
+__device__ __forceinline__ void select_pack_body(const SelectPackParams& p) {
   __shared__ int32_t s_idx[SLOTS * 64];
   __shared__ long long s_part[kThreads / 64];
   __shared__ long long s_before[kThreads / 64];  // plan items of the sequences ordered before b
@@ -238,7 +274,7 @@ __global__ __launch_bounds__(kThreads) void select_pack_kernel(SelectPackParams 
   // or past cap_rows gets an offset past the resource and is dropped.
   const __amdgpu_buffer_rsrc_t out = raw_buffer(p.packed + (off_out + r0) * vpr);
   for (int base = tid; base < nvec; base += kThreads * kCopyUnroll) {
-    uint4 buf[kCopyUnroll];
+    uint4 buf[kCopyUnroll], add[kCopyUnroll];
     uint32_t dst[kCopyUnroll];
 #pragma unroll
     for (int u = 0; u < kCopyUnroll; ++u) {
@@ -247,6 +283,7 @@ __global__ __launch_bounds__(kThreads) void select_pack_kernel(SelectPackParams 
       const long long src_row = off_in + min(max(pos, 0), static_cast<int>(n) - 1);  // always inside the segment
       const long long out_row = off_out + r0 + row;
       buf[u] = in_range ? p.tokens[src_row * vpr + vec] : make_uint4(0u, 0u, 0u, 0u);
+      if constexpr (MODE != kCopy) add[u] = in_range ? p.addend[src_row * vpr + vec] : make_uint4(0u, 0u, 0u, 0u);
       dst[u] = (in_range && out_row >= 0 && out_row < p.cap_rows) ? static_cast<uint32_t>(row * vpr + vec) * 16u
                                                                    : 0xFFFFFFF0u;
       row += step_rows;
@@ -257,13 +294,31 @@ __global__ __launch_bounds__(kThreads) void select_pack_kernel(SelectPackParams 
       }
     }
 #pragma unroll
-    for (int u = 0; u < kCopyUnroll; ++u) store_through(out, dst[u], u32x4{buf[u].x, buf[u].y, buf[u].z, buf[u].w});
+    for (int u = 0; u < kCopyUnroll; ++u) store_through(out, dst[u], combine<MODE>(buf[u], add[u]));
   }
 }
 
+// One workgroup per (image, split) piece.  The plain variant copies rows; the
+// residual variant writes h + a of each kept row.
 template <int SLOTS>
-hipError_t launch(const SelectPackParams& p, hipStream_t stream) {
-  hipLaunchKernelGGL(select_pack_kernel<SLOTS>, dim3(p.B * p.split), dim3(kThreads), 0, stream, p);
+__global__ __launch_bounds__(kThreads) void select_pack_kernel(SelectPackParams p) {
+  select_pack_body<SLOTS, kCopy>(p);
+}
+
+template <int SLOTS, int MODE>
+__global__ __launch_bounds__(kThreads) void select_pack_residual_kernel(SelectPackParams p) {
+  select_pack_body<SLOTS, MODE>(p);
+}
+
+template <int SLOTS>
+hipError_t launch(const SelectPackParams& p, int mode, hipStream_t stream) {
+  const dim3 grid(p.B * p.split), block(kThreads);
+  if (mode == kAddBf16)
+    hipLaunchKernelGGL((select_pack_residual_kernel<SLOTS, kAddBf16>), grid, block, 0, stream, p);
+  else if (mode == kAddF32)
+    hipLaunchKernelGGL((select_pack_residual_kernel<SLOTS, kAddF32>), grid, block, 0, stream, p);
+  else
+    hipLaunchKernelGGL(select_pack_kernel<SLOTS>, grid, block, 0, stream, p);
   return hipGetLastError();
 }
 
@@ -298,6 +353,7 @@ int prepare(const float* scores, const int32_t* keep, const void* tokens, const 
   p->scores = scores;
   p->keep = keep;
   p->tokens = static_cast<const uint4*>(tokens);
+  p->addend = nullptr;
   p->cu_in = cu_in;
   p->total_in = total_in;
   p->B = B;
@@ -316,15 +372,15 @@ int prepare(const float* scores, const int32_t* keep, const void* tokens, const 
   return DORA_OK;
 }
 
-int launch_select_pack(const SelectPackParams& p, void* stream) {
+int launch_select_pack(const SelectPackParams& p, void* stream, int mode = kCopy) {
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t err;
-  if (p.N <= 64) err = launch<1>(p, st);
-  else if (p.N <= 128) err = launch<2>(p, st);
-  else if (p.N <= 256) err = launch<4>(p, st);
-  else if (p.N <= 512) err = launch<8>(p, st);
-  else if (p.N <= 1024) err = launch<16>(p, st);
-  else err = launch<32>(p, st);
+  if (p.N <= 64) err = launch<1>(p, mode, st);
+  else if (p.N <= 128) err = launch<2>(p, mode, st);
+  else if (p.N <= 256) err = launch<4>(p, mode, st);
+  else if (p.N <= 512) err = launch<8>(p, mode, st);
+  else if (p.N <= 1024) err = launch<16>(p, mode, st);
+  else err = launch<32>(p, mode, st);
   return err == hipSuccess ? DORA_OK : DORA_ERR_HIP;
 }
 
@@ -367,4 +423,20 @@ extern "C" int dora_select_pack_plan(const float* scores, const int32_t* keep, c
   p.max_items = static_cast<int32_t>(L.max_items);
   p.plan_total = total;
   return launch_select_pack(p, stream);
+}
+
+extern "C" int dora_select_pack_residual(const float* scores, const int32_t* keep, const void* h,
+                                         const void* a, const int32_t* cu_in, int64_t total_in, int32_t B,
+                                         int32_t N, int32_t C, dora_dtype dtype, int32_t* idx_out,
+                                         int32_t* cu_out, void* packed_out, int64_t cap_rows,
+                                         int32_t* dev_status, void* stream) {
+  using namespace dora;
+  SelectPackParams p;
+  const int rc = prepare(scores, keep, h, cu_in, total_in, B, N, C, dtype, idx_out, cu_out, packed_out, cap_rows,
+                         dev_status, &p);
+  if (rc != DORA_OK) return rc;
+  if (!a) return DORA_ERR_NULL;
+  if (reinterpret_cast<uintptr_t>(a) & 15u) return DORA_ERR_ALIGN;
+  p.addend = static_cast<const uint4*>(a);
+  return launch_select_pack(p, stream, dtype == DORA_BF16 ? kAddBf16 : kAddF32);
 }

@@ -72,6 +72,27 @@ def test_select_pack_host_validation():
     assert call_select(lib, cu_in=FAKE, total_in=-1) == dora.DORA_ERR_SHAPE
 
 
+def test_select_pack_residual_host_validation():
+    lib = dora.load_library()
+
+    def call(a=FAKE, **kw):
+        args = dict(scores=FAKE, keep=FAKE, tokens=FAKE, cu_in=None, total_in=0, B=4, N=197, C=768, dtype=1,
+                    idx=FAKE, cu=FAKE, packed=FAKE, cap=100, status=FAKE, stream=None)
+        args.update(kw)
+        return lib.dora_select_pack_residual(args["scores"], args["keep"], args["tokens"], a, args["cu_in"],
+                                             args["total_in"], args["B"], args["N"], args["C"], args["dtype"],
+                                             args["idx"], args["cu"], args["packed"], args["cap"],
+                                             args["status"], args["stream"])
+
+    assert call(a=None) == dora.DORA_ERR_NULL
+    assert call(a=FAKE + 8) == dora.DORA_ERR_ALIGN
+    assert call(tokens=None) == dora.DORA_ERR_NULL
+    assert call(C=3) == dora.DORA_ERR_ALIGN
+    assert call(dtype=7) == dora.DORA_ERR_DTYPE
+    assert call(cap=0) == dora.DORA_ERR_CAPACITY
+    assert call(N=dora.DORA_MAX_ROW_TOKENS + 1) == dora.DORA_ERR_SHAPE
+
+
 def call_select_plan(lib, **kw):
     ws = dora.dora_varlen_attn_workspace_size(4, 3, 197)
     a = dict(scores=FAKE, keep=FAKE, tokens=FAKE, cu_in=None, total_in=0, B=4, N=197, C=768, dtype=1,

@@ -38,7 +38,44 @@ MUTANTS = {
     "unnormalised": ("const double p = logits[j] / z;", "const double p = logits[j];"),
     "key_index_is_query": ("for (int32_t d = 0; d < D; ++d) dot += qi[d] * kj[d];",
                            "for (int32_t d = 0; d < D; ++d) dot += qi[d] * k[((start + i) * H + h) * D + d];"),
+    "ties_away_from_zero": ("if (frac > 0.5 || (frac == 0.5 && fmod(n, 2.0) != 0.0)) n += 1.0;",
+                            "if (frac >= 0.5) n += 1.0;"),
+    "truncating_round": ("if (frac > 0.5 || (frac == 0.5 && fmod(n, 2.0) != 0.0)) n += 1.0;", ""),
+    "no_subnormal_quantum": ("const int lead = (e - 1 < emin) ? emin : e - 1;", "const int lead = e - 1;"),
+    "bf16_one_bit_too_many": ("is_bf16 ? 8 : 24", "is_bf16 ? 9 : 24"),
+    "sign_dropped": ("return copysign(r, x);", "return r;"),
+    "addend_dropped": ("stored_value(h, i, is_bf16) + stored_value(a, i, is_bf16)",
+                       "stored_value(h, i, is_bf16) + stored_value(h, i, is_bf16)"),
+    "addend_row_shifted": ("stored_value(h, i, is_bf16) + stored_value(a, i, is_bf16)",
+                           "stored_value(h, i, is_bf16) + stored_value(a, i > 0 ? i - 1 : 0, is_bf16)"),
+    "bf16_widened_wrong": ("bits = (uint32_t)((const uint16_t*)v)[i] << 16;",
+                           "bits = (uint32_t)((const uint16_t*)v)[i] << 15;"),
 }
+
+
+def residual_battery(lib, rng):
+    """Residual pins: torch bf16 addition, NumPy fp32 addition, hand-worked roundings."""
+    failed = []
+    n = 20000
+    bits = lambda x: torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    wide = lambda: ((rng.integers(0, 2, n, dtype=np.uint32) << 31) | (rng.integers(0, 255, n, dtype=np.uint32) << 23)
+                    | rng.integers(0, 1 << 23, n, dtype=np.uint32)).view(np.float32)
+    h, a = bits(wide()), bits(np.concatenate([wide()[: n // 2], rng.standard_normal(n - n // 2)]))
+    want = (torch.from_numpy(h.view(np.int16)).view(torch.bfloat16)
+            + torch.from_numpy(a.view(np.int16)).view(torch.bfloat16)).view(torch.int16).numpy().view(np.uint16)
+    got = oracle.residual_add(h, a, "bf16", lib=lib)
+    fin = (want & 0x7F80) != 0x7F80
+    if not np.array_equal(got[fin], want[fin]):
+        failed.append("bf16 add")
+    x, y = wide(), wide()
+    with np.errstate(over="ignore", invalid="ignore"):
+        if not np.array_equal(oracle.residual_add(x, y, "f32", lib=lib).view(np.uint32), (x + y).view(np.uint32)):
+            failed.append("f32 add")
+    ties = np.array([1 + 2.0 ** -8, 1 + 3 * 2.0 ** -8, 1.5 * 2.0 ** -133, (2 - 2.0 ** -8) * 2.0 ** 127])
+    want_t = np.array([1.0, 1 + 2.0 ** -6, 2.0 ** -132, np.inf], np.float32)
+    if not np.array_equal(oracle.round_to_format(ties, "bf16", lib=lib), (want_t.view(np.uint32) >> 16).astype(np.uint16)):
+        failed.append("ties")
+    return failed
 
 
 def build_variant(tmp_path, name, old, new):
@@ -87,7 +124,7 @@ def battery(lib):
     want = want.transpose(1, 2).numpy()
     if any(np.max(np.abs(got[cuq[b]:cuq[b + 1]] - want[b, :lens[b]])) > 1e-12 for b in range(len(lens))):
         failed.append("attention")
-    return failed
+    return failed + residual_battery(lib, rng)
 
 
 def test_unmodified_source_passes(tmp_path):

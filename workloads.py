@@ -16,8 +16,9 @@ Conventions
 -----------
 * Every quantity of every round draws from its own PCG64 stream,
   ``numpy.random.default_rng([seed, round, part])`` with part 0..5 for
-  keep, scores, tokens (first round only), Q, K, V, so any subset can be
-  drawn without changing the others.
+  keep, scores, tokens (first round only), Q, K, V, and part 6 for the
+  attention branch's output that the residual variant adds to the tokens,
+  so any subset can be drawn without changing the others.
 * Keep counts derived from a ratio r use ``clip(rint(r * n), 1, n)``.
 * bf16 values are the round-to-nearest-even truncation of the float32 draw,
   stored as raw ``uint16`` bit patterns.
@@ -101,6 +102,7 @@ class RoundInputs:
     q: Optional[np.ndarray]          # [sum keep, H, 64]
     k: Optional[np.ndarray]
     v: Optional[np.ndarray]
+    attn_out: Optional[np.ndarray] = None  # [B,N,C] (first round) or [sum n_in, C]: attention branch output
 
     @property
     def total_keep(self) -> int:
@@ -153,6 +155,7 @@ def _draw_scores(w: Workload, rng: np.random.Generator, n: np.ndarray) -> np.nda
 
 
 PARTS = ("keep", "scores", "tokens", "qkv")
+ATTN_OUT_STD = 0.5   # attention-branch output relative to the unit-variance residual stream
 
 
 def _rng(seed: int, rnd: int, part: int) -> np.random.Generator:
@@ -189,7 +192,13 @@ def generate(w: Workload, seed: Optional[int] = None, batch: Optional[int] = Non
         q = k = v = None
         if "qkv" in parts:
             q, k, v = (_normal(_rng(sd, r, 3 + i), (tot, w.H, HEAD_DIM), w.dtype) for i in range(3))
-        rounds.append(RoundInputs(keep=keep, scores=scores, n_in=n.copy(), tokens=tokens, q=q, k=k, v=v))
+        attn_out = None
+        if "attn_out" in parts:
+            shape = (w.B, w.N, w.C) if r == 0 else (int(n.astype(np.int64).sum()), w.C)
+            x = _rng(sd, r, 6).standard_normal(size=shape, dtype=np.float32) * np.float32(ATTN_OUT_STD)
+            attn_out = x if w.dtype == "f32" else f32_to_bf16_bits(x)
+        rounds.append(RoundInputs(keep=keep, scores=scores, n_in=n.copy(), tokens=tokens, q=q, k=k, v=v,
+                                  attn_out=attn_out))
         n = keep.copy()
     return rounds
 
