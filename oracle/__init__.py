@@ -16,6 +16,11 @@ The arithmetic lives in ``dora_oracle.c`` (plain C, fp64 for attention):
   attention residual (Sec. 3.1, Eq. (1): rows are removed after the
   residual add and before the MLP): each element is the exact sum rounded
   once, to nearest even, into bf16 or fp32 (``round_to_format``).
+* ``actor_gate`` / ``actor_budget`` / ``negate`` decode the deterministic
+  actor's outputs into the path's inputs (Sec. 3.2 "Sampling and
+  deployment"; App. A.2 legal budgets; App. A.3): gate at p >= 0.5 with a
+  legal budget, gate-on images numbered in image order, the legal budget of
+  the largest logit, keep = tokens - budget, keep-scores = -removal scores.
 * ``varlen_attn`` is exact softmax attention inside each boundary
   (Sec. 3.5; App. E.5), computed as a dense fp64 score matrix per
   (image, head) from the exact values of the bf16 / fp32 inputs.
@@ -61,6 +66,14 @@ def load_library(path: str):
         ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_double,
         ctypes.c_void_p, ctypes.c_int32]
     lib.oracle_max_threads.restype = ctypes.c_int
+    lib.oracle_actor_gate.restype = None
+    lib.oracle_actor_gate.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    lib.oracle_actor_budget.restype = None
+    lib.oracle_actor_budget.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.c_int32, ctypes.c_void_p]
+    lib.oracle_negate.restype = None
+    lib.oracle_negate.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
     lib.oracle_round_to_format.restype = None
     lib.oracle_round_to_format.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p]
     lib.oracle_residual_add.restype = None
@@ -155,6 +168,40 @@ def select_pack_residual(scores: np.ndarray, keep: np.ndarray, h: np.ndarray, a:
     Computed as the definition reads: the whole sum first, then
     ``select_pack`` of it."""
     return select_pack(scores, keep, residual_add(h, a, dtype, lib=lib), cu_in=cu_in, N=N, lib=lib)
+
+
+def actor_gate(p_gate: np.ndarray, n_tok: np.ndarray, M: int, lib=None) -> Tuple[np.ndarray, np.ndarray, int]:
+    """Gate of the deterministic actor (Sec. 3.2; App. A.2-A.3): image b opens
+    when p_gate[b] >= 0.5 and some even budget 2..2M leaves >= 4 visual
+    tokens.  n_tok counts CLS.  Returns (on_rank [B], on_list [B], n_on)."""
+    p_gate = np.ascontiguousarray(p_gate, dtype=np.float32)
+    n_tok = np.ascontiguousarray(n_tok, dtype=np.int32)
+    B = int(n_tok.shape[0])
+    on_rank = np.empty(B, np.int32)
+    on_list = np.empty(B, np.int32)
+    n_on = np.zeros(1, np.int32)
+    _load(lib).oracle_actor_gate(_ptr(p_gate), _ptr(n_tok), B, int(M), _ptr(on_rank), _ptr(on_list), _ptr(n_on))
+    return on_rank, on_list, int(n_on[0])
+
+
+def actor_budget(logits: np.ndarray, n_tok: np.ndarray, on_rank: np.ndarray, lib=None) -> np.ndarray:
+    """Keep counts: n_tok - k for gate-on images, k the legal budget with the
+    largest logit (row on_rank[b] of logits [rows, M]); n_tok otherwise."""
+    logits = np.ascontiguousarray(logits, dtype=np.float32)
+    n_tok = np.ascontiguousarray(n_tok, dtype=np.int32)
+    on_rank = np.ascontiguousarray(on_rank, dtype=np.int32)
+    B = int(n_tok.shape[0])
+    keep = np.empty(B, np.int32)
+    _load(lib).oracle_actor_budget(_ptr(logits), int(logits.shape[1]), _ptr(n_tok), _ptr(on_rank), B, _ptr(keep))
+    return keep
+
+
+def negate(s: np.ndarray, lib=None) -> np.ndarray:
+    """Keep-scores from removal scores: -s."""
+    s = np.ascontiguousarray(s, dtype=np.float32)
+    out = np.empty_like(s)
+    _load(lib).oracle_negate(_ptr(s), s.size, _ptr(out))
+    return out
 
 
 def widen(x: np.ndarray, dtype: str) -> np.ndarray:

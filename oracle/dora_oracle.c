@@ -240,6 +240,67 @@ void oracle_residual_add(const void* h, const void* a, int64_t n, int32_t is_bf1
   }
 }
 
+/* Number of legal budgets of an image of n_tok tokens (CLS included), by
+ * enumerating the grid 2, 4, ..., 2M. */
+static int32_t legal_budget_count(int32_t n_tok, int32_t M) {
+  int32_t count = 0;
+  for (int32_t m = 0; m < M; ++m)
+    if (2 * (m + 1) <= (n_tok - 1) - 4) ++count;
+  return count;
+}
+
+/* Deterministic actor decode, gate (Sec. 3.2 "Sampling and deployment";
+ * Sec. 3.2 "Gate"; App. A.2, Eq. (legal budgets); App. A.3).  Image b holds
+ * n_tok[b] tokens with CLS, so N_l = n_tok[b] - 1 visual tokens.  The legal
+ * budgets are the even counts k = 2, 4, ..., 2M with k <= N_l - 4; the gate
+ * opens when p_gate[b] >= 0.5 and at least one budget is legal.  Gate-on
+ * images are numbered in image order: on_rank[b] is b's number (-1 when the
+ * gate is off), on_list[r] the image numbered r (-1 past the last), *n_on the
+ * count. */
+void oracle_actor_gate(const float* p_gate, const int32_t* n_tok, int32_t B, int32_t M, int32_t* on_rank,
+                       int32_t* on_list, int32_t* n_on) {
+  int32_t r = 0;
+  for (int32_t b = 0; b < B; ++b) on_list[b] = -1;
+  for (int32_t b = 0; b < B; ++b) {
+    const int open = p_gate[b] >= 0.5f && legal_budget_count(n_tok[b], M) > 0;
+    on_rank[b] = open ? r : -1;
+    if (open) on_list[r++] = b;
+  }
+  *n_on = r;
+}
+
+/* Deterministic actor decode, budget and keep counts (App. A.3: the highest
+ * legal budget logit, then the k highest removal scores are deleted).  Row
+ * on_rank[b] of logits [rows, M] belongs to gate-on image b; the budget is
+ * the legal k = 2(m+1) of the largest logit, the first on ties, NaN above
+ * every number (so the first NaN wins), as an argmax over the logits with the
+ * illegal budgets masked out.  keep[b] = n_tok[b] - k (CLS is never removed);
+ * a gate-off image keeps all n_tok[b] tokens. */
+void oracle_actor_budget(const float* logits, int32_t M, const int32_t* n_tok, const int32_t* on_rank,
+                         int32_t B, int32_t* keep) {
+  for (int32_t b = 0; b < B; ++b) {
+    if (on_rank[b] < 0) {
+      keep[b] = n_tok[b];
+      continue;
+    }
+    const float* row = logits + (int64_t)on_rank[b] * M;
+    const int32_t legal = legal_budget_count(n_tok[b], M);
+    int32_t best = 0;
+    for (int32_t m = 1; m < legal; ++m) {
+      const float x = row[m], y = row[best];
+      if (isnan(y)) break;
+      if (isnan(x) || x > y) best = m;
+    }
+    keep[b] = n_tok[b] - 2 * (best + 1);
+  }
+}
+
+/* Keep-scores from the selector's removal scores (Sec. 3.2, Eq. (2): higher
+ * = remove): out = -s, elementwise. */
+void oracle_negate(const float* s, int64_t n, float* out) {
+  for (int64_t i = 0; i < n; ++i) out[i] = -s[i];
+}
+
 int oracle_max_threads(void) {
 #ifdef _OPENMP
   return omp_get_max_threads();

@@ -50,7 +50,49 @@ MUTANTS = {
                            "stored_value(h, i, is_bf16) + stored_value(a, i > 0 ? i - 1 : 0, is_bf16)"),
     "bf16_widened_wrong": ("bits = (uint32_t)((const uint16_t*)v)[i] << 16;",
                            "bits = (uint32_t)((const uint16_t*)v)[i] << 15;"),
+    "gate_strict_threshold": ("p_gate[b] >= 0.5f", "p_gate[b] > 0.5f"),
+    "legal_off_by_one": ("if (2 * (m + 1) <= (n_tok - 1) - 4) ++count;", "if (2 * (m + 1) < (n_tok - 1) - 4) ++count;"),
+    "cls_counted_as_visual": ("if (2 * (m + 1) <= (n_tok - 1) - 4) ++count;", "if (2 * (m + 1) <= n_tok - 4) ++count;"),
+    "argmax_last_tie": ("if (isnan(x) || x > y) best = m;", "if (isnan(x) || x >= y) best = m;"),
+    "argmax_skips_nan": ("if (isnan(x) || x > y) best = m;", "if (x > y) best = m;"),
+    "odd_budget": ("keep[b] = n_tok[b] - 2 * (best + 1);", "keep[b] = n_tok[b] - (2 * best + 1);"),
+    "keep_counts_visual_only": ("keep[b] = n_tok[b] - 2 * (best + 1);", "keep[b] = n_tok[b] - 1 - 2 * (best + 1);"),
+    "rank_not_compacted": ("on_rank[b] = open ? r : -1;", "on_rank[b] = open ? b : -1;"),
+    "gate_off_drops_one": ("keep[b] = n_tok[b];\n      continue;", "keep[b] = n_tok[b] - 1;\n      continue;"),
+    "negate_magnitude": ("out[i] = -s[i];", "out[i] = -fabsf(s[i]);"),
 }
+
+
+def actor_battery(lib, rng):
+    """Actor-decode pins: Table 3 grids, the set definitions, torch's argmax, NumPy compaction / negation."""
+    failed = []
+    for N0, M in ((196, 96), (256, 126)):
+        n_tok = np.full(M, N0 + 1, np.int32)
+        on_rank, _, n_on = oracle.actor_gate(np.ones(M, np.float32), n_tok, M, lib=lib)
+        keep = oracle.actor_budget(np.eye(M, dtype=np.float32), n_tok, on_rank, lib=lib)
+        if n_on != M or list(n_tok - keep) != list(range(2, N0 - 4 + 1, 2)):
+            failed.append("table 3")
+    B, M = 3000, 96
+    n_tok = rng.integers(1, 198, B).astype(np.int32)
+    p = rng.choice(np.array([0.5, np.nextafter(np.float32(0.5), np.float32(0)), 0.9, 0.1, np.nan], np.float32), B)
+    on_rank, on_list, n_on = oracle.actor_gate(p, n_tok, M, lib=lib)
+    n_legal = np.array([len([k for k in range(2, 2 * M + 1, 2) if k <= n - 5]) for n in n_tok])
+    on = (p >= 0.5) & (n_legal > 0)
+    if n_on != on.sum() or not np.array_equal(on_list[:n_on], np.flatnonzero(on)) or \
+            not np.array_equal(on_rank[on], np.arange(n_on)) or not np.all(on_rank[~on] == -1):
+        failed.append("gate")
+        return failed
+    logits = rng.choice(np.array([-1.0, 0.0, 2.0, np.nan], np.float32), (B, M), p=[0.3, 0.3, 0.38, 0.02])
+    keep = oracle.actor_budget(logits, n_tok, on_rank, lib=lib)
+    t = torch.from_numpy(logits[np.maximum(on_rank, 0)])
+    m = torch.argmax(t.masked_fill(torch.arange(M)[None, :] >= torch.from_numpy(n_legal)[:, None], -np.inf),
+                     dim=1).numpy()
+    if not np.array_equal(np.where(on, n_tok - 2 * (m + 1), n_tok), keep):
+        failed.append("budget")
+    s = rng.standard_normal(1000).astype(np.float32)
+    if not np.array_equal(oracle.negate(s, lib=lib).view(np.uint32), np.negative(s).view(np.uint32)):
+        failed.append("negate")
+    return failed
 
 
 def residual_battery(lib, rng):
@@ -124,7 +166,7 @@ def battery(lib):
     want = want.transpose(1, 2).numpy()
     if any(np.max(np.abs(got[cuq[b]:cuq[b + 1]] - want[b, :lens[b]])) > 1e-12 for b in range(len(lens))):
         failed.append("attention")
-    return failed + residual_battery(lib, rng)
+    return failed + residual_battery(lib, rng) + actor_battery(lib, rng)
 
 
 def test_unmodified_source_passes(tmp_path):
