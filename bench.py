@@ -69,6 +69,7 @@ KERNEL_SOURCES = {"attn": "paper_2609_34325_amd/csrc/varlen_attn.hip",
 KERNEL_NAMES = {"attn": ("attn_fwd_bf16_kernel", "attn_fwd_f32_kernel"),
                 "select_pack": ("select_pack_kernel",),
                 "residual": ("select_pack_residual_kernel",),
+                "actor": ("actor_gate_kernel", "actor_decode_kernel"),
                 "plan": ("attn_plan_kernel",)}
 
 
@@ -327,6 +328,7 @@ def main() -> int:
     ap.add_argument("--cold-sets", type=int, default=3,
                     help="also time the step rotating through this many buffer sets (cold MALL); <= 1: off")
     ap.add_argument("--no-peaks", action="store_true", help="skip measuring the copy and MFMA peaks")
+    ap.add_argument("--no-actor", action="store_true", help="skip timing the actor decode (outside the step)")
     ap.add_argument("--no-residual", action="store_true",
                     help="skip timing select/pack after the attention residual (outside the step)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -509,6 +511,47 @@ def main() -> int:
     if args.cold_sets > 1:
         del cold_sets
 
+    # Beside the path: the deterministic actor's decode that produces its
+    # inputs (gate + compaction, then budget argmax, keep counts and
+    # keep-scores), timed as a pair of launches.
+    actor = None
+    if not args.no_actor:
+        M = W.budget_outputs(w)
+        p_h, logits_h, removal_h = W.actor_outputs(w)
+        p_d, logits_d, removal_d = dev(p_h), dev(logits_h), dev(removal_h)
+        on_rank = torch.empty(w.B, dtype=torch.int32, device="cuda")
+        on_list = torch.empty_like(on_rank)
+        n_on = torch.empty(1, dtype=torch.int32, device="cuda")
+        keep_d = torch.empty_like(on_rank)
+        ks_d = torch.empty_like(removal_d)
+        st_a = dora.new_status()
+
+        def actor_pair():
+            dora.dora_actor_gate(p_d, M, w.N, on_rank=on_rank, on_list=on_list, n_on=n_on, dev_status=st_a,
+                                 stream=stream)
+            dora.dora_actor_decode(logits_d, on_rank, w.N, removal_scores=removal_d, keep_out=keep_d,
+                                   scores_out=ks_d, dev_status=st_a, stream=stream)
+
+        for _ in range(args.warmup):
+            actor_pair()
+        reps = []
+        for rep in range(args.repeats):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for _ in range(args.steps):
+                actor_pair()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            reps.append(e0.elapsed_time(e1) / args.steps)
+        assert int(st_a.item()) == 0, f"device status {int(st_a.item())}"
+        ms_actor = sorted(reps)[len(reps) // 2]
+        actor = {"entries": ["dora_actor_gate", "dora_actor_decode"], "bound": "latency",
+                 "us_per_pair": ms_actor * 1e3, "gate_on": int(n_on.item()), "M": M,
+                 "note": "two small launches back to back; the cost is launch and dependency latency"}
+        print(f"[bench] actor decode: {ms_actor * 1e3:.1f} us per gate+decode pair, "
+              f"{actor['gate_on']} of {w.B} gates open", file=sys.stderr, flush=True)
+
     flops = attn_flops(w, r.keep)
     sp_bytes = select_pack_bytes(w, r.keep, r.n_in)
     a_bytes = attn_bytes(w, r.keep)
@@ -583,6 +626,8 @@ def main() -> int:
         if "copy_GBs" in peaks:
             residual["frac_of_measured_copy"] = residual["achieved"] / peaks["copy_GBs"]
         result["residual_select_pack"] = residual
+    if actor is not None:
+        result["actor_decode"] = actor
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         result["cpu_baseline"] = run_cpu_baseline(w, r)

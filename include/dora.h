@@ -65,6 +65,8 @@ typedef enum {
 #define DORA_DEV_CU_SEQLENS 0x8  /* attention offsets invalid (non-monotone, past total, or a
                                     sequence longer than max_seqlen); such sequences were skipped */
 #define DORA_DEV_PLAN 0x10       /* execute called with a workspace not planned for these sizes    */
+#define DORA_DEV_ACTOR 0x20      /* actor decode: a gate-on image without a legal budget or logit row;
+                                    it was left unpruned                                           */
 
 /* Limits of this build. */
 #define DORA_MAX_ROW_TOKENS 2048     /* dora_select_pack: N (tokens per image, CLS included)  */
@@ -199,6 +201,63 @@ int dora_select_pack_residual(const float* scores, const int32_t* keep, const vo
                               const int32_t* cu_in, int64_t total_in, int32_t B, int32_t N, int32_t C,
                               dora_dtype dtype, int32_t* idx_out, int32_t* cu_out, void* packed_out,
                               int64_t cap_rows, int32_t* dev_status, void* stream);
+
+/*
+ * dora_actor_gate -- gate of the deterministic actor and compaction of the
+ * gate-on images (Sec. 3.2 "Gate" and "Sampling and deployment"; App. A.2,
+ * Eq. (legal budgets); App. A.3).
+ *
+ * Image b holds n_b tokens with CLS (N_l = n_b - 1 visual tokens).  The
+ * budget grid is k = 2, 4, ..., 2M (M budget-head outputs, M = (N0 - 4) / 2
+ * in the paper's Table 3) and a budget is legal when k <= N_l - 4, so that at
+ * least four visual tokens survive.  The gate opens when p_gate[b] >= 0.5
+ * (FP32 compare; NaN stays closed) and some budget is legal.  Gate-on images
+ * are numbered in image order, so the controller (encoder, budget head,
+ * selector) can run on them alone.
+ *
+ *   p_gate   fp32 [B], the gate probabilities.
+ *   cu_in    NULL (every image has N tokens) or int32 [B+1] segment offsets
+ *            of packed tokens (a later round); a segment with n_b outside
+ *            [1, N] keeps its gate closed and sets DORA_DEV_CU_IN.
+ *   B        1 .. 2^24 images; N 1 .. DORA_MAX_ROW_TOKENS; M >= 1.
+ *   on_rank  int32 [B] out: b's number among the gate-on images, -1 if closed.
+ *   on_list  int32 [B] out: on_list[r] = the gate-on image numbered r, for
+ *            r < n_on; -1 after that.
+ *   n_on     int32 [1] out (device): number of gate-on images.
+ *
+ * Returns DORA_OK or a negative dora_status; enqueues one single-workgroup
+ * kernel.
+ */
+int dora_actor_gate(const float* p_gate, const int32_t* cu_in, int32_t B, int32_t N, int32_t M,
+                    int32_t* on_rank, int32_t* on_list, int32_t* n_on, int32_t* dev_status, void* stream);
+
+/*
+ * dora_actor_decode -- budget and keep-scores of the deterministic actor
+ * (App. A.3: the legal budget with the largest logit; the k highest removal
+ * scores are deleted; Sec. 3.2, Eq. (2) for the scores).
+ *
+ *   budget_logits  fp32 [logit_rows, M]: row r holds the budget-head logits
+ *            of gate-on image on_list[r] (the controller's sub-batch order).
+ *            The budget of image b is k = 2(m + 1) for the m < (number of
+ *            legal budgets) with the largest logit: the first such m on ties,
+ *            a NaN logit above every number (the first NaN wins), as an
+ *            argmax with the illegal budgets masked out.
+ *   removal_scores, scores_out  fp32, both NULL or both given, in the score
+ *            layout of dora_select_pack ([B, N] dense, [total_in] packed):
+ *            scores_out = -removal_scores element by element (the keep-scores
+ *            dora_select_pack takes).  They may be the same buffer.
+ *   cu_in, total_in, B, N  as for dora_select_pack (cu_in NULL: dense).
+ *   on_rank  int32 [B] from dora_actor_gate.
+ *   keep_out int32 [B] out: n_b - k for a gate-on image, n_b for a gate-off
+ *            one (nothing removed); 0 with DORA_DEV_CU_IN for an invalid
+ *            segment; n_b with DORA_DEV_ACTOR for a gate-on image with no
+ *            legal budget or with on_rank[b] >= logit_rows.
+ *
+ * Returns DORA_OK or a negative dora_status; enqueues one kernel.
+ */
+int dora_actor_decode(const float* budget_logits, int64_t logit_rows, int32_t M, const float* removal_scores,
+                      const int32_t* cu_in, int64_t total_in, int32_t B, int32_t N, const int32_t* on_rank,
+                      int32_t* keep_out, float* scores_out, int32_t* dev_status, void* stream);
 
 /*
  * dora_varlen_attn_execute -- exact softmax attention inside each packed

@@ -43,6 +43,7 @@ DORA_DEV_CU_IN = 0x4
 DORA_DEV_CU_SEQLENS = 0x8
 DORA_DEV_PLAN = 0x10
 
+DORA_DEV_ACTOR = 0x20
 DORA_MAX_ROW_TOKENS = 2048
 DORA_MAX_SEQLEN = 16384
 DORA_HEAD_DIM = 64
@@ -51,6 +52,8 @@ EXPORTS = (
     "dora_select_pack",
     "dora_select_pack_plan",
     "dora_select_pack_residual",
+    "dora_actor_gate",
+    "dora_actor_decode",
     "dora_varlen_attn_workspace_size",
     "dora_varlen_attn_plan",
     "dora_varlen_attn_execute",
@@ -87,6 +90,10 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.dora_select_pack_residual.restype = ctypes.c_int
     lib.dora_select_pack_residual.argtypes = lib.dora_select_pack.argtypes[:3] + [vp] + \
         lib.dora_select_pack.argtypes[3:]
+    lib.dora_actor_gate.restype = ctypes.c_int
+    lib.dora_actor_gate.argtypes = [vp, vp, i32, i32, i32, vp, vp, vp, vp, vp]
+    lib.dora_actor_decode.restype = ctypes.c_int
+    lib.dora_actor_decode.argtypes = [vp, i64, i32, vp, vp, i64, i32, i32, vp, vp, vp, vp, vp]
     lib.dora_varlen_attn_workspace_size.restype = sz
     lib.dora_varlen_attn_workspace_size.argtypes = [i32, i32, i32]
     lib.dora_varlen_attn_plan.restype = ctypes.c_int
@@ -256,6 +263,72 @@ def dora_select_pack_residual(scores: torch.Tensor, keep: torch.Tensor, h: torch
     rc = lib.dora_select_pack_residual(*args, _dev(outs[3], "dev_status", torch.int32), _stream(stream))
     _check("dora_select_pack_residual", rc)
     return outs
+
+
+def dora_actor_gate(p_gate: torch.Tensor, M: int, N: int, cu_in: Optional[torch.Tensor] = None,
+                    on_rank: Optional[torch.Tensor] = None, on_list: Optional[torch.Tensor] = None,
+                    n_on: Optional[torch.Tensor] = None, dev_status: Optional[torch.Tensor] = None,
+                    stream=None) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor, torch.Tensor]:
+    """Gate decisions and the ordered list of gate-on images.  p_gate: fp32 [B];
+    N tokens per image (CLS included) or cu_in [B+1]; M budget-head outputs.
+    Returns (on_rank [B], on_list [B], n_on [1], dev_status)."""
+    B = int(p_gate.shape[0])
+    dev = p_gate.device
+    if cu_in is not None and tuple(cu_in.shape) != (B + 1,):
+        raise ValueError("cu_in must be [B+1]")
+    on_rank = torch.empty(B, dtype=torch.int32, device=dev) if on_rank is None else on_rank
+    on_list = torch.empty(B, dtype=torch.int32, device=dev) if on_list is None else on_list
+    n_on = torch.empty(1, dtype=torch.int32, device=dev) if n_on is None else n_on
+    dev_status = new_status(dev) if dev_status is None else dev_status
+    for t, name in ((on_rank, "on_rank"), (on_list, "on_list")):
+        if t.numel() < B:
+            raise ValueError(f"{name} needs {B} entries")
+    rc = load_library().dora_actor_gate(
+        _dev(p_gate, "p_gate", torch.float32), None if cu_in is None else _dev(cu_in, "cu_in", torch.int32),
+        B, int(N), int(M), _dev(on_rank, "on_rank", torch.int32), _dev(on_list, "on_list", torch.int32),
+        _dev(n_on, "n_on", torch.int32), _dev(dev_status, "dev_status", torch.int32), _stream(stream))
+    _check("dora_actor_gate", rc)
+    return on_rank, on_list, n_on, dev_status
+
+
+def dora_actor_decode(budget_logits: torch.Tensor, on_rank: torch.Tensor, N: int,
+                      removal_scores: Optional[torch.Tensor] = None, cu_in: Optional[torch.Tensor] = None,
+                      keep_out: Optional[torch.Tensor] = None, scores_out: Optional[torch.Tensor] = None,
+                      dev_status: Optional[torch.Tensor] = None,
+                      stream=None) -> Tuple[torch.Tensor, Optional[torch.Tensor], torch.Tensor]:
+    """Keep counts from the budget logits [rows, M] (row r = gate-on image r)
+    and, if removal_scores is given, keep-scores = -removal_scores in the same
+    layout.  Returns (keep [B], keep-scores or None, dev_status)."""
+    B = int(on_rank.shape[0])
+    dev = on_rank.device
+    if budget_logits.dim() != 2:
+        raise ValueError("budget_logits must be [rows, M]")
+    rows, M = int(budget_logits.shape[0]), int(budget_logits.shape[1])
+    keep_out = torch.empty(B, dtype=torch.int32, device=dev) if keep_out is None else keep_out
+    if removal_scores is not None and scores_out is None:
+        scores_out = torch.empty_like(removal_scores)
+    if (removal_scores is None) != (scores_out is None):
+        raise ValueError("removal_scores and scores_out go together")
+    if removal_scores is not None and scores_out.shape != removal_scores.shape:
+        raise ValueError("scores_out must have removal_scores' shape")
+    if cu_in is None:
+        total_in = B * int(N)
+        if removal_scores is not None and tuple(removal_scores.shape) != (B, int(N)):
+            raise ValueError("dense removal_scores must be [B,N]")
+    else:
+        if tuple(cu_in.shape) != (B + 1,):
+            raise ValueError("cu_in must be [B+1]")
+        total_in = int(removal_scores.shape[0]) if removal_scores is not None else 0
+    dev_status = new_status(dev) if dev_status is None else dev_status
+    rc = load_library().dora_actor_decode(
+        _dev(budget_logits, "budget_logits", torch.float32) if rows > 0 else None, rows, M,
+        None if removal_scores is None else _dev(removal_scores, "removal_scores", torch.float32),
+        None if cu_in is None else _dev(cu_in, "cu_in", torch.int32), total_in, B, int(N),
+        _dev(on_rank, "on_rank", torch.int32), _dev(keep_out, "keep_out", torch.int32),
+        None if scores_out is None else _dev(scores_out, "scores_out", torch.float32),
+        _dev(dev_status, "dev_status", torch.int32), _stream(stream))
+    _check("dora_actor_decode", rc)
+    return keep_out, scores_out, dev_status
 
 
 def dora_varlen_attn_workspace_size(B: int, H: int, max_seqlen: int) -> int:

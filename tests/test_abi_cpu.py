@@ -32,7 +32,7 @@ def test_library_exports_every_declared_symbol():
 def test_constants_match_header():
     text = open(HEADER).read()
     for name in ["DORA_DEV_KEEP_RANGE", "DORA_DEV_CAPACITY", "DORA_DEV_CU_IN", "DORA_DEV_CU_SEQLENS",
-                 "DORA_DEV_PLAN", "DORA_MAX_ROW_TOKENS", "DORA_MAX_SEQLEN", "DORA_HEAD_DIM"]:
+                 "DORA_DEV_PLAN", "DORA_DEV_ACTOR", "DORA_MAX_ROW_TOKENS", "DORA_MAX_SEQLEN", "DORA_HEAD_DIM"]:
         m = re.search(r"#define\s+%s\s+(0x[0-9a-fA-F]+|\d+)" % name, text)
         assert m and int(m.group(1), 0) == getattr(dora, name), name
     for name, val in re.findall(r"(DORA_(?:OK|ERR_[A-Z]+))\s*=\s*(-?\d+)", text):
@@ -91,6 +91,36 @@ def test_select_pack_residual_host_validation():
     assert call(dtype=7) == dora.DORA_ERR_DTYPE
     assert call(cap=0) == dora.DORA_ERR_CAPACITY
     assert call(N=dora.DORA_MAX_ROW_TOKENS + 1) == dora.DORA_ERR_SHAPE
+
+
+def test_actor_host_validation():
+    lib = dora.load_library()
+    def gate(**kw):
+        a = dict(p=FAKE, cu=None, B=4, N=197, M=96, rank=FAKE, lst=FAKE, n=FAKE, st=FAKE, s=None)
+        a.update(kw)
+        return lib.dora_actor_gate(*a.values())
+
+    assert gate(p=None) == dora.DORA_ERR_NULL
+    assert gate(n=None) == dora.DORA_ERR_NULL
+    assert gate(B=0) == dora.DORA_ERR_SHAPE
+    assert gate(B=(1 << 24) + 1) == dora.DORA_ERR_SHAPE
+    assert gate(M=0) == dora.DORA_ERR_SHAPE
+    assert gate(N=dora.DORA_MAX_ROW_TOKENS + 1) == dora.DORA_ERR_SHAPE
+
+    def dec(**kw):
+        a = dict(logits=FAKE, rows=4, M=96, rem=FAKE, cu=None, total=0, B=4, N=197, rank=FAKE, keep=FAKE,
+                 out=FAKE, st=FAKE, s=None)
+        a.update(kw)
+        return lib.dora_actor_decode(*a.values())
+
+    assert dec(rank=None) == dora.DORA_ERR_NULL
+    assert dec(keep=None) == dora.DORA_ERR_NULL
+    assert dec(out=None) == dora.DORA_ERR_NULL                       # scores in, no scores out
+    assert dec(logits=None) == dora.DORA_ERR_NULL                    # rows > 0 need logits
+    assert dec(rows=-1) == dora.DORA_ERR_SHAPE
+    assert dec(M=0) == dora.DORA_ERR_SHAPE
+    assert dec(B=0) == dora.DORA_ERR_SHAPE
+    assert dec(cu=FAKE, total=-1) == dora.DORA_ERR_SHAPE
 
 
 def call_select_plan(lib, **kw):

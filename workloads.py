@@ -18,7 +18,8 @@ Conventions
   ``numpy.random.default_rng([seed, round, part])`` with part 0..5 for
   keep, scores, tokens (first round only), Q, K, V, and part 6 for the
   attention branch's output that the residual variant adds to the tokens,
-  so any subset can be drawn without changing the others.
+  and parts 7-9 for the actor's gate probabilities, budget logits and
+  removal scores, so any subset can be drawn without changing the others.
 * Keep counts derived from a ratio r use ``clip(rint(r * n), 1, n)``.
 * bf16 values are the round-to-nearest-even truncation of the float32 draw,
   stored as raw ``uint16`` bit patterns.
@@ -201,6 +202,24 @@ def generate(w: Workload, seed: Optional[int] = None, batch: Optional[int] = Non
                                   attn_out=attn_out))
         n = keep.copy()
     return rounds
+
+
+def budget_outputs(w: Workload) -> int:
+    """Budget-head outputs M = (N0 - 4) / 2 for N0 = N - 1 visual tokens (App. A.2, Table 3)."""
+    return (w.N - 1 - 4) // 2
+
+
+def actor_outputs(w: Workload, seed: Optional[int] = None):
+    """Stand-ins for the trained actor's outputs on the first round of ``w``:
+    gate probabilities U[0, 1] [B], budget logits N(0, 1) [B, M] (one row per
+    image, enough for any number of gate-on images) and removal scores N(0, 1)
+    [B, N]; parts 7, 8, 9 of round 0's streams."""
+    sd = w.seed if seed is None else seed
+    M = budget_outputs(w)
+    p_gate = _rng(sd, 0, 7).uniform(0.0, 1.0, size=w.B).astype(np.float32)
+    logits = _rng(sd, 0, 8).standard_normal(size=(w.B, M), dtype=np.float32)
+    removal = _rng(sd, 0, 9).standard_normal(size=(w.B, w.N), dtype=np.float32)
+    return p_gate, logits, removal
 
 
 def random_qkv(rng: np.random.Generator, lens, H: int, dtype: str):
