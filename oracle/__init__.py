@@ -21,6 +21,10 @@ The arithmetic lives in ``dora_oracle.c`` (plain C, fp64 for attention):
   deployment"; App. A.2 legal budgets; App. A.3): gate at p >= 0.5 with a
   legal budget, gate-on images numbered in image order, the legal budget of
   the largest logit, keep = tokens - budget, keep-scores = -removal scores.
+* ``pl_sample`` / ``pl_logprob``: Plackett-Luce deletion by Gumbel-top-k
+  (keys = removal score + Gumbel noise in FP32, the k largest drawn in
+  decreasing key order) and the ordered log-probability of Eq.
+  (app-actor-pl) in fp64 (App. A.3), written as the definition reads.
 * ``varlen_attn`` is exact softmax attention inside each boundary
   (Sec. 3.5; App. E.5), computed as a dense fp64 score matrix per
   (image, head) from the exact values of the bf16 / fp32 inputs.
@@ -74,6 +78,13 @@ def load_library(path: str):
                                         ctypes.c_int32, ctypes.c_void_p]
     lib.oracle_negate.restype = None
     lib.oracle_negate.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+    lib.oracle_pl_sample.restype = ctypes.c_int
+    lib.oracle_pl_sample.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                     ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64]
+    lib.oracle_pl_logprob.restype = ctypes.c_int
+    lib.oracle_pl_logprob.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                      ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p]
     lib.oracle_round_to_format.restype = None
     lib.oracle_round_to_format.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p]
     lib.oracle_residual_add.restype = None
@@ -202,6 +213,52 @@ def negate(s: np.ndarray, lib=None) -> np.ndarray:
     out = np.empty_like(s)
     _load(lib).oracle_negate(_ptr(s), s.size, _ptr(out))
     return out
+
+
+def _pl_geometry(s, cu_in, B, N):
+    s = np.ascontiguousarray(s, dtype=np.float32)
+    if cu_in is None:
+        N = int(s.shape[1]) if N is None else N
+        return s, None, B * N, N
+    cu = np.ascontiguousarray(cu_in, dtype=np.int32)
+    if N is None:
+        N = int(np.max(np.diff(cu))) if B else 1
+    return s, cu, int(s.shape[0]), N
+
+
+def pl_sample(s: np.ndarray, g: np.ndarray, k: np.ndarray, cu_in: Optional[np.ndarray] = None,
+              N: Optional[int] = None, lib=None) -> Tuple[np.ndarray, np.ndarray, np.ndarray, int]:
+    """Plackett-Luce deletion by Gumbel-top-k: removal scores s and noise g
+    ([B,N] dense or [total_in] with cu_in), k [B] draws per image.  Returns
+    (order [sum k], cu_order [B+1], logprob [B] fp64, status)."""
+    k = np.ascontiguousarray(k, dtype=np.int32)
+    B = int(k.shape[0])
+    s, cu, total_in, N = _pl_geometry(s, cu_in, B, N)
+    g = np.ascontiguousarray(g, dtype=np.float32)
+    cap = int(np.clip(k.astype(np.int64), 0, None).sum())
+    order = np.zeros(max(cap, 1), np.int32)
+    cu_order = np.zeros(B + 1, np.int32)
+    lp = np.zeros(B, np.float64)
+    st = _load(lib).oracle_pl_sample(_ptr(s), _ptr(g), _ptr(k), _ptr(cu), total_in, B, int(N), _ptr(order),
+                                     _ptr(cu_order), _ptr(lp), cap)
+    if st:
+        return np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros(0), int(st)
+    return order[:cap], cu_order, lp, 0
+
+
+def pl_logprob(s: np.ndarray, order: np.ndarray, cu_order: np.ndarray, cu_in: Optional[np.ndarray] = None,
+               N: Optional[int] = None, lib=None) -> Tuple[np.ndarray, int]:
+    """Ordered Plackett-Luce log-probability (Eq. (app-actor-pl)) of given
+    drawing orders under removal scores s.  Returns (logprob [B], status)."""
+    cu_order = np.ascontiguousarray(cu_order, dtype=np.int32)
+    B = int(cu_order.shape[0]) - 1
+    s, cu, total_in, N = _pl_geometry(s, cu_in, B, N)
+    order = np.ascontiguousarray(order, dtype=np.int32)
+    if order.size == 0:
+        order = np.zeros(1, np.int32)
+    lp = np.zeros(B, np.float64)
+    st = _load(lib).oracle_pl_logprob(_ptr(s), _ptr(order), _ptr(cu_order), _ptr(cu), total_in, B, int(N), _ptr(lp))
+    return lp, int(st)
 
 
 def widen(x: np.ndarray, dtype: str) -> np.ndarray:

@@ -301,6 +301,138 @@ void oracle_negate(const float* s, int64_t n, float* out) {
   for (int64_t i = 0; i < n; ++i) out[i] = -s[i];
 }
 
+/* Removal order of the Plackett-Luce sample: "a before b" when a is drawn
+ * (removed) earlier.  This is the keep order of candidate_order on the
+ * keep-score -key, reversed, so that the drawn set is exactly what select +
+ * pack deletes with keep-scores -key: NaN keys first, then larger keys, equal
+ * keys (and NaN vs NaN) by descending position. */
+static int removal_order(const void* pa, const void* pb) {
+  const candidate* a = (const candidate*)pa;
+  const candidate* b = (const candidate*)pb;
+  int an = isnan(a->score), bn = isnan(b->score);
+  if (an != bn) return an ? -1 : 1;
+  if (!an) {
+    double x = (double)a->score, y = (double)b->score;
+    if (x > y) return -1;
+    if (x < y) return 1;
+  }
+  return (a->pos > b->pos) ? -1 : (a->pos < b->pos) ? 1 : 0;
+}
+
+/* Segment geometry shared by the Plackett-Luce functions; returns nonzero
+ * when cu_in is not a valid partition. */
+static int segments(const int32_t* cu_in, int64_t total_in, int32_t B, int32_t N, int64_t* off, int64_t* n) {
+  int bad = 0;
+  for (int32_t b = 0; b < B; ++b) {
+    if (cu_in) {
+      off[b] = cu_in[b];
+      n[b] = (int64_t)cu_in[b + 1] - cu_in[b];
+      if ((b == 0 && cu_in[0] != 0) || cu_in[b] < 0 || n[b] < 1 || n[b] > N || cu_in[b + 1] > total_in) bad = 1;
+    } else {
+      off[b] = (int64_t)b * N;
+      n[b] = N;
+    }
+  }
+  return bad;
+}
+
+/* Ordered Plackett-Luce log-probability (App. A.3, Eq. (app-actor-pl)) of
+ * drawing the visual positions order[0..k) in that order from one image's
+ * removal scores s[1..n) (position 0, CLS, never drawn):
+ *   sum_t [ s_{i_t} - log sum_{j in R_t} exp(s_j) ],
+ *   R_t = visual positions not drawn before step t,
+ * in fp64, each exp taken relative to the largest visual score (the same
+ * value, without overflow).  Scores are expected finite. */
+static double pl_logprob_one(const float* s, int64_t n, const int32_t* order, int32_t k) {
+  char* drawn = (char*)calloc((size_t)n, 1);
+  double m = -INFINITY;
+  for (int64_t j = 1; j < n; ++j) m = fmax(m, (double)s[j]);
+  double lp = 0.0;
+  for (int32_t t = 0; t < k; ++t) {
+    double z = 0.0;
+    for (int64_t j = 1; j < n; ++j)
+      if (!drawn[j]) z += exp((double)s[j] - m);
+    lp += ((double)s[order[t]] - m) - log(z);
+    drawn[order[t]] = 1;
+  }
+  free(drawn);
+  return lp;
+}
+
+/*
+ * Plackett-Luce deletion by Gumbel-top-k (Sec. 3.2 "Sampling and deployment";
+ * App. A.3, Eq. (app-actor-pl)).  For image b with removal scores s and
+ * Gumbel noise g (same layout as the scores of oracle_select_pack; position 0
+ * is CLS and is never drawn), key_j = s_j + g_j in FP32, and the k[b] visual
+ * positions drawn are the first k[b] in removal_order of the keys: a
+ * Plackett-Luce sample without replacement over exp(s).
+ *   order_out : [sum k] drawn positions, image after image, in drawing order
+ *   cu_order  : [B+1] offsets of each image's list
+ *   logprob   : [B] ordered log-probability of the list under s (fp64)
+ * k[b] must lie in [0, n_b - 1].  Returns 0 or ORACLE_* bits (nothing written).
+ */
+int oracle_pl_sample(const float* s, const float* g, const int32_t* k, const int32_t* cu_in, int64_t total_in,
+                     int32_t B, int32_t N, int32_t* order_out, int32_t* cu_order, double* logprob, int64_t cap) {
+  int64_t* off = (int64_t*)malloc(sizeof(int64_t) * (size_t)(B > 0 ? B : 1));
+  int64_t* n = (int64_t*)malloc(sizeof(int64_t) * (size_t)(B > 0 ? B : 1));
+  int status = segments(cu_in, total_in, B, N, off, n) ? ORACLE_BAD_SEGMENTS : 0;
+  int64_t total = 0;
+  for (int32_t b = 0; b < B; ++b) {
+    if (k[b] < 0 || k[b] > n[b] - 1) status |= ORACLE_BAD_KEEP;
+    total += k[b];
+  }
+  if (total > cap) status |= ORACLE_OVERFLOW;
+  if (status) {
+    free(off);
+    free(n);
+    return status;
+  }
+  cu_order[0] = 0;
+  for (int32_t b = 0; b < B; ++b) cu_order[b + 1] = cu_order[b] + k[b];
+  candidate* cand = (candidate*)malloc(sizeof(candidate) * (size_t)(N > 0 ? N : 1));
+  for (int32_t b = 0; b < B; ++b) {
+    const float* sb = s + off[b];
+    const float* gb = g + off[b];
+    for (int64_t j = 1; j < n[b]; ++j) {
+      const float key = sb[j] + gb[j]; /* FP32 sum */
+      cand[j - 1].score = key;
+      cand[j - 1].pos = (int32_t)j;
+    }
+    qsort(cand, (size_t)(n[b] - 1), sizeof(candidate), removal_order);
+    int32_t* ob = order_out + cu_order[b];
+    for (int32_t t = 0; t < k[b]; ++t) ob[t] = cand[t].pos;
+    logprob[b] = pl_logprob_one(sb, n[b], ob, k[b]);
+  }
+  free(cand);
+  free(off);
+  free(n);
+  return 0;
+}
+
+/* Ordered log-probability of given drawing orders (the same action scored
+ * under another policy's scores): order/cu_order as written by
+ * oracle_pl_sample. */
+int oracle_pl_logprob(const float* s, const int32_t* order, const int32_t* cu_order, const int32_t* cu_in,
+                      int64_t total_in, int32_t B, int32_t N, double* logprob) {
+  int64_t* off = (int64_t*)malloc(sizeof(int64_t) * (size_t)(B > 0 ? B : 1));
+  int64_t* n = (int64_t*)malloc(sizeof(int64_t) * (size_t)(B > 0 ? B : 1));
+  int status = segments(cu_in, total_in, B, N, off, n) ? ORACLE_BAD_SEGMENTS : 0;
+  for (int32_t b = 0; b < B && !status; ++b) {
+    const int32_t kb = cu_order[b + 1] - cu_order[b];
+    if (kb < 0 || kb > n[b] - 1) status |= ORACLE_BAD_KEEP;
+    for (int32_t t = 0; t < kb && !status; ++t) {
+      const int32_t j = order[cu_order[b] + t];
+      if (j < 1 || j >= n[b]) status |= ORACLE_BAD_KEEP;
+    }
+  }
+  if (!status)
+    for (int32_t b = 0; b < B; ++b)
+      logprob[b] = pl_logprob_one(s + off[b], n[b], order + cu_order[b], cu_order[b + 1] - cu_order[b]);
+  free(off);
+  free(n);
+  return status;
+}
+
 int oracle_max_threads(void) {
 #ifdef _OPENMP
   return omp_get_max_threads();

@@ -5,6 +5,7 @@ term) into a copy of the oracle's C source, builds it on the CPU, and checks
 that the brute-force / library pins reject the mutant while the unmodified
 source passes the same battery.
 """
+import itertools
 import os
 import subprocess
 
@@ -18,8 +19,8 @@ from test_oracle_select import brute_keep_masks, masks_from_idx
 SRC = os.path.join(os.path.dirname(oracle.__file__), "dora_oracle.c")
 
 MUTANTS = {
-    "score_direction": ("if (x > y) return -1;\n    if (x < y) return 1;",
-                        "if (x < y) return -1;\n    if (x > y) return 1;"),
+    "score_direction": ("if (x > y) return -1;\n    if (x < y) return 1;\n  }\n  return (a->pos < b->pos)",
+                        "if (x < y) return -1;\n    if (x > y) return 1;\n  }\n  return (a->pos < b->pos)"),
     "tie_direction": ("return (a->pos < b->pos) ? -1 : (a->pos > b->pos) ? 1 : 0;",
                       "return (a->pos > b->pos) ? -1 : (a->pos < b->pos) ? 1 : 0;"),
     "nan_on_top": ("if (an != bn) return an ? 1 : -1;", "if (an != bn) return an ? -1 : 1;"),
@@ -60,7 +61,61 @@ MUTANTS = {
     "rank_not_compacted": ("on_rank[b] = open ? r : -1;", "on_rank[b] = open ? b : -1;"),
     "gate_off_drops_one": ("keep[b] = n_tok[b];\n      continue;", "keep[b] = n_tok[b] - 1;\n      continue;"),
     "negate_magnitude": ("out[i] = -s[i];", "out[i] = -fabsf(s[i]);"),
+    "gumbel_subtracted": ("const float key = sb[j] + gb[j];", "const float key = sb[j] - gb[j];"),
+    "draw_smallest_key_first": ("if (x > y) return -1;\n    if (x < y) return 1;\n  }\n  return (a->pos > b->pos)",
+                                "if (x < y) return -1;\n    if (x > y) return 1;\n  }\n  return (a->pos > b->pos)"),
+    "draw_ties_by_lower_position": ("return (a->pos > b->pos) ? -1 : (a->pos < b->pos) ? 1 : 0;",
+                                    "return (a->pos < b->pos) ? -1 : (a->pos > b->pos) ? 1 : 0;"),
+    "draw_nan_last": ("if (an != bn) return an ? -1 : 1;", "if (an != bn) return an ? 1 : -1;"),
+    "cls_in_denominator": ("for (int64_t j = 1; j < n; ++j)\n      if (!drawn[j])",
+                           "for (int64_t j = 0; j < n; ++j)\n      if (!drawn[j])"),
+    "denominator_keeps_drawn": ("if (!drawn[j]) z += exp((double)s[j] - m);", "z += exp((double)s[j] - m);"),
+    "denominator_without_log": ("lp += ((double)s[order[t]] - m) - log(z);", "lp += ((double)s[order[t]] - m) - z;"),
+    "drawn_never_marked": ("drawn[order[t]] = 1;", ""),
 }
+
+
+def pl_battery(lib, rng):
+    """Plackett-Luce pins: all orders sum to one, k = 1 is log_softmax, lexsort order,
+    select/pack consistency, sampled frequencies."""
+    failed = []
+    s5 = np.array([0.0, 1.0, -0.5, 0.3, 2.0], np.float32)
+    orders = list(itertools.permutations(range(1, 5), 3))
+    lp, st = oracle.pl_logprob(np.tile(s5, (len(orders), 1)), np.array(orders, np.int32).reshape(-1),
+                               (np.arange(len(orders) + 1) * 3).astype(np.int32), lib=lib)
+    if st or abs(np.exp(lp).sum() - 1.0) > 1e-12:
+        failed.append("pl mass")
+    B, n = 200, 30
+    s = (rng.standard_normal((B, n)) * 2).astype(np.float32)
+    o1 = rng.integers(1, n, B).astype(np.int32)
+    lp1, _ = oracle.pl_logprob(s, o1, np.arange(B + 1, dtype=np.int32), lib=lib)
+    ls = torch.log_softmax(torch.from_numpy(s[:, 1:].astype(np.float64)), dim=1).numpy()
+    if not np.allclose(lp1, ls[np.arange(B), o1 - 1], rtol=0, atol=1e-12):
+        failed.append("pl log_softmax")
+    g = rng.choice(np.array([0.0, 0.5, -0.0, 1.5], np.float32), (B, n))
+    s[::7, 4] = np.nan
+    s[::5] = np.round(s[::5])
+    k = rng.integers(0, n, B).astype(np.int32)
+    order, cu, _, st = oracle.pl_sample(s, g, k, lib=lib)
+    if st:
+        return failed + ["pl status"]
+    key = s + g
+    pos = np.arange(1, n)
+    for b in range(B):
+        kb = key[b, 1:]
+        nan_first = np.lexsort((-pos, np.where(np.isnan(kb), 0.0, -kb), ~np.isnan(kb)))
+        if not np.array_equal(order[cu[b]:cu[b + 1]], pos[nan_first][:k[b]]):
+            failed.append("pl order")
+            break
+    # frequencies of the first draw against softmax
+    Bs = 60000
+    gs = rng.gumbel(size=(Bs, 5)).astype(np.float32)
+    o, c, _, _ = oracle.pl_sample(np.tile(s5, (Bs, 1)), gs, np.ones(Bs, np.int32), lib=lib)
+    p = np.exp(s5[1:]) / np.exp(s5[1:]).sum()
+    freq = np.bincount(o, minlength=5)[1:] / Bs
+    if np.any(np.abs(freq - p) > 5 * np.sqrt(p * (1 - p) / Bs)):
+        failed.append("pl frequencies")
+    return failed
 
 
 def actor_battery(lib, rng):
@@ -166,7 +221,7 @@ def battery(lib):
     want = want.transpose(1, 2).numpy()
     if any(np.max(np.abs(got[cuq[b]:cuq[b + 1]] - want[b, :lens[b]])) > 1e-12 for b in range(len(lens))):
         failed.append("attention")
-    return failed + residual_battery(lib, rng) + actor_battery(lib, rng)
+    return failed + residual_battery(lib, rng) + actor_battery(lib, rng) + pl_battery(lib, rng)
 
 
 def test_unmodified_source_passes(tmp_path):
