@@ -260,6 +260,60 @@ int dora_actor_decode(const float* budget_logits, int64_t logit_rows, int32_t M,
                       int32_t* keep_out, float* scores_out, int32_t* dev_status, void* stream);
 
 /*
+ * dora_pl_sample -- Plackett-Luce deletion by Gumbel-top-k, with the ordered
+ * log-probability of the draw (Sec. 3.2 "Sampling and deployment": training
+ * draws exactly k distinct tokens without replacement and keeps the order;
+ * App. A.3, Eq. (app-actor-pl)).
+ *
+ * For image b (segment as in dora_select_pack; position 0 is CLS and is never
+ * drawn): key_j = scores_j + gumbel_j in FP32 for the visual positions, and
+ * the k[b] positions drawn are the first k[b] in decreasing key order (NaN
+ * keys first, equal keys by higher position: the order in which
+ * dora_select_pack with keep-scores -key and keep = n_b - k[b] deletes).
+ * With gumbel i.i.d. standard Gumbel noise this is a Plackett-Luce sample
+ * over exp(scores).  logprob_out[b] = sum_t [ s_{i_t} - log sum_{j in R_t}
+ * exp(s_j) ] over the draws i_1..i_k, R_t the visual positions not drawn
+ * before step t, in fp32 (each exp relative to the largest visual score).
+ *
+ *   scores     fp32 removal scores (higher = remove; Sec. 3.2, Eq. (2)),
+ *              [B, N] dense (cu_in NULL) or [total_in] packed.  Finite.
+ *   gumbel     fp32, the noise, same layout (the caller draws it).
+ *   k          int32 [B], 0 .. n_b - 1.
+ *   order_out  int32 [cap]: the draws of image b, in drawing order, at
+ *              [cu_order_out[b], cu_order_out[b+1]); positions local to the
+ *              segment (1 .. n_b - 1).
+ *   cu_order_out  int32 [B+1]: running total of k.
+ *   logprob_out   fp32 [B].
+ *   B 1 .. 8192; N 1 .. DORA_MAX_ROW_TOKENS; cap 1 .. 2^31-1.
+ *   dev_status DORA_DEV_KEEP_RANGE for a k[b] outside [0, n_b - 1] (its
+ *              slots are left unwritten, logprob NaN), DORA_DEV_CU_IN for an
+ *              invalid segment, DORA_DEV_CAPACITY when sum k > cap (draws at
+ *              or past cap are not written).
+ *
+ * Returns DORA_OK or a negative dora_status; enqueues one kernel.
+ */
+int dora_pl_sample(const float* scores, const float* gumbel, const int32_t* k, const int32_t* cu_in,
+                   int64_t total_in, int32_t B, int32_t N, int32_t* order_out, int32_t* cu_order_out,
+                   float* logprob_out, int64_t cap, int32_t* dev_status, void* stream);
+
+/*
+ * dora_pl_logprob -- the ordered log-probability of given draws under
+ * (other) scores (App. A.3: the same action is scored under the old and the
+ * new policy), as in dora_pl_sample.
+ *
+ *   order, cu_order  as written by dora_pl_sample (order holds cu_order[B]
+ *              entries): distinct visual positions per image.
+ *   logprob_out fp32 [B]; NaN with DORA_DEV_KEEP_RANGE when an image's list
+ *              is longer than n_b - 1, repeats a position or holds one outside
+ *              1 .. n_b - 1.
+ * Other arguments as for dora_pl_sample.  Returns DORA_OK or a negative
+ * dora_status; enqueues one kernel.
+ */
+int dora_pl_logprob(const float* scores, const int32_t* order, const int32_t* cu_order, const int32_t* cu_in,
+                    int64_t total_in, int32_t B, int32_t N, float* logprob_out, int32_t* dev_status,
+                    void* stream);
+
+/*
  * dora_varlen_attn_execute -- exact softmax attention inside each packed
  * sequence (Sec. 3.5 "Inference"; App. E.5): for every sequence b and head h
  *   O_b,h = softmax(softmax_scale * Q_b,h K_b,h^T) V_b,h

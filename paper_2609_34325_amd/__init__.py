@@ -54,6 +54,8 @@ EXPORTS = (
     "dora_select_pack_residual",
     "dora_actor_gate",
     "dora_actor_decode",
+    "dora_pl_sample",
+    "dora_pl_logprob",
     "dora_varlen_attn_workspace_size",
     "dora_varlen_attn_plan",
     "dora_varlen_attn_execute",
@@ -94,6 +96,10 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.dora_actor_gate.argtypes = [vp, vp, i32, i32, i32, vp, vp, vp, vp, vp]
     lib.dora_actor_decode.restype = ctypes.c_int
     lib.dora_actor_decode.argtypes = [vp, i64, i32, vp, vp, i64, i32, i32, vp, vp, vp, vp, vp]
+    lib.dora_pl_sample.restype = ctypes.c_int
+    lib.dora_pl_sample.argtypes = [vp, vp, vp, vp, i64, i32, i32, vp, vp, vp, i64, vp, vp]
+    lib.dora_pl_logprob.restype = ctypes.c_int
+    lib.dora_pl_logprob.argtypes = [vp, vp, vp, vp, i64, i32, i32, vp, vp, vp]
     lib.dora_varlen_attn_workspace_size.restype = sz
     lib.dora_varlen_attn_workspace_size.argtypes = [i32, i32, i32]
     lib.dora_varlen_attn_plan.restype = ctypes.c_int
@@ -329,6 +335,68 @@ def dora_actor_decode(budget_logits: torch.Tensor, on_rank: torch.Tensor, N: int
         _dev(dev_status, "dev_status", torch.int32), _stream(stream))
     _check("dora_actor_decode", rc)
     return keep_out, scores_out, dev_status
+
+
+def _pl_geometry(scores, B, cu_in, N):
+    if cu_in is None:
+        if scores.dim() != 2 or int(scores.shape[0]) != B:
+            raise ValueError("dense scores must be [B,N]")
+        return int(scores.shape[1]), B * int(scores.shape[1])
+    if tuple(cu_in.shape) != (B + 1,) or scores.dim() != 1:
+        raise ValueError("packed scores must be [total_in] with cu_in [B+1]")
+    if N is None:
+        raise ValueError("packed input needs N (an upper bound on segment lengths)")
+    return int(N), int(scores.shape[0])
+
+
+def dora_pl_sample(scores: torch.Tensor, gumbel: torch.Tensor, k: torch.Tensor,
+                   cu_in: Optional[torch.Tensor] = None, N: Optional[int] = None,
+                   order_out: Optional[torch.Tensor] = None, cu_order_out: Optional[torch.Tensor] = None,
+                   logprob_out: Optional[torch.Tensor] = None, cap: Optional[int] = None,
+                   dev_status: Optional[torch.Tensor] = None, stream=None):
+    """Gumbel-top-k Plackett-Luce draws of k[b] visual tokens per image (removal
+    scores + noise), in drawing order, and their ordered log-probability.
+    Returns (order [cap], cu_order [B+1], logprob [B], dev_status)."""
+    B = int(k.shape[0])
+    N, total_in = _pl_geometry(scores, B, cu_in, N)
+    if gumbel.shape != scores.shape:
+        raise ValueError("gumbel must have the scores' shape")
+    dev = scores.device
+    cap = (int(order_out.numel()) if order_out is not None else B * max(N - 1, 1)) if cap is None else cap
+    order_out = torch.empty(cap, dtype=torch.int32, device=dev) if order_out is None else order_out
+    cu_order_out = torch.empty(B + 1, dtype=torch.int32, device=dev) if cu_order_out is None else cu_order_out
+    logprob_out = torch.empty(B, dtype=torch.float32, device=dev) if logprob_out is None else logprob_out
+    dev_status = new_status(dev) if dev_status is None else dev_status
+    if order_out.numel() < cap:
+        raise ValueError("order_out smaller than cap")
+    rc = load_library().dora_pl_sample(
+        _dev(scores, "scores", torch.float32), _dev(gumbel, "gumbel", torch.float32), _dev(k, "k", torch.int32),
+        None if cu_in is None else _dev(cu_in, "cu_in", torch.int32), total_in, B, N,
+        _dev(order_out, "order_out", torch.int32), _dev(cu_order_out, "cu_order_out", torch.int32),
+        _dev(logprob_out, "logprob_out", torch.float32), int(cap), _dev(dev_status, "dev_status", torch.int32),
+        _stream(stream))
+    _check("dora_pl_sample", rc)
+    return order_out, cu_order_out, logprob_out, dev_status
+
+
+def dora_pl_logprob(scores: torch.Tensor, order: torch.Tensor, cu_order: torch.Tensor,
+                    cu_in: Optional[torch.Tensor] = None, N: Optional[int] = None,
+                    logprob_out: Optional[torch.Tensor] = None, dev_status: Optional[torch.Tensor] = None,
+                    stream=None):
+    """Ordered log-probability of given draws (order, cu_order) under scores.
+    Returns (logprob [B], dev_status)."""
+    B = int(cu_order.shape[0]) - 1
+    N, total_in = _pl_geometry(scores, B, cu_in, N)
+    dev = scores.device
+    logprob_out = torch.empty(B, dtype=torch.float32, device=dev) if logprob_out is None else logprob_out
+    dev_status = new_status(dev) if dev_status is None else dev_status
+    rc = load_library().dora_pl_logprob(
+        _dev(scores, "scores", torch.float32), _dev(order, "order", torch.int32),
+        _dev(cu_order, "cu_order", torch.int32), None if cu_in is None else _dev(cu_in, "cu_in", torch.int32),
+        total_in, B, N, _dev(logprob_out, "logprob_out", torch.float32),
+        _dev(dev_status, "dev_status", torch.int32), _stream(stream))
+    _check("dora_pl_logprob", rc)
+    return logprob_out, dev_status
 
 
 def dora_varlen_attn_workspace_size(B: int, H: int, max_seqlen: int) -> int:

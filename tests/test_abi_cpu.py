@@ -123,6 +123,33 @@ def test_actor_host_validation():
     assert dec(cu=FAKE, total=-1) == dora.DORA_ERR_SHAPE
 
 
+def test_pl_host_validation():
+    lib = dora.load_library()
+
+    def smp(**kw):
+        a = dict(s=FAKE, g=FAKE, k=FAKE, cu=None, total=0, B=4, N=197, order=FAKE, cuo=FAKE, lp=FAKE, cap=100,
+                 st=FAKE, stream=None)
+        a.update(kw)
+        return lib.dora_pl_sample(*a.values())
+
+    def lpr(**kw):
+        a = dict(s=FAKE, order=FAKE, cuo=FAKE, cu=None, total=0, B=4, N=197, lp=FAKE, st=FAKE, stream=None)
+        a.update(kw)
+        return lib.dora_pl_logprob(*a.values())
+
+    assert smp(s=None) == dora.DORA_ERR_NULL
+    assert smp(g=None) == dora.DORA_ERR_NULL
+    assert smp(lp=None) == dora.DORA_ERR_NULL
+    assert smp(B=0) == dora.DORA_ERR_SHAPE
+    assert smp(B=8193) == dora.DORA_ERR_SHAPE
+    assert smp(N=dora.DORA_MAX_ROW_TOKENS + 1) == dora.DORA_ERR_SHAPE
+    assert smp(cu=FAKE, total=-1) == dora.DORA_ERR_SHAPE
+    assert smp(cap=0) == dora.DORA_ERR_CAPACITY
+    assert lpr(order=None) == dora.DORA_ERR_NULL
+    assert lpr(cuo=None) == dora.DORA_ERR_NULL
+    assert lpr(N=0) == dora.DORA_ERR_SHAPE
+
+
 def call_select_plan(lib, **kw):
     ws = dora.dora_varlen_attn_workspace_size(4, 3, 197)
     a = dict(scores=FAKE, keep=FAKE, tokens=FAKE, cu_in=None, total_in=0, B=4, N=197, C=768, dtype=1,
