@@ -25,6 +25,9 @@ The arithmetic lives in ``dora_oracle.c`` (plain C, fp64 for attention):
   (keys = removal score + Gumbel noise in FP32, the k largest drawn in
   decreasing key order) and the ordered log-probability of Eq.
   (app-actor-pl) in fp64 (App. A.3), written as the definition reads.
+* ``lc1_readout``: the DINOv2 LC1 readout input on pruned tokens (App. E.3):
+  LayerNorm of CLS next to the mean of the LayerNorms of the surviving
+  visual tokens, per packed sequence, in fp64.
 * ``varlen_attn`` is exact softmax attention inside each boundary
   (Sec. 3.5; App. E.5), computed as a dense fp64 score matrix per
   (image, head) from the exact values of the bf16 / fp32 inputs.
@@ -85,6 +88,9 @@ def load_library(path: str):
     lib.oracle_pl_logprob.restype = ctypes.c_int
     lib.oracle_pl_logprob.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                       ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p]
+    lib.oracle_lc1_readout.restype = None
+    lib.oracle_lc1_readout.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_double, ctypes.c_void_p]
     lib.oracle_round_to_format.restype = None
     lib.oracle_round_to_format.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p]
     lib.oracle_residual_add.restype = None
@@ -259,6 +265,23 @@ def pl_logprob(s: np.ndarray, order: np.ndarray, cu_order: np.ndarray, cu_in: Op
     lp = np.zeros(B, np.float64)
     st = _load(lib).oracle_pl_logprob(_ptr(s), _ptr(order), _ptr(cu_order), _ptr(cu), total_in, B, int(N), _ptr(lp))
     return lp, int(st)
+
+
+def lc1_readout(x: np.ndarray, cu: np.ndarray, gamma: np.ndarray, beta: np.ndarray, eps: float, dtype: str,
+                lib=None) -> np.ndarray:
+    """[B, 2C] fp64: LayerNorm of each image's CLS row next to the mean of the
+    LayerNorms of its other rows (App. E.3, DINOv2 LC1 readout).  x: packed
+    [total, C] bf16 bits or fp32; gamma, beta: fp32 [C]."""
+    xd = np.ascontiguousarray(widen(x, dtype))
+    total, C = xd.shape
+    cu = np.ascontiguousarray(cu, dtype=np.int32)
+    B = int(cu.shape[0]) - 1
+    g = np.ascontiguousarray(np.asarray(gamma, np.float32).astype(np.float64))
+    bt = np.ascontiguousarray(np.asarray(beta, np.float32).astype(np.float64))
+    out = np.zeros((B, 2 * C))
+    with np.errstate(invalid="ignore"):
+        _load(lib).oracle_lc1_readout(_ptr(xd), _ptr(cu), B, C, _ptr(g), _ptr(bt), float(eps), _ptr(out))
+    return out
 
 
 def widen(x: np.ndarray, dtype: str) -> np.ndarray:

@@ -433,6 +433,45 @@ int oracle_pl_logprob(const float* s, const int32_t* order, const int32_t* cu_or
   return status;
 }
 
+/* LayerNorm of one row of C values (biased variance, eps inside the square
+ * root, then the affine gamma, beta), in fp64. */
+static void layer_norm_row(const double* x, int32_t C, const double* gamma, const double* beta, double eps,
+                           double* y) {
+  double mu = 0.0, var = 0.0;
+  for (int32_t c = 0; c < C; ++c) mu += x[c];
+  mu /= C;
+  for (int32_t c = 0; c < C; ++c) var += (x[c] - mu) * (x[c] - mu);
+  var /= C;
+  const double r = 1.0 / sqrt(var + eps);
+  for (int32_t c = 0; c < C; ++c) y[c] = (x[c] - mu) * r * gamma[c] + beta[c];
+}
+
+/*
+ * Readout input of a DINOv2 linear classifier on pruned tokens (App. E.3
+ * "Baseline implementations": the LC1 readout joins the normalised CLS token
+ * with the mean of the normalised surviving visual tokens).  For image b with
+ * packed rows [cu[b], cu[b+1]) (the first row is CLS):
+ *   out[b, 0:C]  = LayerNorm(x_CLS)
+ *   out[b, C:2C] = mean over the other rows of LayerNorm(x_j)
+ * (0/0 = NaN when only CLS survives).  x holds the exact values, fp64.
+ */
+void oracle_lc1_readout(const double* x, const int32_t* cu, int32_t B, int32_t C, const double* gamma,
+                        const double* beta, double eps, double* out) {
+  double* y = (double*)malloc(sizeof(double) * (size_t)C);
+  for (int32_t b = 0; b < B; ++b) {
+    double* ob = out + (int64_t)b * 2 * C;
+    const int64_t r0 = cu[b], r1 = cu[b + 1];
+    layer_norm_row(x + r0 * C, C, gamma, beta, eps, ob);
+    for (int32_t c = 0; c < C; ++c) ob[C + c] = 0.0;
+    for (int64_t r = r0 + 1; r < r1; ++r) {
+      layer_norm_row(x + r * C, C, gamma, beta, eps, y);
+      for (int32_t c = 0; c < C; ++c) ob[C + c] += y[c];
+    }
+    for (int32_t c = 0; c < C; ++c) ob[C + c] /= (double)(r1 - r0 - 1);
+  }
+  free(y);
+}
+
 int oracle_max_threads(void) {
 #ifdef _OPENMP
   return omp_get_max_threads();

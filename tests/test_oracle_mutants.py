@@ -72,7 +72,31 @@ MUTANTS = {
     "denominator_keeps_drawn": ("if (!drawn[j]) z += exp((double)s[j] - m);", "z += exp((double)s[j] - m);"),
     "denominator_without_log": ("lp += ((double)s[order[t]] - m) - log(z);", "lp += ((double)s[order[t]] - m) - z;"),
     "drawn_never_marked": ("drawn[order[t]] = 1;", ""),
+    "variance_unbiased": ("  var /= C;", "  var /= (C - 1);"),
+    "eps_outside_root": ("const double r = 1.0 / sqrt(var + eps);", "const double r = 1.0 / (sqrt(var) + eps);"),
+    "variance_not_centred": ("var += (x[c] - mu) * (x[c] - mu);", "var += x[c] * x[c];"),
+    "mean_includes_cls": ("for (int64_t r = r0 + 1; r < r1; ++r) {", "for (int64_t r = r0; r < r1; ++r) {"),
+    "mean_over_all_rows": ("ob[C + c] /= (double)(r1 - r0 - 1);", "ob[C + c] /= (double)(r1 - r0);"),
+    "gamma_beta_swapped": ("y[c] = (x[c] - mu) * r * gamma[c] + beta[c];", "y[c] = (x[c] - mu) * r * beta[c] + gamma[c];"),
 }
+
+
+def lc1_battery(lib, rng):
+    """LC1 readout pin: torch layer_norm + mean in fp64."""
+    lens = np.array([2, 7, 40])
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    C = 48
+    x = (rng.standard_normal((int(cu[-1]), C)) * 2 + 1).astype(np.float32)
+    gamma = rng.uniform(0.5, 1.5, C).astype(np.float32)
+    beta = rng.standard_normal(C).astype(np.float32)
+    got = oracle.lc1_readout(x, cu, gamma, beta, 1e-6, "f32", lib=lib)
+    g, bt = torch.from_numpy(gamma.astype(np.float64)), torch.from_numpy(beta.astype(np.float64))
+    want = []
+    for i in range(len(lens)):
+        y = torch.nn.functional.layer_norm(torch.from_numpy(x[cu[i]:cu[i + 1]].astype(np.float64)), (C,), g, bt,
+                                           1e-6)
+        want.append(torch.cat([y[0], y[1:].mean(dim=0)]).numpy())
+    return [] if np.allclose(got, np.stack(want), rtol=0, atol=1e-12) else ["lc1"]
 
 
 def pl_battery(lib, rng):
@@ -221,7 +245,8 @@ def battery(lib):
     want = want.transpose(1, 2).numpy()
     if any(np.max(np.abs(got[cuq[b]:cuq[b + 1]] - want[b, :lens[b]])) > 1e-12 for b in range(len(lens))):
         failed.append("attention")
-    return failed + residual_battery(lib, rng) + actor_battery(lib, rng) + pl_battery(lib, rng)
+    return failed + residual_battery(lib, rng) + actor_battery(lib, rng) + pl_battery(lib, rng) + \
+        lc1_battery(lib, rng)
 
 
 def test_unmodified_source_passes(tmp_path):
