@@ -54,6 +54,12 @@ def residual_bytes(w: W.Workload, keep: np.ndarray, n_in: np.ndarray) -> int:
     return 3 * sk * w.C * w.elt + 4 * (int(n_in.sum()) + sk + 2 * w.B + 1)
 
 
+def lc1_bytes(w: W.Workload, keep: np.ndarray) -> int:
+    """Algorithmic HBM bytes of the LC1 readout input: read every packed row
+    once, cu_seqlens, gamma and beta; write B x 2C fp32."""
+    return int(keep.sum()) * w.C * w.elt + 4 * (w.B + 1) + 8 * w.C + 8 * w.B * w.C
+
+
 def attn_flops(w: W.Workload, keep: np.ndarray) -> float:
     k = keep.astype(np.float64)
     return 4.0 * w.H * W.HEAD_DIM * float(np.sum(k * k))
@@ -63,13 +69,16 @@ def attn_bytes(w: W.Workload, keep: np.ndarray) -> int:
     return 4 * int(keep.sum()) * w.H * W.HEAD_DIM * w.elt   # Q, K, V read once, O written once
 
 
-KERNEL_SOURCES = {"attn": "paper_2609_34325_amd/csrc/varlen_attn.hip",
+KERNEL_SOURCES = {"lc1": "paper_2609_34325_amd/csrc/lc1_readout.hip",
+                  "attn": "paper_2609_34325_amd/csrc/varlen_attn.hip",
                   "select_pack": "paper_2609_34325_amd/csrc/select_pack.hip",
                   "residual": "paper_2609_34325_amd/csrc/select_pack.hip"}
 KERNEL_NAMES = {"attn": ("attn_fwd_bf16_kernel", "attn_fwd_f32_kernel"),
                 "select_pack": ("select_pack_kernel",),
                 "residual": ("select_pack_residual_kernel",),
                 "actor": ("actor_gate_kernel", "actor_decode_kernel"),
+                "pl": ("pl_kernel",),
+                "lc1": ("lc1_readout_kernel",),
                 "plan": ("attn_plan_kernel",)}
 
 
@@ -329,6 +338,8 @@ def main() -> int:
                     help="also time the step rotating through this many buffer sets (cold MALL); <= 1: off")
     ap.add_argument("--no-peaks", action="store_true", help="skip measuring the copy and MFMA peaks")
     ap.add_argument("--no-actor", action="store_true", help="skip timing the actor decode (outside the step)")
+    ap.add_argument("--no-pl", action="store_true", help="skip timing the Plackett-Luce draw (outside the step)")
+    ap.add_argument("--no-lc1", action="store_true", help="skip timing the LC1 readout input (outside the step)")
     ap.add_argument("--no-residual", action="store_true",
                     help="skip timing select/pack after the attention residual (outside the step)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -511,6 +522,23 @@ def main() -> int:
     if args.cold_sets > 1:
         del cold_sets
 
+    def time_calls(fn):
+        """Median over repeats of the mean time of `steps` back-to-back calls
+        of fn (after `warmup` calls), HIP events at the two ends, in ms."""
+        for _ in range(args.warmup):
+            fn()
+        reps = []
+        for _ in range(args.repeats):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for _ in range(args.steps):
+                fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            reps.append(e0.elapsed_time(e1) / args.steps)
+        return sorted(reps)[len(reps) // 2]
+
     # Beside the path: the deterministic actor's decode that produces its
     # inputs (gate + compaction, then budget argmax, keep counts and
     # keep-scores), timed as a pair of launches.
@@ -532,25 +560,60 @@ def main() -> int:
             dora.dora_actor_decode(logits_d, on_rank, w.N, removal_scores=removal_d, keep_out=keep_d,
                                    scores_out=ks_d, dev_status=st_a, stream=stream)
 
-        for _ in range(args.warmup):
-            actor_pair()
-        reps = []
-        for rep in range(args.repeats):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            torch.cuda.synchronize()
-            e0.record(stream)
-            for _ in range(args.steps):
-                actor_pair()
-            e1.record(stream)
-            torch.cuda.synchronize()
-            reps.append(e0.elapsed_time(e1) / args.steps)
+        ms_actor = time_calls(actor_pair)
         assert int(st_a.item()) == 0, f"device status {int(st_a.item())}"
-        ms_actor = sorted(reps)[len(reps) // 2]
         actor = {"entries": ["dora_actor_gate", "dora_actor_decode"], "bound": "latency",
                  "us_per_pair": ms_actor * 1e3, "gate_on": int(n_on.item()), "M": M,
                  "note": "two small launches back to back; the cost is launch and dependency latency"}
         print(f"[bench] actor decode: {ms_actor * 1e3:.1f} us per gate+decode pair, "
               f"{actor['gate_on']} of {w.B} gates open", file=sys.stderr, flush=True)
+
+    # Beside the path: the LC1 readout input (LayerNorm + segmented mean over
+    # the packed rows of the same batch), an HBM-bound segmented reduction.
+    lc1 = None
+    if not args.no_lc1:
+        x_h, gamma_h, beta_h = W.readout_rows(w, r.keep)
+        cu_h = np.concatenate([[0], np.cumsum(r.keep)]).astype(np.int32)
+        x_d, cu_d, gamma_d, beta_d = dev(x_h), dev(cu_h), dev(gamma_h), dev(beta_h)
+        out_d = torch.empty((w.B, 2 * w.C), dtype=torch.float32, device="cuda")
+        st_l = dora.new_status()
+
+        def lc1_call():
+            dora.dora_lc1_readout(x_d, cu_d, gamma_d, beta_d, 1e-6, out=out_d, dev_status=st_l, stream=stream)
+
+        ms_lc1 = time_calls(lc1_call)
+        assert int(st_l.item()) == 0, f"device status {int(st_l.item())}"
+        lb = lc1_bytes(w, r.keep)
+        lc1 = {"entry": "dora_lc1_readout", "kernel": "lc1_readout_kernel", "bound": "hbm", "us": ms_lc1 * 1e3,
+               "achieved": lb / (ms_lc1 * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+               "frac": lb / (ms_lc1 * 1e-3) / 1e9 / HBM_PEAK_GBS, "algorithmic_bytes": lb, "regime": "warm"}
+        print(f"[bench] lc1 readout: {ms_lc1 * 1e3:.1f} us per launch ({lc1['achieved']:.0f} GB/s)",
+              file=sys.stderr, flush=True)
+        del x_d
+
+    # Beside the path: the training-time draw (Gumbel-top-k Plackett-Luce
+    # deletion of n - keep tokens per image, with its ordered log-probability).
+    pl = None
+    if not args.no_pl:
+        k_h = (r.n_in - r.keep).astype(np.int32)
+        g_h = W.gumbel_noise(w)
+        s_d, g_d, k_d = dev(r.scores), dev(g_h), dev(k_h)
+        order = torch.empty(int(k_h.sum()) + 1, dtype=torch.int32, device="cuda")
+        cu_o = torch.empty(w.B + 1, dtype=torch.int32, device="cuda")
+        lp_d = torch.empty(w.B, dtype=torch.float32, device="cuda")
+        st_p = dora.new_status()
+
+        def pl_call():
+            dora.dora_pl_sample(s_d, g_d, k_d, order_out=order, cu_order_out=cu_o, logprob_out=lp_d,
+                                dev_status=st_p, stream=stream)
+
+        ms_pl = time_calls(pl_call)
+        assert int(st_p.item()) == 0, f"device status {int(st_p.item())}"
+        pl = {"entry": "dora_pl_sample", "kernel": "pl_kernel", "bound": "latency", "us": ms_pl * 1e3,
+              "draws": int(k_h.sum()), "images": w.B,
+              "note": "one workgroup per image: LDS bitonic sort of the visual keys and a block scan"}
+        print(f"[bench] pl sample: {ms_pl * 1e3:.1f} us per launch ({int(k_h.sum())} draws)",
+              file=sys.stderr, flush=True)
 
     flops = attn_flops(w, r.keep)
     sp_bytes = select_pack_bytes(w, r.keep, r.n_in)
@@ -626,8 +689,15 @@ def main() -> int:
         if "copy_GBs" in peaks:
             residual["frac_of_measured_copy"] = residual["achieved"] / peaks["copy_GBs"]
         result["residual_select_pack"] = residual
+    if lc1 is not None:
+        lc1["traffic"] = traffic.get("lc1")
+        if "copy_GBs" in peaks:
+            lc1["frac_of_measured_copy"] = lc1["achieved"] / peaks["copy_GBs"]
+        result["lc1_readout"] = lc1
     if actor is not None:
         result["actor_decode"] = actor
+    if pl is not None:
+        result["pl_sample"] = pl
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         result["cpu_baseline"] = run_cpu_baseline(w, r)

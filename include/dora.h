@@ -314,6 +314,32 @@ int dora_pl_logprob(const float* scores, const int32_t* order, const int32_t* cu
                     void* stream);
 
 /*
+ * dora_lc1_readout -- readout input of a DINOv2 linear classifier on the
+ * packed, pruned tokens (App. E.3 "Baseline implementations": the LC1 readout
+ * joins the normalised CLS token with the mean of the normalised surviving
+ * visual tokens), fused with the backbone's final LayerNorm.  For sequence b
+ * (rows [cu_seqlens[b], cu_seqlens[b+1]) of x; the first is CLS):
+ *   LN(x_j)        = (x_j - mean(x_j)) / sqrt(var(x_j) + eps) * gamma + beta
+ *                    (mean and biased variance over the C channels)
+ *   out[b, 0:C]    = LN(x_CLS)
+ *   out[b, C:2C]   = mean of LN(x_j) over the sequence's other rows
+ *                    (NaN when only CLS survives).
+ * Arithmetic in fp32 from the exact input values.
+ *
+ *   x          dtype [total, C], 16-byte aligned; C * sizeof(dtype) a multiple
+ *              of 16 and at most 4096 bytes (else DORA_ERR_UNSUPPORTED).
+ *   cu_seqlens int32 [B+1]; a sequence that is empty or reaches past total
+ *              sets DORA_DEV_CU_SEQLENS and gets a NaN output row.
+ *   gamma, beta fp32 [C]; eps >= 0 (DINOv2: 1e-6).
+ *   out        fp32 [B, 2C].
+ *
+ * Returns DORA_OK or a negative dora_status; enqueues one kernel.
+ */
+int dora_lc1_readout(const void* x, const int32_t* cu_seqlens, int64_t total, int32_t B, int32_t C,
+                     dora_dtype dtype, const float* gamma, const float* beta, float eps, float* out,
+                     int32_t* dev_status, void* stream);
+
+/*
  * dora_varlen_attn_execute -- exact softmax attention inside each packed
  * sequence (Sec. 3.5 "Inference"; App. E.5): for every sequence b and head h
  *   O_b,h = softmax(softmax_scale * Q_b,h K_b,h^T) V_b,h

@@ -56,6 +56,7 @@ EXPORTS = (
     "dora_actor_decode",
     "dora_pl_sample",
     "dora_pl_logprob",
+    "dora_lc1_readout",
     "dora_varlen_attn_workspace_size",
     "dora_varlen_attn_plan",
     "dora_varlen_attn_execute",
@@ -100,6 +101,8 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.dora_pl_sample.argtypes = [vp, vp, vp, vp, i64, i32, i32, vp, vp, vp, i64, vp, vp]
     lib.dora_pl_logprob.restype = ctypes.c_int
     lib.dora_pl_logprob.argtypes = [vp, vp, vp, vp, i64, i32, i32, vp, vp, vp]
+    lib.dora_lc1_readout.restype = ctypes.c_int
+    lib.dora_lc1_readout.argtypes = [vp, vp, i64, i32, i32, ctypes.c_int, vp, vp, ctypes.c_float, vp, vp, vp]
     lib.dora_varlen_attn_workspace_size.restype = sz
     lib.dora_varlen_attn_workspace_size.argtypes = [i32, i32, i32]
     lib.dora_varlen_attn_plan.restype = ctypes.c_int
@@ -397,6 +400,28 @@ def dora_pl_logprob(scores: torch.Tensor, order: torch.Tensor, cu_order: torch.T
         _dev(dev_status, "dev_status", torch.int32), _stream(stream))
     _check("dora_pl_logprob", rc)
     return logprob_out, dev_status
+
+
+def dora_lc1_readout(x: torch.Tensor, cu_seqlens: torch.Tensor, gamma: torch.Tensor, beta: torch.Tensor,
+                     eps: float = 1e-6, out: Optional[torch.Tensor] = None,
+                     dev_status: Optional[torch.Tensor] = None, stream=None):
+    """LayerNorm of each packed sequence's CLS row next to the mean LayerNorm of
+    its other rows: x [total, C] bf16/fp32, cu_seqlens [B+1] -> out fp32 [B, 2C].
+    Returns (out, dev_status)."""
+    if x.dim() != 2:
+        raise ValueError("x must be [total, C]")
+    B = int(cu_seqlens.shape[0]) - 1
+    total, C = int(x.shape[0]), int(x.shape[1])
+    out = torch.empty((B, 2 * C), dtype=torch.float32, device=x.device) if out is None else out
+    dev_status = new_status(x.device) if dev_status is None else dev_status
+    if tuple(out.shape) != (B, 2 * C):
+        raise ValueError("out must be [B, 2C]")
+    rc = load_library().dora_lc1_readout(
+        _dev(x, "x"), _dev(cu_seqlens, "cu_seqlens", torch.int32), total, B, C, _dtype_code(x),
+        _dev(gamma, "gamma", torch.float32), _dev(beta, "beta", torch.float32), float(eps),
+        _dev(out, "out", torch.float32), _dev(dev_status, "dev_status", torch.int32), _stream(stream))
+    _check("dora_lc1_readout", rc)
+    return out, dev_status
 
 
 def dora_varlen_attn_workspace_size(B: int, H: int, max_seqlen: int) -> int:

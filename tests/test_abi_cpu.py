@@ -150,6 +150,26 @@ def test_pl_host_validation():
     assert lpr(N=0) == dora.DORA_ERR_SHAPE
 
 
+def test_lc1_host_validation():
+    lib = dora.load_library()
+
+    def call(**kw):
+        a = dict(x=FAKE, cu=FAKE, total=100, B=4, C=768, dtype=1, g=FAKE, b=FAKE, eps=1e-6, out=FAKE, st=FAKE,
+                 stream=None)
+        a.update(kw)
+        return lib.dora_lc1_readout(*a.values())
+
+    assert call(x=None) == dora.DORA_ERR_NULL
+    assert call(g=None) == dora.DORA_ERR_NULL
+    assert call(dtype=9) == dora.DORA_ERR_DTYPE
+    assert call(C=3) == dora.DORA_ERR_ALIGN
+    assert call(x=FAKE + 4) == dora.DORA_ERR_ALIGN
+    assert call(C=4096) == dora.DORA_ERR_UNSUPPORTED                 # 8 KB bf16 rows
+    assert call(B=0) == dora.DORA_ERR_SHAPE
+    assert call(total=0) == dora.DORA_ERR_SHAPE
+    assert call(eps=-1.0) == dora.DORA_ERR_SHAPE
+
+
 def call_select_plan(lib, **kw):
     ws = dora.dora_varlen_attn_workspace_size(4, 3, 197)
     a = dict(scores=FAKE, keep=FAKE, tokens=FAKE, cu_in=None, total_in=0, B=4, N=197, C=768, dtype=1,

@@ -1,0 +1,86 @@
+"""GPU parity for dora_lc1_readout against the fp64 oracle.
+
+The kernel computes in fp32; each image's outputs must lie within a bound
+derived from its arithmetic (`fp32_bound`): row sums of at most 32 values
+per lane plus a 6-level butterfly (38 roundings per element), the centred
+second moment likewise, the reciprocal square root and the affine step (a
+few roundings each), and the mean over the rows (at most n/8 sequential
+adds per wave, 8 across waves, one scale).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from gpu_util import to_dev
+
+pytestmark = pytest.mark.gpu
+
+U = 2.0 ** -24
+
+
+def fp32_bound(x64, cu, gamma, beta, eps):
+    tol = []
+    for b in range(len(cu) - 1):
+        r = x64[cu[b]:cu[b + 1]]
+        mu = r.mean(axis=1, keepdims=True)
+        rstd = 1.0 / np.sqrt(((r - mu) ** 2).mean(axis=1, keepdims=True) + eps)
+        a = np.abs((r - mu) * rstd * gamma)
+        y = np.abs(a) + np.abs(beta)
+        n = r.shape[0]
+        tol.append(U * (100 * a.max() + 40 * np.abs(r).max() * rstd.max() * np.abs(gamma).max()
+                        + (n / 8 + 14) * y.max()))
+    return np.array(tol)
+
+
+def compare(dora, x, cu, gamma, beta, dtype, eps=1e-6):
+    out, st = dora.dora_lc1_readout(to_dev(x), to_dev(cu), to_dev(gamma), to_dev(beta), eps)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    got = out.cpu().numpy().astype(np.float64)
+    want = oracle.lc1_readout(x, cu, gamma, beta, eps, dtype)
+    nan = np.isnan(want)
+    assert np.array_equal(np.isnan(got), nan)
+    tol = fp32_bound(oracle.widen(x, dtype), cu, gamma.astype(np.float64), beta.astype(np.float64), eps)
+    err = np.where(nan, 0.0, np.abs(got - want))
+    assert np.all(err <= tol[:, None]), (err.max(), tol.min())
+    return err.max()
+
+
+@pytest.mark.parametrize("C,dtype", [(768, "bf16"), (1024, "bf16"), (384, "bf16"), (192, "f32"), (64, "bf16"),
+                                     (2048, "bf16"), (1024, "f32"), (8, "bf16")])
+def test_ragged_sequences(gpu, C, dtype):
+    rng = np.random.default_rng(C)
+    lens = np.array([1, 2, 3, 8, 9, 16, 17, 31, 197, 257, 1000])
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    x = (rng.standard_normal((int(cu[-1]), C)) * rng.uniform(0.5, 2, C) + rng.standard_normal(C)).astype(np.float32)
+    xs = W.f32_to_bf16_bits(x) if dtype == "bf16" else x
+    gamma = rng.uniform(0.5, 1.5, C).astype(np.float32)
+    beta = (0.1 * rng.standard_normal(C)).astype(np.float32)
+    err = compare(gpu, xs, cu, gamma, beta, dtype)
+    print(f"[lc1] C={C} {dtype} max err {err:.2e}", flush=True)
+
+
+@pytest.mark.parametrize("name", ["dinov2_b14_bf16", "deit_b_bf16"])
+def test_workload_full_size(gpu, name):
+    w = W.WORKLOADS[name]
+    keep = W.generate(w, parts=("keep",))[0].keep
+    x, gamma, beta = W.readout_rows(w, keep)
+    cu = np.concatenate([[0], np.cumsum(keep)]).astype(np.int32)
+    err = compare(gpu, x, cu, gamma, beta, w.dtype)
+    print(f"[lc1] {name} max err {err:.2e}", flush=True)
+
+
+def test_invalid_sequences_set_status(gpu):
+    rng = np.random.default_rng(3)
+    C = 64
+    x = rng.standard_normal((20, C)).astype(np.float32)
+    g, b = np.ones(C, np.float32), np.zeros(C, np.float32)
+    for cu in ([0, 5, 5, 20], [0, 5, 21, 20], [1, 5, 10, 20]):
+        out, st = gpu.dora_lc1_readout(to_dev(x), to_dev(np.array(cu, np.int32)), to_dev(g), to_dev(b))
+        torch.cuda.synchronize()
+        o = out.cpu().numpy()
+        assert int(st.item()) & gpu.DORA_DEV_CU_SEQLENS, cu
+        bad = [i for i in range(3) if not (cu[i] >= 0 and cu[i + 1] > cu[i] and cu[i + 1] <= 20 and (i or cu[0] == 0))]
+        assert np.all(np.isnan(o[bad])), cu

@@ -5,7 +5,7 @@ arithmetic (no selection, packing or attention) and is shared by the tests,
 the benchmark and the oracle checks so that both sides of every parity
 comparison see the same bytes.
 
-The five workloads mirror the shapes of the paper's backbones (Sec. 4.1 and
+The six workloads mirror the shapes of the paper's backbones (Sec. 4.1 and
 Table 3: patch-16 ViTs with 196 visual tokens plus CLS, d = 768 for DeiT-B /
 ViT-B, d = 1024 for ViT-L) and the ragged, per-image keep counts that an
 input-adaptive pruning policy produces (Sec. 3.1, Fig. 3).  ImageNet images,
@@ -18,8 +18,9 @@ Conventions
   ``numpy.random.default_rng([seed, round, part])`` with part 0..5 for
   keep, scores, tokens (first round only), Q, K, V, and part 6 for the
   attention branch's output that the residual variant adds to the tokens,
-  and parts 7-9 for the actor's gate probabilities, budget logits and
-  removal scores, so any subset can be drawn without changing the others.
+  parts 7-9 for the actor's gate probabilities, budget logits and removal
+  scores, part 10 for Gumbel noise and part 11 for the readout rows, so
+  any subset can be drawn without changing the others.
 * Keep counts derived from a ratio r use ``clip(rint(r * n), 1, n)``.
 * bf16 values are the round-to-nearest-even truncation of the float32 draw,
   stored as raw ``uint16`` bit patterns.
@@ -87,6 +88,9 @@ WORKLOADS = {
         Workload("vit_b384_skew_bf16", 5, 64, 577, 12, "bf16", "bimodal_skew",
                  description="ViT-Base/384 shape, bf16, skewed: B=64, N=577, H=12, C=768, "
                              "half keep 90-100%, half keep 8-15%, scores with a spatial bump"),
+        Workload("dinov2_b14_bf16", 6, 256, 257, 12, "bf16", "ratio_beta43_0.3_1.0",
+                 description="DINOv2-B/14 shape, bf16: B=256, N=257 (256 patches + CLS), H=12, C=768, "
+                             "keep ratio 0.3+0.7*Beta(4,3)"),
     ]
 }
 
@@ -220,6 +224,29 @@ def actor_outputs(w: Workload, seed: Optional[int] = None):
     logits = _rng(sd, 0, 8).standard_normal(size=(w.B, M), dtype=np.float32)
     removal = _rng(sd, 0, 9).standard_normal(size=(w.B, w.N), dtype=np.float32)
     return p_gate, logits, removal
+
+
+def gumbel_noise(w: Workload, seed: Optional[int] = None) -> np.ndarray:
+    """Standard Gumbel noise [B, N] for a Plackett-Luce draw over the first
+    round's scores (part 10 of round 0's streams)."""
+    sd = w.seed if seed is None else seed
+    return _rng(sd, 0, 10).gumbel(size=(w.B, w.N)).astype(np.float32)
+
+
+def readout_rows(w: Workload, keep: np.ndarray, seed: Optional[int] = None):
+    """Packed final-block token rows [sum keep, C] for the LC1 readout, with a
+    per-channel offset N(0, 1) and scale U[0.5, 2] on N(0, 1) rows (residual
+    streams carry channel-wise biases), and LayerNorm gamma U[0.5, 1.5], beta
+    N(0, 0.1^2); part 11 of round 0's streams."""
+    sd = w.seed if seed is None else seed
+    rng = _rng(sd, 0, 11)
+    off = rng.standard_normal(w.C).astype(np.float32)
+    scale = rng.uniform(0.5, 2.0, w.C).astype(np.float32)
+    rows = rng.standard_normal((int(keep.astype(np.int64).sum()), w.C), dtype=np.float32) * scale + off
+    gamma = rng.uniform(0.5, 1.5, w.C).astype(np.float32)
+    beta = (0.1 * rng.standard_normal(w.C)).astype(np.float32)
+    x = rows.astype(np.float32)
+    return (x if w.dtype == "f32" else f32_to_bf16_bits(x)), gamma, beta
 
 
 def random_qkv(rng: np.random.Generator, lens, H: int, dtype: str):
