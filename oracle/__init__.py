@@ -28,6 +28,10 @@ The arithmetic lives in ``dora_oracle.c`` (plain C, fp64 for attention):
 * ``lc1_readout``: the DINOv2 LC1 readout input on pruned tokens (App. E.3):
   LayerNorm of CLS next to the mean of the LayerNorms of the surviving
   visual tokens, per packed sequence, in fp64.
+* ``trajectory_flops``: FLOPs of the complete forward along each image's
+  realised token trajectory (App. E.4): two per multiply-accumulate of the
+  patch embedding, every linear layer and the attention products, with the
+  actor's gate and controller where they run (App. A.1), in exact integers.
 * ``varlen_attn`` is exact softmax attention inside each boundary
   (Sec. 3.5; App. E.5), computed as a dense fp64 score matrix per
   (image, head) from the exact values of the bf16 / fp32 inputs.
@@ -281,6 +285,73 @@ def lc1_readout(x: np.ndarray, cu: np.ndarray, gamma: np.ndarray, beta: np.ndarr
     out = np.zeros((B, 2 * C))
     with np.errstate(invalid="ignore"):
         _load(lib).oracle_lc1_readout(_ptr(xd), _ptr(cu), B, C, _ptr(g), _ptr(bt), float(eps), _ptr(out))
+    return out
+
+
+# --- FLOP accounting of a realised token trajectory (App. E.4) -------------
+#
+# One multiply-accumulate counts as two FLOPs; counted are the products of
+# the linear layers, the patch-embedding convolution and the two attention
+# products (the paper's accounting also lists no other operation kind; see
+# the tests for how close this comes to its Native figures).
+
+def _attention_block_macs(n: int, d: int, r: int) -> Tuple[int, int]:
+    """MACs of one pre-LN Transformer block of width d over n tokens, split
+    into the attention part (QKV, Q K^T, P V, output projection) and the MLP
+    part (d -> r d -> d) per token."""
+    attn = n * d * 3 * d + n * n * d + n * n * d + n * d * d
+    mlp_per_token = d * r * d + r * d * d
+    return attn, mlp_per_token
+
+
+def actor_gate_macs(d: int, gate_hidden: int = 64, embed: int = 16, hist: int = 3) -> int:
+    """Gate MLP (d + 16 + 3) -> 64 -> 1 on the CLS key (App. A.1)."""
+    return (d + embed + hist) * gate_hidden + gate_hidden * 1
+
+
+def actor_controller_macs(n: int, d: int, M: int, width: int = 128, heads: int = 4, ffn: int = 256,
+                          budget_hidden: int = 128, sel_hidden: int = 64, hist: int = 3) -> int:
+    """Controller of a gate-on block over n tokens (CLS included; App. A.1):
+    input projection d -> 128 of every key and 3 -> 128 of the history into
+    CLS; one width-128 Transformer block (QKV, Q K^T, P V, projection, FFN
+    128 -> 256 -> 128); budget head 128 -> 128 -> M on CLS; the 1 -> 128
+    projection of k / N; selector 128 -> 64 -> 1 on the n - 1 visual tokens."""
+    enc_in = n * d * width + hist * width
+    attn, mlp_tok = _attention_block_macs(n, width, ffn // width)
+    block = attn + n * mlp_tok
+    budget = width * budget_hidden + budget_hidden * M
+    selector = 1 * width + (n - 1) * (width * sel_hidden + sel_hidden * 1)
+    return enc_in + block + budget + selector
+
+
+def trajectory_flops(tokens: np.ndarray, d: int, L: int, N0: int, patch: int, M: int, mlp_ratio: int = 4,
+                     in_chans: int = 3, classes: int = 1000, head_inputs: int = 1, actor: bool = True
+                     ) -> np.ndarray:
+    """FLOPs per image of the complete forward along its realised token
+    trajectory (App. E.4, Eq. (app-experiments-flops) before averaging).
+    tokens: int [L+1, B]; tokens[l] enters block l (N_l + 1, CLS included) and
+    tokens[l+1] is what its MLP keeps (N_l - k_l + 1); tokens[0] = N0 + 1.
+    Block l: attention over tokens[l], MLP over tokens[l+1]; with the actor,
+    the gate runs at every block with a legal budget (N_l >= 6) and the
+    controller wherever tokens were removed.  Plus the patch embedding
+    (in_chans * patch^2 -> d per patch) and the classifier
+    (head_inputs * d -> classes)."""
+    T = np.asarray(tokens, dtype=np.int64)
+    if T.shape[0] != L + 1:
+        raise ValueError("tokens must be [L+1, B]")
+    out = np.zeros(T.shape[1], dtype=np.int64)
+    for b in range(T.shape[1]):
+        macs = N0 * (in_chans * patch * patch) * d + head_inputs * d * classes
+        for l in range(L):
+            n, m = int(T[l, b]), int(T[l + 1, b])
+            attn, mlp_tok = _attention_block_macs(n, d, mlp_ratio)
+            macs += attn + m * mlp_tok
+            if actor:
+                if n - 1 >= 6:
+                    macs += actor_gate_macs(d)
+                if m < n:
+                    macs += actor_controller_macs(n, d, M)
+        out[b] = 2 * macs
     return out
 
 
