@@ -339,6 +339,49 @@ int dora_lc1_readout(const void* x, const int32_t* cu_seqlens, int64_t total, in
                      dora_dtype dtype, const float* gamma, const float* beta, float eps, float* out,
                      int32_t* dev_status, void* stream);
 
+/* Backbone shape for dora_trajectory_flops (Table 3; DINOv2's LC1 readout has
+ * head_inputs = 2).  actor: 1 to count DORA's actor, 0 for the bare backbone. */
+typedef struct {
+  int32_t d;           /* token width                                        */
+  int32_t L;           /* blocks                                             */
+  int32_t N0;          /* visual tokens at the input (patches)               */
+  int32_t patch;       /* patch side; the embedding is in_chans*patch^2 -> d */
+  int32_t in_chans;    /* image channels (3)                                 */
+  int32_t classes;     /* classifier outputs (1000)                          */
+  int32_t head_inputs; /* classifier input width in units of d               */
+  int32_t mlp_ratio;   /* MLP hidden width in units of d (4)                 */
+  int32_t M;           /* budget-head outputs, (N0 - 4) / 2                  */
+  int32_t actor;       /* 0 or 1                                             */
+} dora_flops_config;
+
+/*
+ * dora_trajectory_flops -- FLOPs of the complete forward of each image along
+ * its realised token trajectory (App. E.4, Eq. (app-experiments-flops) before
+ * averaging): two per multiply-accumulate of the patch embedding, every
+ * linear layer, the two attention products and the classifier.  At block l
+ * the attention runs over tokens[l] tokens and the MLP over tokens[l+1]
+ * (CLS included).  With actor = 1 (App. A.1): the gate (d + 19 -> 64 -> 1)
+ * at every block whose visual tokens allow a budget (N_l >= 6), and where
+ * tokens were removed the controller: d -> 128 projection of every key,
+ * 3 -> 128 history projection, a width-128 Transformer block (4 heads, FFN
+ * 128 -> 256 -> 128), budget head 128 -> 128 -> M, the 1 -> 128 projection of
+ * k / N and the selector 128 -> 64 -> 1 on the visual tokens.  LayerNorm,
+ * softmax, activations and additions are not counted.
+ *
+ *   tokens     device int32 [L+1, B]: tokens[0][b] = N0 + 1 and
+ *              1 <= tokens[l+1][b] <= tokens[l][b].  An image that breaks
+ *              this gets flops_out = -1, is left out of the total and sets
+ *              DORA_DEV_KEEP_RANGE.
+ *   config     host pointer, read during the call.
+ *   flops_out  device int64 [B]; total_out device int64 [1]: the sum over the
+ *              valid images.
+ *   B 1 .. 2^24.
+ * Returns DORA_OK or a negative dora_status (DORA_ERR_SHAPE for a config
+ * field out of range); enqueues one single-workgroup kernel.
+ */
+int dora_trajectory_flops(const int32_t* tokens, int32_t B, const dora_flops_config* config, int64_t* flops_out,
+                          int64_t* total_out, int32_t* dev_status, void* stream);
+
 /*
  * dora_varlen_attn_execute -- exact softmax attention inside each packed
  * sequence (Sec. 3.5 "Inference"; App. E.5): for every sequence b and head h

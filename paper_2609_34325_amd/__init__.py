@@ -57,6 +57,7 @@ EXPORTS = (
     "dora_pl_sample",
     "dora_pl_logprob",
     "dora_lc1_readout",
+    "dora_trajectory_flops",
     "dora_varlen_attn_workspace_size",
     "dora_varlen_attn_plan",
     "dora_varlen_attn_execute",
@@ -65,6 +66,12 @@ EXPORTS = (
 )
 
 _lib = None
+
+
+class FlopsConfig(ctypes.Structure):
+    """dora_flops_config of include/dora.h."""
+    _fields_ = [(name, ctypes.c_int32) for name in
+                ("d", "L", "N0", "patch", "in_chans", "classes", "head_inputs", "mlp_ratio", "M", "actor")]
 
 
 class DoraError(RuntimeError):
@@ -103,6 +110,8 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.dora_pl_logprob.argtypes = [vp, vp, vp, vp, i64, i32, i32, vp, vp, vp]
     lib.dora_lc1_readout.restype = ctypes.c_int
     lib.dora_lc1_readout.argtypes = [vp, vp, i64, i32, i32, ctypes.c_int, vp, vp, ctypes.c_float, vp, vp, vp]
+    lib.dora_trajectory_flops.restype = ctypes.c_int
+    lib.dora_trajectory_flops.argtypes = [vp, i32, ctypes.POINTER(FlopsConfig), vp, vp, vp, vp]
     lib.dora_varlen_attn_workspace_size.restype = sz
     lib.dora_varlen_attn_workspace_size.argtypes = [i32, i32, i32]
     lib.dora_varlen_attn_plan.restype = ctypes.c_int
@@ -422,6 +431,29 @@ def dora_lc1_readout(x: torch.Tensor, cu_seqlens: torch.Tensor, gamma: torch.Ten
         _dev(out, "out", torch.float32), _dev(dev_status, "dev_status", torch.int32), _stream(stream))
     _check("dora_lc1_readout", rc)
     return out, dev_status
+
+
+def dora_trajectory_flops(tokens: torch.Tensor, d: int, N0: int, patch: int, M: Optional[int] = None,
+                          mlp_ratio: int = 4, in_chans: int = 3, classes: int = 1000, head_inputs: int = 1,
+                          actor: bool = True, flops_out: Optional[torch.Tensor] = None,
+                          total_out: Optional[torch.Tensor] = None, dev_status: Optional[torch.Tensor] = None,
+                          stream=None):
+    """FLOPs per image along realised token trajectories tokens [L+1, B] (int32).
+    Returns (flops [B] int64, total [1] int64, dev_status)."""
+    if tokens.dim() != 2:
+        raise ValueError("tokens must be [L+1, B]")
+    L, B = int(tokens.shape[0]) - 1, int(tokens.shape[1])
+    cfg = FlopsConfig(int(d), L, int(N0), int(patch), int(in_chans), int(classes), int(head_inputs),
+                      int(mlp_ratio), int((N0 - 4) // 2 if M is None else M), int(bool(actor)))
+    dev = tokens.device
+    flops_out = torch.empty(B, dtype=torch.int64, device=dev) if flops_out is None else flops_out
+    total_out = torch.empty(1, dtype=torch.int64, device=dev) if total_out is None else total_out
+    dev_status = new_status(dev) if dev_status is None else dev_status
+    rc = load_library().dora_trajectory_flops(
+        _dev(tokens, "tokens", torch.int32), B, ctypes.byref(cfg), _dev(flops_out, "flops_out", torch.int64),
+        _dev(total_out, "total_out", torch.int64), _dev(dev_status, "dev_status", torch.int32), _stream(stream))
+    _check("dora_trajectory_flops", rc)
+    return flops_out, total_out, dev_status
 
 
 def dora_varlen_attn_workspace_size(B: int, H: int, max_seqlen: int) -> int:

@@ -16,7 +16,7 @@ LIB = os.path.join(PKG, "libdora.so")
 # Measurement helper for bench.py (sustained MFMA rate); not part of the boundary.
 CALIB_LIB = os.path.join(PKG, "libdora_calibrate.so")
 CALIB_SOURCES = ["calibrate.hip"]
-SOURCES = ["select_pack.hip", "varlen_attn.hip", "actor_decode.hip", "pl_sample.hip", "lc1_readout.hip"]
+SOURCES = ["select_pack.hip", "varlen_attn.hip", "actor_decode.hip", "pl_sample.hip", "lc1_readout.hip", "flops.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

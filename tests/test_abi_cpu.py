@@ -170,6 +170,25 @@ def test_lc1_host_validation():
     assert call(eps=-1.0) == dora.DORA_ERR_SHAPE
 
 
+def test_trajectory_flops_host_validation():
+    lib = dora.load_library()
+    good = dict(d=768, L=12, N0=196, patch=16, in_chans=3, classes=1000, head_inputs=1, mlp_ratio=4, M=96, actor=1)
+
+    def call(B=4, tokens=FAKE, out=FAKE, **kw):
+        cfg = dora.FlopsConfig(**{**good, **kw})
+        return lib.dora_trajectory_flops(tokens, B, ctypes.byref(cfg), out, FAKE, FAKE, None)
+
+    assert call(tokens=None) == dora.DORA_ERR_NULL
+    assert call(out=None) == dora.DORA_ERR_NULL
+    assert lib.dora_trajectory_flops(FAKE, 4, None, FAKE, FAKE, FAKE, None) == dora.DORA_ERR_NULL
+    assert call(B=0) == dora.DORA_ERR_SHAPE
+    assert call(d=0) == dora.DORA_ERR_SHAPE
+    assert call(L=0) == dora.DORA_ERR_SHAPE
+    assert call(M=0) == dora.DORA_ERR_SHAPE
+    assert call(actor=2) == dora.DORA_ERR_SHAPE
+    assert call(N0=dora.DORA_MAX_ROW_TOKENS + 1) == dora.DORA_ERR_SHAPE
+
+
 def call_select_plan(lib, **kw):
     ws = dora.dora_varlen_attn_workspace_size(4, 3, 197)
     a = dict(scores=FAKE, keep=FAKE, tokens=FAKE, cu_in=None, total_in=0, B=4, N=197, C=768, dtype=1,
