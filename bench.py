@@ -6,8 +6,10 @@ One step = one pass of the whole path over one batch:
                                packed layout, in one launch)
     dora_varlen_attn_execute  (varlen attention, bf16 MFMA)
 on synthetic inputs already resident in HBM.  Prints one JSON line.  Beside
-the step it also times dora_select_pack_residual (the kept rows of tokens +
-attention output) on the same batch.
+the step it also times, on the same batch, the adjacent entry points:
+dora_select_pack_residual (the kept rows of tokens + attention output), the
+actor decode (dora_actor_gate + dora_actor_decode), dora_lc1_readout,
+dora_trajectory_flops and dora_pl_sample.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 """
@@ -79,6 +81,7 @@ KERNEL_NAMES = {"attn": ("attn_fwd_bf16_kernel", "attn_fwd_f32_kernel"),
                 "actor": ("actor_gate_kernel", "actor_decode_kernel"),
                 "pl": ("pl_kernel",),
                 "lc1": ("lc1_readout_kernel",),
+                "flops": ("trajectory_flops_kernel",),
                 "plan": ("attn_plan_kernel",)}
 
 
@@ -340,6 +343,7 @@ def main() -> int:
     ap.add_argument("--no-actor", action="store_true", help="skip timing the actor decode (outside the step)")
     ap.add_argument("--no-pl", action="store_true", help="skip timing the Plackett-Luce draw (outside the step)")
     ap.add_argument("--no-lc1", action="store_true", help="skip timing the LC1 readout input (outside the step)")
+    ap.add_argument("--no-flops", action="store_true", help="skip timing the trajectory FLOP count (outside the step)")
     ap.add_argument("--no-residual", action="store_true",
                     help="skip timing select/pack after the attention residual (outside the step)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -591,6 +595,29 @@ def main() -> int:
               file=sys.stderr, flush=True)
         del x_d
 
+    # Beside the path: FLOP accounting of the batch's realised trajectories
+    # over a 12-block backbone (pruning at block 0 with this batch's keep
+    # counts, then none): one small latency-bound launch.
+    traj = None
+    if not args.no_flops:
+        L_blocks = 12
+        T = np.vstack([np.full((1, w.B), w.N, np.int32), np.tile(r.keep.astype(np.int32), (L_blocks, 1))])
+        T_d = dev(np.ascontiguousarray(T))
+        f_d = torch.empty(w.B, dtype=torch.int64, device="cuda")
+        tot_d = torch.empty(1, dtype=torch.int64, device="cuda")
+        st_f = dora.new_status()
+
+        def flops_call():
+            dora.dora_trajectory_flops(T_d, w.C, w.N - 1, 16, flops_out=f_d, total_out=tot_d, dev_status=st_f,
+                                       stream=stream)
+
+        ms_fl = time_calls(flops_call)
+        assert int(st_f.item()) == 0, f"device status {int(st_f.item())}"
+        traj = {"entry": "dora_trajectory_flops", "kernel": "trajectory_flops_kernel", "bound": "latency",
+                 "us": ms_fl * 1e3, "images": w.B, "blocks": L_blocks,
+                 "gflops_per_image": int(tot_d.item()) / w.B / 1e9}
+        print(f"[bench] trajectory flops: {ms_fl * 1e3:.1f} us per launch", file=sys.stderr, flush=True)
+
     # Beside the path: the training-time draw (Gumbel-top-k Plackett-Luce
     # deletion of n - keep tokens per image, with its ordered log-probability).
     pl = None
@@ -698,6 +725,8 @@ def main() -> int:
         result["actor_decode"] = actor
     if pl is not None:
         result["pl_sample"] = pl
+    if traj is not None:
+        result["trajectory_flops"] = traj
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         result["cpu_baseline"] = run_cpu_baseline(w, r)
