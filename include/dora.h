@@ -302,7 +302,9 @@ int dora_pl_sample(const float* scores, const float* gumbel, const int32_t* k, c
  * new policy), as in dora_pl_sample.
  *
  *   order, cu_order  as written by dora_pl_sample (order holds cu_order[B]
- *              entries): distinct visual positions per image.
+ *              entries; cu_order[0] = 0, non-decreasing): distinct visual
+ *              positions per image.  An image whose offsets break this gets
+ *              NaN and DORA_DEV_KEEP_RANGE, and none of its entries is read.
  *   logprob_out fp32 [B]; NaN with DORA_DEV_KEEP_RANGE when an image's list
  *              is longer than n_b - 1, repeats a position or holds one outside
  *              1 .. n_b - 1.

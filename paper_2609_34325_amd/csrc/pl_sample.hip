@@ -153,8 +153,12 @@ __global__ __launch_bounds__(kPLThreads) void pl_kernel(PLParams p) {
       p.cu_order_out[b + 1] = static_cast<int32_t>(out0 + min(max(kb, 0), p.N));
     }
   } else {
-    out0 = p.cu_order_in[b];
-    kb = p.cu_order_in[b + 1] - p.cu_order_in[b];
+    // The list of image b is [cu_order[b], cu_order[b+1]) inside the caller's
+    // cu_order[B] entries; offsets outside that range are rejected before any
+    // entry is read.
+    const int o0 = p.cu_order_in[b], o1 = p.cu_order_in[b + 1], oend = p.cu_order_in[p.B];
+    out0 = o0;
+    kb = (o0 >= 0 && o1 >= o0 && o1 <= oend && p.cu_order_in[0] == 0) ? o1 - o0 : -1;
   }
   bool ok = seg_ok && kb >= 0 && kb <= nv;
   if (!seg_ok && tid == 0) atomicOr(p.status, DORA_DEV_CU_IN);

@@ -180,6 +180,25 @@ def test_invalid_draw_counts_and_orders_set_status(gpu):
         assert int(stb.item()) & gpu.DORA_DEV_KEEP_RANGE and np.isnan(lpb[0]) and np.all(np.isfinite(lpb[1:]))
 
 
+def test_invalid_order_offsets_are_rejected_without_reading(gpu):
+    rng = np.random.default_rng(12)
+    B, N = 4, 30
+    s = rng.standard_normal((B, N)).astype(np.float32)
+    # every list stays inside the order array (cu_order[B] entries), as the
+    # contract requires; the offsets themselves are what is wrong
+    short = np.array([3, 4, 5, 6, 7, 8, 9, 10], np.int32)
+    long_ = (np.arange(36) % (N - 1) + 1).astype(np.int32)
+    for order, cu, bad in ((short, [0, 2, 1, 5, 8], [1]),         # decreasing
+                           (short, [0, -5, 4, 6, 8], [0, 1]),     # negative
+                           (long_, [0, 30, 32, 34, 36], [0])):    # 30 draws from 29 visual tokens
+        lp, st = gpu.dora_pl_logprob(to_dev(s), to_dev(order), to_dev(np.array(cu, np.int32)))
+        torch.cuda.synchronize()
+        lp = lp.cpu().numpy()
+        assert int(st.item()) & gpu.DORA_DEV_KEEP_RANGE, cu
+        good = [i for i in range(B) if i not in bad]
+        assert np.all(np.isnan(lp[bad])) and np.all(np.isfinite(lp[good])), (cu, lp)
+
+
 def test_capacity_overflow(gpu):
     rng = np.random.default_rng(11)
     B, N = 8, 50
