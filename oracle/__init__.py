@@ -95,6 +95,10 @@ def load_library(path: str):
     lib.oracle_lc1_readout.restype = None
     lib.oracle_lc1_readout.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_double, ctypes.c_void_p]
+    lib.oracle_varlen_attn_rows.restype = None
+    lib.oracle_varlen_attn_rows.argtypes = [
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+        ctypes.c_int32, ctypes.c_double, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
     lib.oracle_round_to_format.restype = None
     lib.oracle_round_to_format.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p]
     lib.oracle_residual_add.restype = None
@@ -374,6 +378,21 @@ def varlen_attn(q: np.ndarray, k: np.ndarray, v: np.ndarray, cu: np.ndarray, dty
     out = np.zeros_like(qd)
     _load(lib).oracle_varlen_attn(_ptr(qd), _ptr(kd), _ptr(vd), _ptr(cu), B, H, D, float(scale),
                                _ptr(out), int(threads))
+    return out
+
+
+def varlen_attn_rows(q, k, v, cu, rows, dtype: str, scale: Optional[float] = None, lib=None) -> np.ndarray:
+    """Oracle outputs of selected packed query rows only: [len(rows), H, D] fp64
+    (each row attends to every key of its own sequence)."""
+    qd, kd, vd = (np.ascontiguousarray(widen(a, dtype)) for a in (q, k, v))
+    total, H, D = qd.shape
+    cu = np.ascontiguousarray(cu, dtype=np.int32)
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    if scale is None:
+        scale = 1.0 / np.sqrt(D)
+    out = np.zeros((len(rows), H, D))
+    _load(lib).oracle_varlen_attn_rows(_ptr(qd), _ptr(kd), _ptr(vd), _ptr(cu), int(cu.shape[0]) - 1, H, D,
+                                       float(scale), _ptr(rows), len(rows), _ptr(out))
     return out
 
 

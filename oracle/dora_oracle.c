@@ -472,6 +472,46 @@ void oracle_lc1_readout(const double* x, const int32_t* cu, int32_t B, int32_t C
   free(y);
 }
 
+/* The same attention for selected query rows only: out[r] = the output of
+ * packed row rows[r] (all heads), which attends to every key of its own
+ * sequence.  Rows are found in their sequence by the offsets cu. */
+void oracle_varlen_attn_rows(const double* q, const double* k, const double* v, const int32_t* cu,
+                             int32_t B, int32_t H, int32_t D, double scale, const int64_t* rows, int64_t nrows,
+                             double* out) {
+#pragma omp parallel for collapse(2) schedule(dynamic)
+  for (int64_t r = 0; r < nrows; ++r) {
+    for (int32_t h = 0; h < H; ++h) {
+      const int64_t i = rows[r];
+      int32_t b = 0;
+      while (b < B && cu[b + 1] <= i) ++b;
+      const int64_t start = cu[b], len = (int64_t)cu[b + 1] - cu[b];
+      double* logits = (double*)malloc(sizeof(double) * (size_t)len);
+      const double* qi = q + (i * H + h) * D;
+      double mx = -INFINITY;
+      for (int64_t j = 0; j < len; ++j) {
+        const double* kj = k + ((start + j) * H + h) * D;
+        double dot = 0.0;
+        for (int32_t d = 0; d < D; ++d) dot += qi[d] * kj[d];
+        logits[j] = scale * dot;
+        if (logits[j] > mx) mx = logits[j];
+      }
+      double z = 0.0;
+      for (int64_t j = 0; j < len; ++j) {
+        logits[j] = exp(logits[j] - mx);
+        z += logits[j];
+      }
+      double* oi = out + (r * H + h) * D;
+      for (int32_t d = 0; d < D; ++d) oi[d] = 0.0;
+      for (int64_t j = 0; j < len; ++j) {
+        const double* vj = v + ((start + j) * H + h) * D;
+        const double p = logits[j] / z;
+        for (int32_t d = 0; d < D; ++d) oi[d] += p * vj[d];
+      }
+      free(logits);
+    }
+  }
+}
+
 int oracle_max_threads(void) {
 #ifdef _OPENMP
   return omp_get_max_threads();

@@ -221,3 +221,30 @@ def test_invalid_offsets_set_status(gpu):
         out, st = gpu_attn(gpu, q, k, v, cu, max_seqlen=ms, out_fill=0x1234)
         assert st & gpu.DORA_DEV_CU_SEQLENS, bad
         assert np.all(to_host_bits(out) == 0x1234), bad
+
+
+def test_maximum_sequence_length(gpu):
+    """One sequence of DORA_MAX_SEQLEN tokens (69 query chunks, 64 key
+    stages): sampled query rows against the oracle, and the convex-hull bound
+    on every output."""
+    n = gpu.DORA_MAX_SEQLEN
+    rng = np.random.default_rng(42)
+    q, k, v = qkv(rng, [n], 1, "bf16")
+    cu = cu_of([n])
+    out, st = gpu_attn(gpu, q, k, v, cu)
+    assert st == 0
+    got = widen(out)
+    vv = W.bf16_bits_to_f32(v).astype(np.float64)
+    assert np.all(np.isfinite(got))
+    assert np.all(got <= vv.max(axis=0) + 1e-2) and np.all(got >= vv.min(axis=0) - 1e-2)
+    rows = np.unique(np.concatenate([[0, 239, 240, n - 241, n - 1], rng.choice(n, 40, replace=False)]))
+    want = oracle.varlen_attn_rows(q, k, v, cu, rows, "bf16")
+    assert_attn_close(got[rows], want, "bf16", "len 16384")
+
+
+def test_maximum_sequence_count(gpu):
+    """8192 short sequences (the most one plan orders), lengths 1..4, H = 2."""
+    rng = np.random.default_rng(43)
+    lens = rng.integers(1, 5, 8192)
+    q, k, v = qkv(rng, lens, 2, "bf16")
+    full_compare(gpu, q, k, v, cu_of(lens), "bf16", what="8192 sequences")

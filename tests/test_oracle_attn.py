@@ -190,3 +190,14 @@ def test_bf16_inputs_decode_then_attend():
     dec = lambda a: workloads.bf16_bits_to_f32(a)
     want = oracle.varlen_attn(dec(qb), dec(kb), dec(vb), cu, "f32")
     assert np.array_equal(got, want)
+
+
+def test_selected_rows_equal_the_full_oracle():
+    """varlen_attn_rows evaluates the same definition for chosen query rows."""
+    rng = np.random.default_rng(77)
+    lens = np.array([5, 1, 37, 12])
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    q, k, v = (rng.standard_normal((int(lens.sum()), 3, 64)).astype(np.float32) for _ in range(3))
+    full = oracle.varlen_attn(q, k, v, cu, "f32")
+    rows = np.array([0, 4, 5, 6, 20, 42, 54])
+    assert np.array_equal(oracle.varlen_attn_rows(q, k, v, cu, rows, "f32"), full[rows])
