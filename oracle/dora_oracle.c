@@ -146,6 +146,32 @@ int oracle_select_pack(const float* scores, const int32_t* keep, const uint8_t* 
  *   cu           : [B+1] sequence boundaries
  * O_b = softmax(scale * Q_b K_b^T) V_b for every sequence b and head h.
  */
+/* Output of query row i (head h) of the sequence at rows [start, start + len):
+ * a dense fp64 logit row, its softmax, and the weighted sum of V. */
+static void attend_row(const double* q, const double* k, const double* v, int64_t start, int64_t len, int64_t i,
+                       int32_t H, int32_t h, int32_t D, double scale, double* logits, double* oi) {
+  const double* qi = q + (i * H + h) * D;
+  double mx = -INFINITY;
+  for (int64_t j = 0; j < len; ++j) {
+    const double* kj = k + ((start + j) * H + h) * D;
+    double dot = 0.0;
+    for (int32_t d = 0; d < D; ++d) dot += qi[d] * kj[d];
+    logits[j] = scale * dot;
+    if (logits[j] > mx) mx = logits[j];
+  }
+  double z = 0.0;
+  for (int64_t j = 0; j < len; ++j) {
+    logits[j] = exp(logits[j] - mx);
+    z += logits[j];
+  }
+  for (int32_t d = 0; d < D; ++d) oi[d] = 0.0;
+  for (int64_t j = 0; j < len; ++j) {
+    const double* vj = v + ((start + j) * H + h) * D;
+    const double p = logits[j] / z;
+    for (int32_t d = 0; d < D; ++d) oi[d] += p * vj[d];
+  }
+}
+
 void oracle_varlen_attn(const double* q, const double* k, const double* v, const int32_t* cu,
                         int32_t B, int32_t H, int32_t D, double scale, double* out,
                         int32_t nthreads) {
@@ -161,29 +187,8 @@ void oracle_varlen_attn(const double* q, const double* k, const double* v, const
       const int64_t len = (int64_t)cu[b + 1] - cu[b];
       if (len <= 0) continue;
       double* logits = (double*)malloc(sizeof(double) * (size_t)len);
-      for (int64_t i = 0; i < len; ++i) {
-        const double* qi = q + ((start + i) * H + h) * D;
-        double mx = -INFINITY;
-        for (int64_t j = 0; j < len; ++j) {
-          const double* kj = k + ((start + j) * H + h) * D;
-          double dot = 0.0;
-          for (int32_t d = 0; d < D; ++d) dot += qi[d] * kj[d];
-          logits[j] = scale * dot;
-          if (logits[j] > mx) mx = logits[j];
-        }
-        double z = 0.0;
-        for (int64_t j = 0; j < len; ++j) {
-          logits[j] = exp(logits[j] - mx);
-          z += logits[j];
-        }
-        double* oi = out + ((start + i) * H + h) * D;
-        for (int32_t d = 0; d < D; ++d) oi[d] = 0.0;
-        for (int64_t j = 0; j < len; ++j) {
-          const double* vj = v + ((start + j) * H + h) * D;
-          const double p = logits[j] / z;
-          for (int32_t d = 0; d < D; ++d) oi[d] += p * vj[d];
-        }
-      }
+      for (int64_t i = 0; i < len; ++i)
+        attend_row(q, k, v, start, len, start + i, H, h, D, scale, logits, out + ((start + i) * H + h) * D);
       free(logits);
     }
   }
@@ -486,27 +491,7 @@ void oracle_varlen_attn_rows(const double* q, const double* k, const double* v, 
       while (b < B && cu[b + 1] <= i) ++b;
       const int64_t start = cu[b], len = (int64_t)cu[b + 1] - cu[b];
       double* logits = (double*)malloc(sizeof(double) * (size_t)len);
-      const double* qi = q + (i * H + h) * D;
-      double mx = -INFINITY;
-      for (int64_t j = 0; j < len; ++j) {
-        const double* kj = k + ((start + j) * H + h) * D;
-        double dot = 0.0;
-        for (int32_t d = 0; d < D; ++d) dot += qi[d] * kj[d];
-        logits[j] = scale * dot;
-        if (logits[j] > mx) mx = logits[j];
-      }
-      double z = 0.0;
-      for (int64_t j = 0; j < len; ++j) {
-        logits[j] = exp(logits[j] - mx);
-        z += logits[j];
-      }
-      double* oi = out + (r * H + h) * D;
-      for (int32_t d = 0; d < D; ++d) oi[d] = 0.0;
-      for (int64_t j = 0; j < len; ++j) {
-        const double* vj = v + ((start + j) * H + h) * D;
-        const double p = logits[j] / z;
-        for (int32_t d = 0; d < D; ++d) oi[d] += p * vj[d];
-      }
+      attend_row(q, k, v, start, len, i, H, h, D, scale, logits, out + (r * H + h) * D);
       free(logits);
     }
   }

@@ -38,7 +38,7 @@ MUTANTS = {
                           "const double* vj = v + ((start + j) * H + 0) * D;"),
     "unnormalised": ("const double p = logits[j] / z;", "const double p = logits[j];"),
     "key_index_is_query": ("for (int32_t d = 0; d < D; ++d) dot += qi[d] * kj[d];",
-                           "for (int32_t d = 0; d < D; ++d) dot += qi[d] * k[((start + i) * H + h) * D + d];"),
+                           "for (int32_t d = 0; d < D; ++d) dot += qi[d] * k[(i * H + h) * D + d];"),
     "ties_away_from_zero": ("if (frac > 0.5 || (frac == 0.5 && fmod(n, 2.0) != 0.0)) n += 1.0;",
                             "if (frac >= 0.5) n += 1.0;"),
     "truncating_round": ("if (frac > 0.5 || (frac == 0.5 && fmod(n, 2.0) != 0.0)) n += 1.0;", ""),
