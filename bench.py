@@ -195,7 +195,7 @@ N_SIMD = 256 * 4      # 256 CUs x 4 SIMDs
 def summarize_pmc(d: str, workload: str) -> int:
     """Reads rocprofv3 --pmc CSV output of runs of this script under DIR/*/
     and prints, per kernel, the matrix-unit and LDS counters the attention
-    design is judged by: MFMA busy share (SQ_VALU_MFMA_BUSY_CYCLES over
+    kernel is measured by: MFMA busy share (SQ_VALU_MFMA_BUSY_CYCLES over
     GRBM_GUI_ACTIVE x SIMDs, rocprofv3's MfmaUtil), bf16 MFMA flops executed
     (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512) against the algorithmic flops, and
     LDS bank conflicts per LDS access cycle.  Averages are per dispatch, over

@@ -52,7 +52,7 @@ typedef enum {
   DORA_ERR_SHAPE = -2,       /* a size is out of range (B, N, C, H, D, max_seqlen)  */
   DORA_ERR_DTYPE = -3,       /* unknown dora_dtype                                  */
   DORA_ERR_ALIGN = -4,       /* a row-data pointer is not 16-byte aligned           */
-  DORA_ERR_UNSUPPORTED = -5, /* valid request outside what this build implements    */
+  DORA_ERR_UNSUPPORTED = -5, /* valid request outside what this library implements  */
   DORA_ERR_CAPACITY = -6,    /* an output capacity cannot be represented            */
   DORA_ERR_HIP = -7,         /* the HIP runtime reported an error at launch         */
   DORA_ERR_WORKSPACE = -8    /* workspace NULL, misaligned or smaller than required */
@@ -68,7 +68,7 @@ typedef enum {
 #define DORA_DEV_ACTOR 0x20      /* actor decode: a gate-on image without a legal budget or logit row;
                                     it was left unpruned                                           */
 
-/* Limits of this build. */
+/* Limits of this library. */
 #define DORA_MAX_ROW_TOKENS 2048     /* dora_select_pack: N (tokens per image, CLS included)  */
 #define DORA_MAX_SEQLEN 16384        /* dora_varlen_attn: max_seqlen                          */
 #define DORA_HEAD_DIM 64             /* dora_varlen_attn: D                                   */

@@ -1146,7 +1146,7 @@ extern "C" const char* dora_status_string(int status) {
     case DORA_ERR_SHAPE: return "DORA_ERR_SHAPE: a size is out of range";
     case DORA_ERR_DTYPE: return "DORA_ERR_DTYPE: unknown dtype";
     case DORA_ERR_ALIGN: return "DORA_ERR_ALIGN: row data must be 16-byte aligned";
-    case DORA_ERR_UNSUPPORTED: return "DORA_ERR_UNSUPPORTED: outside what this build implements";
+    case DORA_ERR_UNSUPPORTED: return "DORA_ERR_UNSUPPORTED: outside what this library implements";
     case DORA_ERR_CAPACITY: return "DORA_ERR_CAPACITY: output capacity out of range";
     case DORA_ERR_HIP: return "DORA_ERR_HIP: HIP runtime error at launch";
     case DORA_ERR_WORKSPACE: return "DORA_ERR_WORKSPACE: workspace missing, misaligned or too small";
