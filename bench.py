@@ -36,8 +36,8 @@ METRIC = "packed tokens/s + varlen-attn TFLOP/s (% MFMA peak), DeiT-B shape, B=2
 
 
 def plan_items(w: W.Workload, keep: np.ndarray) -> int:
-    """Attention work items: one per (image, head, chunk of 240 queries)."""
-    return w.H * int(np.sum((keep.astype(np.int64) + 239) // 240))
+    """Attention work items: one per (image, head, chunk of 192 queries)."""
+    return w.H * int(np.sum((keep.astype(np.int64) + 191) // 192))
 
 
 def select_pack_bytes(w: W.Workload, keep: np.ndarray, n_in: np.ndarray) -> int:

@@ -57,7 +57,7 @@ __device__ __forceinline__ int lanes_below(uint64_t mask) {
 // sub-queues carry near-equal work.
 // ---------------------------------------------------------------------------
 constexpr int32_t kPlanMagic = 0x444F5241;  // "DORA"
-constexpr int kAttnQTile = 240;             // queries per work item (15 tiles of 16)
+constexpr int kAttnQTile = 192;             // queries per work item (12 tiles of 16, one per wave)
 constexpr int kPlanMaxB = 8192;             // sequences one plan can order
 constexpr int kSubQueues = 8;               // ticket counters (one per XCD of an MI355X)
 

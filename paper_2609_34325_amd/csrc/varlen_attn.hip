@@ -15,8 +15,10 @@
 //            last workgroup to leave resets the counters so the plan can run
 //            again (e.g. for every layer between two pruning steps).
 //
-// bf16 kernel, per work item: each wave owns up to two 16-query tiles of the
-// chunk.  K and V (row-major) stream through LDS in stages of kKRes keys by
+// bf16 kernel, per work item: each of the 12 waves owns one 16-query tile of
+// the chunk (three waves per SIMD: with one tile each a wave needs about 170
+// registers, so three fit where two-tile waves fit only two, and the extra
+// wave per SIMD overlaps more of the softmax with the matrix products).  K and V (row-major) stream through LDS in stages of kKRes keys by
 // LDS DMA, double-buffered, so the transfer of the next stage (the rest of
 // this item, or the next item) overlaps the MFMA work of the current one; the
 // next item's queries also arrive in LDS by DMA, and the queue ticket and
@@ -40,9 +42,9 @@ namespace dora {
 namespace {
 
 constexpr int kD = 64;
-constexpr int kWaves = 8;
+constexpr int kWaves = 12;
 constexpr int kThreads = kWaves * 64;
-constexpr int kTilesPerWave = 2;  // 16-query tiles per wave (1 or 2)
+constexpr int kTilesPerWave = 1;  // 16-query tiles per wave (1 or 2)
 static_assert(kTilesPerWave == 1 || kTilesPerWave == 2, "tiles per wave");
 static_assert(kWaves * kTilesPerWave * 16 >= kAttnQTile && kAttnQTile % 16 == 0, "tile size");
 constexpr int kF32Waves = 8;  // fp32 kernel: 8 waves x 32 queries

@@ -54,9 +54,9 @@ def test_ragged_tile_edges(gpu, dtype):
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_query_chunk_and_stage_edges(gpu, dtype):
-    """Lengths around the 240-query chunks and the 256-key stages, several
+    """Lengths around the 192-query chunks and the 256-key stages, several
     chunks and stages in one sequence, and heads that wrap a DMA round."""
-    lens = np.array([239, 240, 241, 255, 256, 257, 479, 480, 481, 511, 512, 513, 720, 721])
+    lens = np.array([191, 192, 193, 255, 256, 257, 383, 384, 385, 511, 512, 513, 575, 576, 577, 768, 769])
     rng = np.random.default_rng(41)
     q, k, v = qkv(rng, lens, 5, dtype)
     print(f"[attn] chunk/stage edges {dtype}", flush=True)
@@ -224,7 +224,7 @@ def test_invalid_offsets_set_status(gpu):
 
 
 def test_maximum_sequence_length(gpu):
-    """One sequence of DORA_MAX_SEQLEN tokens (69 query chunks, 64 key
+    """One sequence of DORA_MAX_SEQLEN tokens (86 query chunks, 64 key
     stages): sampled query rows against the oracle, and the convex-hull bound
     on every output."""
     n = gpu.DORA_MAX_SEQLEN
@@ -237,7 +237,7 @@ def test_maximum_sequence_length(gpu):
     vv = W.bf16_bits_to_f32(v).astype(np.float64)
     assert np.all(np.isfinite(got))
     assert np.all(got <= vv.max(axis=0) + 1e-2) and np.all(got >= vv.min(axis=0) - 1e-2)
-    rows = np.unique(np.concatenate([[0, 239, 240, n - 241, n - 1], rng.choice(n, 40, replace=False)]))
+    rows = np.unique(np.concatenate([[0, 191, 192, n - 193, n - 1], rng.choice(n, 40, replace=False)]))
     want = oracle.varlen_attn_rows(q, k, v, cu, rows, "bf16")
     assert_attn_close(got[rows], want, "bf16", "len 16384")
 

@@ -20,7 +20,7 @@ from gpu_util import assert_attn_close, to_dev, to_host_bits, widen
 
 pytestmark = pytest.mark.gpu
 
-Q_TILE = 240       # queries per item, as the library's workspace layout defines
+Q_TILE = 192       # queries per item, as the library's workspace layout defines
 HDR_BYTES = 2048   # plan header: sizes, a row of zeros, eight queue counters
 ITEMS_OFF = HDR_BYTES
 QUEUE_INTS = [64 + 32 * q for q in range(8)]   # one counter per 128-byte line
