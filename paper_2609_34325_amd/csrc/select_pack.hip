@@ -35,6 +35,7 @@ namespace dora {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kDigitSelectSlots = 8;  // rows of more than 256 tokens select by 8-bit digits
 constexpr int kCopyUnroll = 2;  // loads in flight per lane: few, so stores start early (measured best)
 
 struct SelectPackParams {
@@ -72,6 +73,62 @@ __device__ __forceinline__ long long wave_sum(long long v) {
   return v;
 }
 
+// Inclusive running sum over the 64 lanes of a wave, in DPP steps: shifts by
+// 1, 2, 4 and 8 within each row of 16 lanes (lanes shifted in from outside
+// the row add 0), then lane 15 of each row is added to the next row and lane
+// 31 to the upper half.
+__device__ __forceinline__ uint32_t wave_inclusive_sum(uint32_t x) {
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x111, 0xF, 0xF, false);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x112, 0xF, 0xF, false);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x114, 0xF, 0xF, false);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x118, 0xF, 0xF, false);  // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x142, 0xA, 0xF, false);  // row_bcast:15 into rows 1 and 3
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x143, 0xC, 0xF, false);  // row_bcast:31 into rows 2 and 3
+  return x;
+}
+
+// Threshold of one wave's valid keys for long rows: T = the need-th largest
+// valid key (counted with multiplicity) and q = how many keys equal to T are
+// kept, found one 8-bit digit at a time from the most significant.  A pass
+// builds the 256-bin histogram (in LDS) of the digit of every valid key that
+// matches the digits fixed so far, and fixes the largest digit whose count
+// of keys at or above it still reaches the number of keys left to take; the
+// keys above that digit are all taken.  Four dependent passes instead of 32
+// one-bit steps.  hist: 256 words of LDS used by this wave only.
+template <int SLOTS>
+__device__ __forceinline__ void digit_threshold(const uint32_t (&key)[SLOTS], const uint64_t (&valid)[SLOTS],
+                                                int need, uint32_t* hist, int lane, uint32_t& T, int& q) {
+  uint4* hist4 = reinterpret_cast<uint4*>(hist);
+  uint32_t prefix = 0u, fixed = 0u;
+  uint32_t left = static_cast<uint32_t>(need);
+#pragma unroll
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    hist4[lane] = make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+    for (int r = 0; r < SLOTS; ++r)
+      if (((valid[r] >> lane) & 1ull) && (key[r] & fixed) == prefix) atomicAdd(&hist[(key[r] >> shift) & 255u], 1u);
+    const uint4 h = hist4[lane];  // bins 4 lane .. 4 lane + 3 (LDS accesses of one wave complete in order)
+    const uint32_t s3 = h.w, s2 = h.z + s3, s1 = h.y + s2, s0 = h.x + s1;
+    const uint32_t upto = wave_inclusive_sum(s0);
+    const uint32_t above = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(upto), 63)) - upto;
+    // at_or_above[i]: keys whose digit is >= 4 lane + i.
+    const uint32_t c0 = above + s0, c1 = above + s1, c2 = above + s2, c3 = above + s3;
+    const int d = __popcll(__ballot(c0 >= left)) + __popcll(__ballot(c1 >= left)) +
+                  __popcll(__ballot(c2 >= left)) + __popcll(__ballot(c3 >= left)) - 1;
+    uint32_t taken = 0u;  // keys whose digit is > d
+    if (d < 255) {
+      const int i = (d + 1) & 3;
+      const uint32_t c = i == 0 ? c0 : i == 1 ? c1 : i == 2 ? c2 : c3;
+      taken = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(c), (d + 1) >> 2));
+    }
+    left -= taken;
+    prefix |= static_cast<uint32_t>(d) << shift;
+    fixed |= 255u << shift;
+  }
+  T = prefix;
+  q = static_cast<int>(left);
+}
+
 // What the copy writes for one 16-byte piece of a kept row.
 enum PackMode { kCopy = 0, kAddBf16 = 1, kAddF32 = 2 };
 
@@ -105,6 +162,7 @@ __device__ __forceinline__ u32x4 combine(uint4 x, uint4 y) {
 template <int SLOTS, int MODE>
 __device__ __forceinline__ void select_pack_body(const SelectPackParams& p) {
   __shared__ int32_t s_idx[SLOTS * 64];
+  __shared__ __align__(16) uint32_t s_hist[SLOTS >= kDigitSelectSlots ? 256 : 1];  // digit histogram of the long-row select
   __shared__ long long s_part[kThreads / 64];
   __shared__ long long s_before[kThreads / 64];  // plan items of the sequences ordered before b
   __shared__ long long s_items[kThreads / 64];   // plan items of all sequences
@@ -176,13 +234,23 @@ __device__ __forceinline__ void select_pack_body(const SelectPackParams& p) {
   } else if (img_ok) {
     // Candidates are positions 1..n-1 (CLS, position 0, is not a candidate).
     // Position pos = r*64 + lane lives in key[r] of that lane.
+    // All SLOTS loads are issued before the first is used: positions past
+    // the segment read its last score (they are not candidates), and the
+    // empty asm consumes every loaded value, so the compiler cannot sink a
+    // load into the branch of its only use, where each would wait alone.
     uint32_t key[SLOTS];
     uint64_t valid[SLOTS];
+    float x[SLOTS];
+    const long long last = off_in + n - 1;
+#pragma unroll
+    for (int r = 0; r < SLOTS; ++r) x[r] = p.scores[min(off_in + r * 64 + lane, last)];
+#pragma unroll
+    for (int r = 0; r < SLOTS; ++r) asm volatile("" : "+v"(x[r]));
 #pragma unroll
     for (int r = 0; r < SLOTS; ++r) {
       const int pos = r * 64 + lane;
       const bool v = pos >= 1 && pos < n;
-      key[r] = v ? keep_key(p.scores[off_in + pos]) : 0u;
+      key[r] = v ? keep_key(x[r]) : 0u;
       valid[r] = __ballot(v);
     }
     // Threshold T = the need-th largest candidate key; q = how many of the
@@ -190,7 +258,9 @@ __device__ __forceinline__ void select_pack_body(const SelectPackParams& p) {
     const int need = kb - 1;
     uint32_t T = 0xFFFFFFFFu;  // need == 0: nothing compares above or equal
     int q = 0;
-    if (need > 0) {
+    if (need > 0 && SLOTS >= kDigitSelectSlots) {
+      digit_threshold<SLOTS>(key, valid, need, s_hist, lane, T, q);
+    } else if (need > 0) {
       T = 0u;
       for (int bit = 31; bit >= 0; --bit) {
         const uint32_t t = T | (1u << bit);
