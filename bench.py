@@ -586,9 +586,11 @@ def main() -> int:
         x_d, cu_d, gamma_d, beta_d = dev(x_h), dev(cu_h), dev(gamma_h), dev(beta_h)
         out_d = torch.empty((w.B, 2 * w.C), dtype=torch.float32, device="cuda")
         st_l = dora.new_status()
+        ws_l = dora.new_lc1_workspace(w.B, w.C)
 
         def lc1_call():
-            dora.dora_lc1_readout(x_d, cu_d, gamma_d, beta_d, 1e-6, out=out_d, dev_status=st_l, stream=stream)
+            dora.dora_lc1_readout(x_d, cu_d, gamma_d, beta_d, 1e-6, out=out_d, workspace=ws_l, dev_status=st_l,
+                                  stream=stream)
 
         ms_lc1 = time_calls(lc1_call)
         assert int(st_l.item()) == 0, f"device status {int(st_l.item())}"

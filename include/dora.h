@@ -334,12 +334,23 @@ int dora_pl_logprob(const float* scores, const int32_t* order, const int32_t* cu
  *              sets DORA_DEV_CU_SEQLENS and gets a NaN output row.
  *   gamma, beta fp32 [C]; eps >= 0 (DINOv2: 1e-6).
  *   out        fp32 [B, 2C].
+ *   B          1 .. 2^24.
+ *   workspace  NULL: one workgroup per sequence.  Otherwise device memory of
+ *              at least dora_lc1_readout_workspace_size(B, C) bytes, 256-byte
+ *              aligned (else DORA_ERR_WORKSPACE / DORA_ERR_ALIGN), with no
+ *              required contents: when the batch is small against the GPU,
+ *              the rows of a sequence are split over up to 8 workgroups,
+ *              which write their sums there, and a second kernel adds them in
+ *              a fixed order (the result does not depend on timing).  Calls
+ *              that share a workspace must not overlap in time.
  *
- * Returns DORA_OK or a negative dora_status; enqueues one kernel.
+ * Returns DORA_OK or a negative dora_status; enqueues one kernel, or two when
+ * the rows are split.
  */
+size_t dora_lc1_readout_workspace_size(int32_t B, int32_t C);  /* 0 when B or C is out of range */
 int dora_lc1_readout(const void* x, const int32_t* cu_seqlens, int64_t total, int32_t B, int32_t C,
                      dora_dtype dtype, const float* gamma, const float* beta, float eps, float* out,
-                     int32_t* dev_status, void* stream);
+                     void* workspace, size_t workspace_bytes, int32_t* dev_status, void* stream);
 
 /* Backbone shape for dora_trajectory_flops (Table 3; DINOv2's LC1 readout has
  * head_inputs = 2).  actor: 1 to count DORA's actor, 0 for the bare backbone. */

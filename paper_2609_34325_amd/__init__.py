@@ -56,6 +56,7 @@ EXPORTS = (
     "dora_actor_decode",
     "dora_pl_sample",
     "dora_pl_logprob",
+    "dora_lc1_readout_workspace_size",
     "dora_lc1_readout",
     "dora_trajectory_flops",
     "dora_varlen_attn_workspace_size",
@@ -109,7 +110,10 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.dora_pl_logprob.restype = ctypes.c_int
     lib.dora_pl_logprob.argtypes = [vp, vp, vp, vp, i64, i32, i32, vp, vp, vp]
     lib.dora_lc1_readout.restype = ctypes.c_int
-    lib.dora_lc1_readout.argtypes = [vp, vp, i64, i32, i32, ctypes.c_int, vp, vp, ctypes.c_float, vp, vp, vp]
+    lib.dora_lc1_readout.argtypes = [vp, vp, i64, i32, i32, ctypes.c_int, vp, vp, ctypes.c_float, vp, vp, sz, vp,
+                                     vp]
+    lib.dora_lc1_readout_workspace_size.restype = sz
+    lib.dora_lc1_readout_workspace_size.argtypes = [i32, i32]
     lib.dora_trajectory_flops.restype = ctypes.c_int
     lib.dora_trajectory_flops.argtypes = [vp, i32, ctypes.POINTER(FlopsConfig), vp, vp, vp, vp]
     lib.dora_varlen_attn_workspace_size.restype = sz
@@ -411,12 +415,27 @@ def dora_pl_logprob(scores: torch.Tensor, order: torch.Tensor, cu_order: torch.T
     return logprob_out, dev_status
 
 
+def dora_lc1_readout_workspace_size(B: int, C: int) -> int:
+    return int(load_library().dora_lc1_readout_workspace_size(int(B), int(C)))
+
+
+def new_lc1_workspace(B: int, C: int, device=None) -> torch.Tensor:
+    """A workspace for dora_lc1_readout (no required contents)."""
+    n = dora_lc1_readout_workspace_size(B, C)
+    if n == 0:
+        raise DoraError("dora_lc1_readout_workspace_size", DORA_ERR_SHAPE)
+    return torch.empty(n, dtype=torch.uint8, device=device or "cuda")
+
+
 def dora_lc1_readout(x: torch.Tensor, cu_seqlens: torch.Tensor, gamma: torch.Tensor, beta: torch.Tensor,
                      eps: float = 1e-6, out: Optional[torch.Tensor] = None,
+                     workspace: Optional[torch.Tensor] = None, single: bool = False,
                      dev_status: Optional[torch.Tensor] = None, stream=None):
     """LayerNorm of each packed sequence's CLS row next to the mean LayerNorm of
     its other rows: x [total, C] bf16/fp32, cu_seqlens [B+1] -> out fp32 [B, 2C].
-    Returns (out, dev_status)."""
+    With a workspace (a new one when None) a sequence's rows may be
+    split over several workgroups; single=True passes none (one workgroup per
+    sequence).  Returns (out, dev_status)."""
     if x.dim() != 2:
         raise ValueError("x must be [total, C]")
     B = int(cu_seqlens.shape[0]) - 1
@@ -425,10 +444,14 @@ def dora_lc1_readout(x: torch.Tensor, cu_seqlens: torch.Tensor, gamma: torch.Ten
     dev_status = new_status(x.device) if dev_status is None else dev_status
     if tuple(out.shape) != (B, 2 * C):
         raise ValueError("out must be [B, 2C]")
+    if not single and workspace is None:
+        workspace = new_lc1_workspace(B, C, x.device)
+    ws, ws_bytes = (None, 0) if single else (_dev(workspace, "workspace"), workspace.numel() * workspace.element_size())
     rc = load_library().dora_lc1_readout(
         _dev(x, "x"), _dev(cu_seqlens, "cu_seqlens", torch.int32), total, B, C, _dtype_code(x),
         _dev(gamma, "gamma", torch.float32), _dev(beta, "beta", torch.float32), float(eps),
-        _dev(out, "out", torch.float32), _dev(dev_status, "dev_status", torch.int32), _stream(stream))
+        _dev(out, "out", torch.float32), ws, ws_bytes, _dev(dev_status, "dev_status", torch.int32),
+        _stream(stream))
     _check("dora_lc1_readout", rc)
     return out, dev_status
 

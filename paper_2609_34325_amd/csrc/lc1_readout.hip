@@ -20,6 +20,16 @@
 // and are added in wave order (the result does not depend on timing); then
 // gamma * sum / (n - 1) + beta is the mean of the normalised rows and
 // gamma * cls + beta the normalised CLS.
+//
+// Small batches (a caller workspace given): the rows of an image are split
+// into up to 8 contiguous parts, one workgroup each, so that about 256
+// workgroups run; each writes its sum of normalised rows to the workspace and
+// lc1_combine_kernel, launched next, adds the parts in order.  The launch
+// boundary makes the sums visible: a last-workgroup-combines protocol needs
+// an agent-scope release per workgroup, which writes back the die's whole L2
+// and serialised the workgroups (55 ns each).
+#include <algorithm>
+
 #include "dora_internal.h"
 
 namespace dora {
@@ -27,6 +37,8 @@ namespace {
 
 constexpr int kLCCombine = 8;  // waves whose partial sums meet in LDS (LDS holds kLCCombine x C floats)
 constexpr int kLCMaxRowBytes = 4096;  // 64 lanes x 4 pieces of 16 bytes
+constexpr int kLCMaxSplit = 8;        // workgroups per image with a workspace
+constexpr int32_t kLCMaxB = 1 << 24;  // images per call (B x kLCMaxSplit workgroups fit a grid)
 
 struct LCParams {
   const uint4* x;      // packed rows
@@ -38,6 +50,8 @@ struct LCParams {
   int64_t total;
   float* out;          // [B, 2C]
   int32_t* status;
+  int32_t split;       // workgroups per image
+  float* part;         // split > 1: [B, split, C] sums of the workgroups
 };
 
 template <bool BF16>
@@ -99,15 +113,19 @@ __global__ __launch_bounds__((Flight<VPL, Piece<BF16>::kElems>::kWaves * 64)) vo
   static_assert(kLCWaves == kLCCombine || kLCWaves == 2 * kLCCombine, "two combine rounds at most");
   extern __shared__ float s_acc[];  // [kLCCombine][C], then the normalised CLS row [C]
   float* s_cls = s_acc + kLCCombine * p.C;
-  const int b = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int b = blockIdx.x / p.split, part_id = blockIdx.x - b * p.split;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lo = p.cu[b], hi = p.cu[b + 1];
   if (!(lo >= 0 && hi > lo && hi <= p.total && (b > 0 || lo == 0))) {
-    if (threadIdx.x == 0) {
+    if (threadIdx.x == 0 && part_id == 0) {
       atomicOr(p.status, DORA_DEV_CU_SEQLENS);
       for (int c = 0; c < 2 * p.C; ++c) p.out[static_cast<int64_t>(b) * 2 * p.C + c] = __builtin_nanf("");
     }
     return;
   }
+  // This workgroup's rows [rlo, rhi) of the image; CLS (row lo) falls in part 0.
+  const int per_part = (hi - lo + p.split - 1) / p.split;
+  const int rlo = min(hi, lo + part_id * per_part), rhi = min(hi, rlo + per_part);
   // Per lane: the sum over this wave's visual rows of (x - mean) * rstd for
   // its channels; gamma and beta are applied once at the end (the affine map
   // commutes with the mean).
@@ -123,7 +141,8 @@ __global__ __launch_bounds__((Flight<VPL, Piece<BF16>::kElems>::kWaves * 64)) vo
   // the compiler can count them in order instead of waiting for all of them;
   // values past the sequence or the row are masked to zero where they are used.
   constexpr int kStep = R * kLCWaves;
-  const int last_row = hi - 1, last_vec = p.vpr - 1;
+  // An empty range (rlo == rhi == hi) reads the image's last row, masked.
+  const int last_row = min(max(rhi, rlo + 1), hi) - 1, last_vec = p.vpr - 1;
   auto load = [&](int r0, uint4 (&dst)[R][VPL]) {
 #pragma unroll
     for (int q = 0; q < R; ++q)
@@ -138,7 +157,7 @@ __global__ __launch_bounds__((Flight<VPL, Piece<BF16>::kElems>::kWaves * 64)) vo
 #pragma unroll
     for (int q = 0; q < R; ++q) {
       s[q] = 0.0f;
-      const bool row_in = r0 + q * kLCWaves < hi;
+      const bool row_in = r0 + q * kLCWaves < rhi;
 #pragma unroll
       for (int i = 0; i < VPL; ++i) {
         const uint32_t mk = (row_in && lane + 64 * i < p.vpr) ? ~0u : 0u;
@@ -172,7 +191,7 @@ __global__ __launch_bounds__((Flight<VPL, Piece<BF16>::kElems>::kWaves * 64)) vo
       // a row past the sequence has d = 0; its scale is kept finite (1) so it
       // adds exactly nothing, without a branch
       const int r = r0 + q * kLCWaves;
-      const float pad = r < hi ? 0.0f : 1.0f;
+      const float pad = r < rhi ? 0.0f : 1.0f;
       const float rstd = 1.0f / sqrtf(ss[q] * inv_c + p.eps + pad);
       if (r == lo) {  // CLS: kept in LDS, gamma and beta applied at the end
 #pragma unroll
@@ -191,11 +210,11 @@ __global__ __launch_bounds__((Flight<VPL, Piece<BF16>::kElems>::kWaves * 64)) vo
     }
   };
   uint4 buf_a[R][VPL], buf_b[R][VPL];
-  int r0 = lo + wave;
+  int r0 = rlo + wave;
   load(r0, buf_a);
   // Whole rounds of two steps, one basic block (so no load is moved next to
   // its use); a step past the sequence sees masked rows and adds nothing.
-  for (; r0 < hi; r0 += 2 * kStep) {
+  for (; r0 < rhi; r0 += 2 * kStep) {
     load(r0 + kStep, buf_b);
     process(r0, buf_a);
     load(r0 + 2 * kStep, buf_a);
@@ -226,13 +245,43 @@ __global__ __launch_bounds__((Flight<VPL, Piece<BF16>::kElems>::kWaves * 64)) vo
   __syncthreads();
   const float inv_n = 1.0f / static_cast<float>(hi - lo - 1);
   float* o = p.out + static_cast<int64_t>(b) * 2 * p.C + p.C;
+  if (p.split == 1) {
+    for (int c = threadIdx.x; c < p.C; c += kLCThreads) {
+      float t = 0.0f;
+#pragma unroll
+      for (int w = 0; w < kLCCombine; ++w) t += s_acc[w * p.C + c];
+      const float gc = p.gamma[c], bc = p.beta[c];
+      o[c] = hi - lo > 1 ? t * inv_n * gc + bc : __builtin_nanf("");
+      o[c - p.C] = s_cls[c] * gc + bc;
+    }
+    return;
+  }
+  // Several workgroups per image: each writes its sum, part 0 the CLS half;
+  // lc1_combine_kernel, the next launch, adds the sums.
+  float* mine_part = p.part + (static_cast<int64_t>(b) * p.split + part_id) * p.C;
   for (int c = threadIdx.x; c < p.C; c += kLCThreads) {
     float t = 0.0f;
 #pragma unroll
     for (int w = 0; w < kLCCombine; ++w) t += s_acc[w * p.C + c];
-    const float gc = p.gamma[c], bc = p.beta[c];
-    o[c] = hi - lo > 1 ? t * inv_n * gc + bc : __builtin_nanf("");
-    o[c - p.C] = s_cls[c] * gc + bc;
+    mine_part[c] = t;
+    if (part_id == 0) o[c - p.C] = s_cls[c] * p.gamma[c] + p.beta[c];
+  }
+}
+
+// Mean half of the split readout: the parts' sums of image b added in part
+// order (the result does not depend on timing), scaled, gamma and beta.  An
+// invalid sequence keeps the NaN row the first launch wrote.
+__global__ __launch_bounds__(256) void lc1_combine_kernel(LCParams p) {
+  const int b = blockIdx.x;
+  const int lo = p.cu[b], hi = p.cu[b + 1];
+  if (!(lo >= 0 && hi > lo && hi <= p.total && (b > 0 || lo == 0))) return;
+  const float inv_n = 1.0f / static_cast<float>(hi - lo - 1);
+  const float* parts = p.part + static_cast<int64_t>(b) * p.split * p.C;
+  float* o = p.out + static_cast<int64_t>(b) * 2 * p.C + p.C;
+  for (int c = threadIdx.x; c < p.C; c += 256) {
+    float t = 0.0f;
+    for (int q = 0; q < p.split; ++q) t += parts[static_cast<int64_t>(q) * p.C + c];
+    o[c] = hi - lo > 1 ? t * inv_n * p.gamma[c] + p.beta[c] : __builtin_nanf("");
   }
 }
 
@@ -240,26 +289,42 @@ template <int VPL, bool BF16>
 hipError_t launch_lc1(const LCParams& p, hipStream_t stream) {
   const size_t lds = static_cast<size_t>(kLCCombine + 1) * p.C * sizeof(float);
   constexpr int threads = Flight<VPL, Piece<BF16>::kElems>::kWaves * 64;
-  hipLaunchKernelGGL((lc1_readout_kernel<VPL, BF16>), dim3(p.B), dim3(threads), lds, stream, p);
+  hipLaunchKernelGGL((lc1_readout_kernel<VPL, BF16>), dim3(p.B * p.split), dim3(threads), lds, stream, p);
+  if (p.split > 1) hipLaunchKernelGGL(lc1_combine_kernel, dim3(p.B), dim3(256), 0, stream, p);
   return hipGetLastError();
 }
+
 
 }  // namespace
 }  // namespace dora
 
+extern "C" size_t dora_lc1_readout_workspace_size(int32_t B, int32_t C) {
+  using namespace dora;
+  if (B < 1 || C < 1 || B > kLCMaxB || C > kLCMaxRowBytes / 2) return 0;
+  return static_cast<size_t>(B) * kLCMaxSplit * C * sizeof(float);  // [B, kLCMaxSplit, C] partial sums
+}
+
 extern "C" int dora_lc1_readout(const void* x, const int32_t* cu_seqlens, int64_t total, int32_t B, int32_t C,
                                 dora_dtype dtype, const float* gamma, const float* beta, float eps, float* out,
-                                int32_t* dev_status, void* stream) {
+                                void* workspace, size_t workspace_bytes, int32_t* dev_status, void* stream) {
   using namespace dora;
   if (!x || !cu_seqlens || !gamma || !beta || !out || !dev_status) return DORA_ERR_NULL;
   if (dtype != DORA_BF16 && dtype != DORA_F32) return DORA_ERR_DTYPE;
   const int elt = dtype == DORA_BF16 ? 2 : 4;
-  if (B < 1 || B > 0x7FFFFFFF / 2 || C < 1 || total < 1 || total > 0x7FFFFFFF || !(eps >= 0.0f))
+  if (B < 1 || B > kLCMaxB || C < 1 || total < 1 || total > 0x7FFFFFFF || !(eps >= 0.0f))
     return DORA_ERR_SHAPE;
   if ((static_cast<int64_t>(C) * elt) % 16 != 0 || reinterpret_cast<uintptr_t>(x) & 15u) return DORA_ERR_ALIGN;
   if (static_cast<int64_t>(C) * elt > kLCMaxRowBytes) return DORA_ERR_UNSUPPORTED;
   LCParams p{static_cast<const uint4*>(x), cu_seqlens, gamma, beta, eps, B, C, C * elt / 16, total, out,
-             dev_status};
+             dev_status, 1, nullptr};
+  if (workspace) {
+    if (reinterpret_cast<uintptr_t>(workspace) & 255u) return DORA_ERR_ALIGN;
+    if (workspace_bytes < dora_lc1_readout_workspace_size(B, C)) return DORA_ERR_WORKSPACE;
+    // About 256 workgroups in all, each with at least ~64 rows on average.
+    const int64_t by_grid = (256 + B - 1) / B, by_rows = total / (64 * static_cast<int64_t>(B));
+    p.split = static_cast<int32_t>(std::max<int64_t>(1, std::min<int64_t>({by_grid, by_rows, kLCMaxSplit})));
+    p.part = static_cast<float*>(workspace);
+  }
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int vpl = (p.vpr + 63) / 64;
   hipError_t err;

@@ -154,8 +154,8 @@ def test_lc1_host_validation():
     lib = dora.load_library()
 
     def call(**kw):
-        a = dict(x=FAKE, cu=FAKE, total=100, B=4, C=768, dtype=1, g=FAKE, b=FAKE, eps=1e-6, out=FAKE, st=FAKE,
-                 stream=None)
+        a = dict(x=FAKE, cu=FAKE, total=100, B=4, C=768, dtype=1, g=FAKE, b=FAKE, eps=1e-6, out=FAKE, ws=None,
+                 wsb=0, st=FAKE, stream=None)
         a.update(kw)
         return lib.dora_lc1_readout(*a.values())
 
@@ -168,6 +168,13 @@ def test_lc1_host_validation():
     assert call(B=0) == dora.DORA_ERR_SHAPE
     assert call(total=0) == dora.DORA_ERR_SHAPE
     assert call(eps=-1.0) == dora.DORA_ERR_SHAPE
+    assert call(B=(1 << 24) + 1) == dora.DORA_ERR_SHAPE
+    need = lib.dora_lc1_readout_workspace_size(4, 768)
+    assert need == 4 * 8 * 768 * 4
+    assert call(ws=FAKE, wsb=need - 1) == dora.DORA_ERR_WORKSPACE
+    assert call(ws=FAKE + 16, wsb=need) == dora.DORA_ERR_ALIGN
+    assert lib.dora_lc1_readout_workspace_size(0, 768) == 0
+    assert lib.dora_lc1_readout_workspace_size(4, 0) == 0
 
 
 def test_trajectory_flops_host_validation():

@@ -84,3 +84,54 @@ def test_invalid_sequences_set_status(gpu):
         assert int(st.item()) & gpu.DORA_DEV_CU_SEQLENS, cu
         bad = [i for i in range(3) if not (cu[i] >= 0 and cu[i + 1] > cu[i] and cu[i + 1] <= 20 and (i or cu[0] == 0))]
         assert np.all(np.isnan(o[bad])), cu
+
+
+def run_lc1(dora, x, cu, gamma, beta, eps=1e-6, **kw):
+    out, st = dora.dora_lc1_readout(to_dev(x), to_dev(cu), to_dev(gamma), to_dev(beta), eps, **kw)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    return out.cpu().numpy().astype(np.float64)
+
+
+@pytest.mark.parametrize("lens,C,dtype", [
+    ([1, 2, 600], 768, "bf16"),                    # only CLS; 2 rows over 3 parts (one empty); a long row
+    ([577] * 4 + [70] * 4, 768, "bf16"),           # skewed, few images: 5 parts per image
+    ([300, 1, 299, 5, 1000, 64], 192, "f32"),
+    ([129] * 16, 1024, "bf16"),
+])
+def test_split_and_single_workgroup_paths(gpu, lens, C, dtype):
+    """With a workspace a sequence's rows are split over several workgroups
+    and a second kernel adds their sums in part order; without one, one
+    workgroup per sequence.  Both meet the fp32 bound against the oracle, the
+    split result repeats bit for bit on a reused workspace, and a fresh
+    workspace gives the same bits."""
+    rng = np.random.default_rng(sum(lens) + C)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    x = (rng.standard_normal((int(cu[-1]), C)) * rng.uniform(0.5, 2, C) + rng.standard_normal(C)).astype(np.float32)
+    xs = W.f32_to_bf16_bits(x) if dtype == "bf16" else x
+    gamma = rng.uniform(0.5, 1.5, C).astype(np.float32)
+    beta = (0.1 * rng.standard_normal(C)).astype(np.float32)
+    want = oracle.lc1_readout(xs, cu, gamma, beta, 1e-6, dtype)
+    tol = fp32_bound(oracle.widen(xs, dtype), cu, gamma.astype(np.float64), beta.astype(np.float64), 1e-6)
+    ws = gpu.new_lc1_workspace(len(lens), C)
+    outs = [run_lc1(gpu, xs, cu, gamma, beta, workspace=ws) for _ in range(3)]
+    outs.append(run_lc1(gpu, xs, cu, gamma, beta))
+    single = run_lc1(gpu, xs, cu, gamma, beta, single=True)
+    nan = np.isnan(want)
+    for got in outs + [single]:
+        assert np.array_equal(np.isnan(got), nan)
+        err = np.where(nan, 0.0, np.abs(got - want))
+        assert np.all(err <= tol[:, None]), (err.max(), tol.min())
+    for got in outs[1:]:
+        assert np.array_equal(got, outs[0], equal_nan=True)
+    print(f"[lc1] split lens={lens[:4]}... C={C} {dtype} ok", flush=True)
+
+
+def test_vit_b384_skewed_batch(gpu):
+    """64 images of 577 tokens, half keeping 90-100 % and half 8-15 %."""
+    w = W.WORKLOADS["vit_b384_skew_bf16"]
+    keep = W.generate(w, parts=("keep",))[0].keep
+    x, gamma, beta = W.readout_rows(w, keep)
+    cu = np.concatenate([[0], np.cumsum(keep)]).astype(np.int32)
+    err = compare(gpu, x, cu, gamma, beta, w.dtype)
+    print(f"[lc1] vit_b384_skew_bf16 max err {err:.2e}", flush=True)

@@ -173,3 +173,22 @@ def test_invalid_cu_in_sets_status(gpu):
     assert st == 0
     *_, st, _ = run_gpu(gpu, scores, keep, tokens, cu_in=cu_in, N=8, cap=6)   # segment longer than N
     assert st & gpu.DORA_DEV_CU_IN
+
+
+@pytest.mark.parametrize("n", [257, 300, 577])
+def test_digit_prefix_ties_every_keep_count(gpu, n):
+    """Rows over 256 tokens select one 8-bit digit of the key at a time.
+    Scores whose bit patterns share every prefix of 1, 2 and 3 bytes with
+    many others (4 choices per byte, so about n / 4 keys per bucket at each
+    pass, and many exact ties), one image for every keep count 1..n."""
+    rng = np.random.default_rng(700 + n)
+    byte_vals = np.array([0x3F, 0x40, 0xBF, 0xC0], np.uint32)                # both signs, around 1.0 and 2.0
+    low_vals = np.array([0x00, 0x01, 0x80, 0xFF], np.uint32)
+    bits = (byte_vals[rng.integers(0, 4, n)] << 24) | (low_vals[rng.integers(0, 4, n)] << 16) \
+        | (low_vals[rng.integers(0, 4, n)] << 8) | low_vals[rng.integers(0, 4, n)]
+    row = bits.astype(np.uint32).view(np.float32)
+    scores = np.tile(row, (n, 1))
+    keep = np.arange(1, n + 1, dtype=np.int32)
+    tokens = rng.integers(0, 2 ** 16, size=(n, n, 8)).astype(np.uint16)
+    print(f"[select_pack] digit prefix ties n={n}", flush=True)
+    check_round(gpu, scores, keep, tokens)
