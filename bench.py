@@ -80,7 +80,7 @@ KERNEL_NAMES = {"attn": ("attn_fwd_bf16_kernel", "attn_fwd_f32_kernel"),
                 "residual": ("select_pack_residual_kernel",),
                 "actor": ("actor_gate_kernel", "actor_decode_kernel"),
                 "pl": ("pl_kernel",),
-                "lc1": ("lc1_readout_kernel",),
+                "lc1": ("lc1_readout_kernel", "lc1_combine_kernel"),
                 "flops": ("trajectory_flops_kernel",),
                 "plan": ("attn_plan_kernel",)}
 
@@ -595,7 +595,8 @@ def main() -> int:
         ms_lc1 = time_calls(lc1_call)
         assert int(st_l.item()) == 0, f"device status {int(st_l.item())}"
         lb = lc1_bytes(w, r.keep)
-        lc1 = {"entry": "dora_lc1_readout", "kernel": "lc1_readout_kernel", "bound": "hbm", "us": ms_lc1 * 1e3,
+        lc1 = {"entry": "dora_lc1_readout", "kernel": "lc1_readout_kernel (+ lc1_combine_kernel when split)",
+               "bound": "hbm", "us": ms_lc1 * 1e3,
                "achieved": lb / (ms_lc1 * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                "frac": lb / (ms_lc1 * 1e-3) / 1e9 / HBM_PEAK_GBS, "algorithmic_bytes": lb, "regime": "warm"}
         print(f"[bench] lc1 readout: {ms_lc1 * 1e3:.1f} us per launch ({lc1['achieved']:.0f} GB/s)",
