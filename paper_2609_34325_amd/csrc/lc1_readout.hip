@@ -272,17 +272,24 @@ __global__ __launch_bounds__((Flight<VPL, Piece<BF16>::kElems>::kWaves * 64)) vo
 // order (the result does not depend on timing), scaled, gamma and beta.  An
 // invalid sequence keeps the NaN row the first launch wrote.
 __global__ __launch_bounds__(256) void lc1_combine_kernel(LCParams p) {
-  const int b = blockIdx.x;
+  const int b = blockIdx.x, c = blockIdx.y * 256 + threadIdx.x;
   const int lo = p.cu[b], hi = p.cu[b + 1];
-  if (!(lo >= 0 && hi > lo && hi <= p.total && (b > 0 || lo == 0))) return;
+  if (c >= p.C || !(lo >= 0 && hi > lo && hi <= p.total && (b > 0 || lo == 0))) return;
+  // One channel per thread; the loads of all parts are issued together
+  // (parts past split re-read the last one and add zero), and the empty asm
+  // keeps the compiler from moving each load into a branch of its own.
+  const float* parts = p.part + static_cast<int64_t>(b) * p.split * p.C + c;
+  float v[kLCMaxSplit];
+#pragma unroll
+  for (int q = 0; q < kLCMaxSplit; ++q) v[q] = parts[static_cast<int64_t>(min(q, p.split - 1)) * p.C];
+#pragma unroll
+  for (int q = 0; q < kLCMaxSplit; ++q) asm volatile("" : "+v"(v[q]));
+  float t = 0.0f;
+#pragma unroll
+  for (int q = 0; q < kLCMaxSplit; ++q) t += q < p.split ? v[q] : 0.0f;
   const float inv_n = 1.0f / static_cast<float>(hi - lo - 1);
-  const float* parts = p.part + static_cast<int64_t>(b) * p.split * p.C;
-  float* o = p.out + static_cast<int64_t>(b) * 2 * p.C + p.C;
-  for (int c = threadIdx.x; c < p.C; c += 256) {
-    float t = 0.0f;
-    for (int q = 0; q < p.split; ++q) t += parts[static_cast<int64_t>(q) * p.C + c];
-    o[c] = hi - lo > 1 ? t * inv_n * p.gamma[c] + p.beta[c] : __builtin_nanf("");
-  }
+  p.out[static_cast<int64_t>(b) * 2 * p.C + p.C + c] = hi - lo > 1 ? t * inv_n * p.gamma[c] + p.beta[c]
+                                                                  : __builtin_nanf("");
 }
 
 template <int VPL, bool BF16>
@@ -290,7 +297,7 @@ hipError_t launch_lc1(const LCParams& p, hipStream_t stream) {
   const size_t lds = static_cast<size_t>(kLCCombine + 1) * p.C * sizeof(float);
   constexpr int threads = Flight<VPL, Piece<BF16>::kElems>::kWaves * 64;
   hipLaunchKernelGGL((lc1_readout_kernel<VPL, BF16>), dim3(p.B * p.split), dim3(threads), lds, stream, p);
-  if (p.split > 1) hipLaunchKernelGGL(lc1_combine_kernel, dim3(p.B), dim3(256), 0, stream, p);
+  if (p.split > 1) hipLaunchKernelGGL(lc1_combine_kernel, dim3(p.B, (p.C + 255) / 256), dim3(256), 0, stream, p);
   return hipGetLastError();
 }
 
