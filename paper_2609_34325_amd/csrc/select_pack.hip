@@ -393,12 +393,7 @@ hipError_t launch(const SelectPackParams& p, int mode, hipStream_t stream) {
 }
 
 int pick_split(int B, int N) {
-  static int override_split = -1;
-  if (override_split < 0) {
-    const char* e = getenv("DORA_SELECT_SPLIT");
-    override_split = e ? atoi(e) : 0;
-  }
-  int split = override_split > 0 ? override_split : (1024 + B - 1) / B;  // ~4 workgroups per compute unit
+  int split = (1024 + B - 1) / B;  // ~4 workgroups per compute unit
   const int max_split = N / 16 > 1 ? N / 16 : 1;  // at least ~16 rows per workgroup
   if (split > max_split) split = max_split;
   if (split < 1) split = 1;
