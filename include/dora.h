@@ -21,7 +21,8 @@
  *   - All array arguments are DEVICE pointers allocated by the caller; the
  *     library never allocates device memory, never frees caller memory and
  *     keeps no state between calls other than a per-device cache of the
- *     compute-unit count.
+ *     compute-unit count and of the attention kernels' occupancy (atomics,
+ *     safe to fill from several host threads at once).
  *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
  *     Every call only enqueues work on that stream and returns without
  *     synchronising the host.

@@ -36,6 +36,8 @@
 #include <limits.h>
 #include <math.h>
 
+#include <atomic>
+
 #include "dora_internal.h"
 
 namespace dora {
@@ -1014,37 +1016,40 @@ __global__ __launch_bounds__(kF32Threads) void attn_fwd_f32_kernel(AttnParams p)
 }
 
 // Persistent grid: every compute unit filled to the kernel's occupancy.
+// The occupancy is queried once per device and kernel and cached; the cache
+// entries are atomics, so concurrent first calls from several host threads
+// store the same value without a data race.
 template <typename KernelT>
 int persistent_grid(KernelT kernel, int threads, int slot, int* grid) {
-  static int per_cu_cache[64][2];
+  static std::atomic<int> per_cu_cache[64][2];
   int dev = 0;
   const int cus = device_cu_count(&dev);
   if (cus <= 0 || dev >= 64) return DORA_ERR_HIP;
-  if (per_cu_cache[dev][slot] == 0) {
-    int per_cu = 0;
+  int per_cu = per_cu_cache[dev][slot].load(std::memory_order_relaxed);
+  if (per_cu == 0) {
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess ||
         per_cu < 1)
       per_cu = 1;
-    per_cu_cache[dev][slot] = per_cu;
+    per_cu_cache[dev][slot].store(per_cu, std::memory_order_relaxed);
   }
-  *grid = cus * per_cu_cache[dev][slot];
+  *grid = cus * per_cu;
   return DORA_OK;
 }
 
 }  // namespace
 
 int device_cu_count(int* device_out) {
-  static int cache[64];
+  static std::atomic<int> cache[64];  // per device, written once (same value from any thread)
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return -1;
   if (device_out) *device_out = dev;
   if (dev < 0 || dev >= 64) return -1;
-  if (cache[dev] == 0) {
-    int n = 0;
+  int n = cache[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return -1;
-    cache[dev] = n;
+    cache[dev].store(n, std::memory_order_relaxed);
   }
-  return cache[dev];
+  return n;
 }
 
 }  // namespace dora
