@@ -135,3 +135,28 @@ def test_vit_b384_skewed_batch(gpu):
     cu = np.concatenate([[0], np.cumsum(keep)]).astype(np.int32)
     err = compare(gpu, x, cu, gamma, beta, w.dtype)
     print(f"[lc1] vit_b384_skew_bf16 max err {err:.2e}", flush=True)
+
+
+def test_invalid_sequence_on_the_split_path(gpu):
+    """An empty sequence among long ones, with a workspace (so the rows are
+    split over several workgroups): its row is NaN with DORA_DEV_CU_SEQLENS,
+    and the valid sequences still meet the bound against the oracle."""
+    rng = np.random.default_rng(4)
+    C = 256
+    cu = np.array([0, 300, 300, 900], np.int32)                            # sequence 1 is empty
+    x = W.f32_to_bf16_bits(rng.standard_normal((900, C)).astype(np.float32))
+    gamma = rng.uniform(0.5, 1.5, C).astype(np.float32)
+    beta = (0.1 * rng.standard_normal(C)).astype(np.float32)
+    assert 900 // (64 * 3) >= 2                                            # the host picks a split > 1
+    out, st = gpu.dora_lc1_readout(to_dev(x), to_dev(cu), to_dev(gamma), to_dev(beta), 1e-6,
+                                   workspace=gpu.new_lc1_workspace(3, C))
+    torch.cuda.synchronize()
+    assert int(st.item()) & gpu.DORA_DEV_CU_SEQLENS
+    o = out.cpu().numpy().astype(np.float64)
+    assert np.all(np.isnan(o[1]))
+    for b in (0, 2):
+        seg = np.array([0, cu[b + 1] - cu[b]], np.int32)
+        xb = x[cu[b]:cu[b + 1]]
+        want = oracle.lc1_readout(xb, seg, gamma, beta, 1e-6, "bf16")[0]
+        tol = fp32_bound(oracle.widen(xb, "bf16"), seg, gamma.astype(np.float64), beta.astype(np.float64), 1e-6)
+        assert np.all(np.abs(o[b] - want) <= tol[0]), b
