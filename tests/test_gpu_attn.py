@@ -1,9 +1,9 @@
 """GPU parity for dora_varlen_attn against the fp64 oracle.
 
 bf16 inputs: max |err| <= 2e-2 and mean |err| <= 2e-3; fp32 inputs:
-max |err| <= 1e-5.  Small cases compare every element; full-size workloads
-(in the launch configuration the benchmark times) compare sampled sequences
-element by element and check a bound that holds at any size on all outputs.
+max |err| <= 1e-5.  Every case compares every output element with the
+oracle, the full-size workloads included (in the launch configuration the
+benchmark times).
 """
 import numpy as np
 import pytest
@@ -85,49 +85,27 @@ def test_deit_s_bf16_workload(gpu):
     print(f"[attn] {w.name} max err {mx:.2e} mean {mean:.2e}", flush=True)
 
 
-def sampled_compare(dora, r, dtype, nsample, seed, what):
-    cu = cu_of(r.keep)
-    out, st = gpu_attn(dora, r.q, r.k, r.v, cu)
-    assert st == 0
-    got_all = widen(out)
-    # Any size: each output is a convex combination of its sequence's V rows.
-    vv = W.bf16_bits_to_f32(r.v).astype(np.float64) if dtype == "bf16" else r.v.astype(np.float64)
-    lens = np.diff(cu)
-    nz = lens > 0
-    vmax = np.maximum.reduceat(vv, cu[:-1][nz], axis=0)
-    vmin = np.minimum.reduceat(vv, cu[:-1][nz], axis=0)
-    seg = np.repeat(np.arange(nz.sum()), lens[nz])
-    slack = 1e-2 if dtype == "bf16" else 1e-6
-    assert np.all(np.isfinite(got_all))
-    assert np.all(got_all <= vmax[seg] + slack) and np.all(got_all >= vmin[seg] - slack)
-    # Sampled sequences, element by element: longest, shortest and random ones.
-    rng = np.random.default_rng(seed)
-    order = np.argsort(lens)
-    pick = sorted(set([int(order[-1]), int(order[0])] + list(rng.choice(len(lens), nsample, replace=False))))
-    want = oracle.varlen_attn_segments(r.q, r.k, r.v, cu, pick, dtype)
-    got = np.concatenate([got_all[cu[b]:cu[b + 1]] for b in pick])
-    ref = np.concatenate([want[b] for b in pick])
-    return assert_attn_close(got, ref, dtype, what)
-
-
-def test_deit_b_bf16_full_size_sampled(gpu):
+def test_deit_b_bf16_full_size(gpu):
+    """The headline batch (B = 256, H = 12), every output element."""
     w = W.WORKLOADS["deit_b_bf16"]
     r = W.generate(w, parts=("keep", "qkv"))[0]
-    mx, mean = sampled_compare(gpu, r, "bf16", 14, 1, w.name)
-    print(f"[attn] {w.name} sampled max err {mx:.2e} mean {mean:.2e}", flush=True)
+    mx, mean = full_compare(gpu, r.q, r.k, r.v, cu_of(r.keep), "bf16", what=w.name)
+    print(f"[attn] {w.name} max err {mx:.2e} mean {mean:.2e}", flush=True)
 
 
-def test_vit_b384_skew_full_size_sampled(gpu):
+def test_vit_b384_skew_full_size(gpu):
+    """The skewed ViT-B/384 batch (sequences of 46-577 tokens), every element."""
     w = W.WORKLOADS["vit_b384_skew_bf16"]
     r = W.generate(w, parts=("keep", "qkv"))[0]
-    mx, mean = sampled_compare(gpu, r, "bf16", 6, 2, w.name)
-    print(f"[attn] {w.name} sampled max err {mx:.2e} mean {mean:.2e}", flush=True)
+    mx, mean = full_compare(gpu, r.q, r.k, r.v, cu_of(r.keep), "bf16", what=w.name)
+    print(f"[attn] {w.name} max err {mx:.2e} mean {mean:.2e}", flush=True)
 
 
-def test_vit_l_cascade_rounds_sampled(gpu):
+def test_vit_l_cascade_rounds_full_size(gpu):
+    """Each of the three ViT-L rounds (H = 16), every element."""
     w = W.WORKLOADS["vit_l_cascade_bf16"]
     for i, r in enumerate(W.generate(w, parts=("keep", "qkv"))):
-        mx, mean = sampled_compare(gpu, r, "bf16", 6, 3 + i, f"{w.name} round {i}")
+        mx, mean = full_compare(gpu, r.q, r.k, r.v, cu_of(r.keep), "bf16", what=f"{w.name} round {i}")
         print(f"[attn] {w.name} round {i} max err {mx:.2e} mean {mean:.2e}", flush=True)
 
 
@@ -225,21 +203,16 @@ def test_invalid_offsets_set_status(gpu):
 
 def test_maximum_sequence_length(gpu):
     """One sequence of DORA_MAX_SEQLEN tokens (86 query chunks, 64 key
-    stages): sampled query rows against the oracle, and the convex-hull bound
-    on every output."""
+    stages), every output row against the oracle."""
     n = gpu.DORA_MAX_SEQLEN
     rng = np.random.default_rng(42)
     q, k, v = qkv(rng, [n], 1, "bf16")
     cu = cu_of([n])
     out, st = gpu_attn(gpu, q, k, v, cu)
     assert st == 0
-    got = widen(out)
-    vv = W.bf16_bits_to_f32(v).astype(np.float64)
-    assert np.all(np.isfinite(got))
-    assert np.all(got <= vv.max(axis=0) + 1e-2) and np.all(got >= vv.min(axis=0) - 1e-2)
-    rows = np.unique(np.concatenate([[0, 191, 192, n - 193, n - 1], rng.choice(n, 40, replace=False)]))
-    want = oracle.varlen_attn_rows(q, k, v, cu, rows, "bf16")
-    assert_attn_close(got[rows], want, "bf16", "len 16384")
+    want = oracle.varlen_attn_rows(q, k, v, cu, np.arange(n), "bf16")
+    mx, mean = assert_attn_close(widen(out), want, "bf16", "len 16384")
+    print(f"[attn] len {n} max err {mx:.2e} mean {mean:.2e}", flush=True)
 
 
 def test_maximum_sequence_count(gpu):

@@ -88,13 +88,9 @@ def test_fused_plan_matches_oracle_and_separate_plan(gpu, name):
     torch.cuda.synchronize()
     assert int(st_t.item()) == 0
     assert np.array_equal(to_host_bits(out_fused), to_host_bits(out_sep))
-    # and against the oracle on a few whole images
-    rng = np.random.default_rng(5)
-    for b in rng.choice(w.B, size=min(4, w.B), replace=False):
-        a, e = int(cu_o[b]), int(cu_o[b + 1])
-        seg = np.array([0, e - a], np.int32)
-        want = oracle.varlen_attn(r.q[a:e], r.k[a:e], r.v[a:e], seg, w.dtype)
-        assert_attn_close(widen(out_fused[a:e]), want, w.dtype, f"image {b}")
+    # and against the oracle, every element
+    want = oracle.varlen_attn(r.q, r.k, r.v, cu_o, w.dtype)
+    assert_attn_close(widen(out_fused), want, w.dtype, name)
 
 
 def test_fused_plan_on_cascade_round(gpu):
