@@ -5,17 +5,22 @@ One step = one pass of the whole path over one batch:
                                gather, and the attention work queue of the
                                packed layout, in one launch)
     dora_varlen_attn_execute  (varlen attention, bf16 MFMA)
-on synthetic inputs already resident in HBM.  Prints one JSON line.  Beside
-the step it also times, on the same batch, the adjacent entry points:
-dora_select_pack_residual (the kept rows of tokens + attention output), the
-actor decode (dora_actor_gate + dora_actor_decode), dora_lc1_readout,
-dora_trajectory_flops and dora_pl_sample.
+on synthetic inputs already resident in HBM; a cascaded workload chains its
+rounds inside one step (round r+1 reads round r's packed output and
+cu_seqlens).  Prints one JSON line for the headline workload (DeiT-B), with a
+record of its own for every other workload, each checked against the oracle
+in the CPU-baseline leg.  Beside the step it also times, on the headline
+batch, the adjacent entry points: dora_select_pack_residual (the kept rows of
+tokens + attention output), the actor decode (dora_actor_gate +
+dora_actor_decode), dora_lc1_readout, dora_trajectory_flops and
+dora_pl_sample.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 """
 from __future__ import annotations
 
 import argparse
+import collections
 import json
 import os
 import platform
@@ -33,19 +38,21 @@ import workloads as W  # noqa: E402
 HBM_PEAK_GBS = 8000.0            # MI355X HBM3E, GB/s
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # dense matrix peaks, TFLOP/s
 METRIC = "packed tokens/s + varlen-attn TFLOP/s (% MFMA peak), DeiT-B shape, B=256"
+# Workloads with a record of their own next to the headline (the DINOv2 shape
+# serves the LC1 readout only).
+CONFIG_ORDER = ("deit_tiny_fp32", "deit_s_bf16", "deit_b_bf16", "vit_l_cascade_bf16", "vit_b384_skew_bf16")
+BF16_MAX_ABS, BF16_MEAN_ABS, F32_MAX_ABS = 2e-2, 2e-3, 1e-5   # attention tolerances
 
 
-def plan_items(w: W.Workload, keep: np.ndarray) -> int:
-    """Attention work items: one per (image, head, chunk of 192 queries)."""
-    return w.H * int(np.sum((keep.astype(np.int64) + 191) // 192))
-
-
-def select_pack_bytes(w: W.Workload, keep: np.ndarray, n_in: np.ndarray) -> int:
+def select_pack_bytes(w: W.Workload, keep: np.ndarray, n_in: np.ndarray, n_items: int, packed_in: bool) -> int:
     """Algorithmic HBM bytes of select/pack with its attention plan: read scores
-    and keep, read and write each kept row once, write the kept indices,
-    cu_seqlens, the plan's items (8 bytes each) and its 2 KB header."""
+    and keep (and cu_in for packed input), read and write each kept row once,
+    write the kept indices, cu_seqlens, the plan's items (8 bytes each) and
+    its 2 KB header."""
     sk = int(keep.sum())
-    return 2 * sk * w.C * w.elt + 4 * (int(n_in.sum()) + sk + 2 * w.B + 1) + 8 * plan_items(w, keep) + 2048
+    B = len(keep)
+    cu_in = 4 * (B + 1) if packed_in else 0
+    return 2 * sk * w.C * w.elt + 4 * (int(n_in.sum()) + sk + 2 * B + 1) + cu_in + 8 * n_items + 2048
 
 
 def residual_bytes(w: W.Workload, keep: np.ndarray, n_in: np.ndarray) -> int:
@@ -63,6 +70,7 @@ def lc1_bytes(w: W.Workload, keep: np.ndarray) -> int:
 
 
 def attn_flops(w: W.Workload, keep: np.ndarray) -> float:
+    """4 H d sum(k^2): QK^T and PV of every (sequence, head)."""
     k = keep.astype(np.float64)
     return 4.0 * w.H * W.HEAD_DIM * float(np.sum(k * k))
 
@@ -76,7 +84,7 @@ KERNEL_SOURCES = {"lc1": "paper_2609_34325_amd/csrc/lc1_readout.hip",
                   "select_pack": "paper_2609_34325_amd/csrc/select_pack.hip",
                   "residual": "paper_2609_34325_amd/csrc/select_pack.hip"}
 KERNEL_NAMES = {"attn": ("attn_fwd_bf16_kernel", "attn_fwd_f32_kernel"),
-                "select_pack": ("select_pack_kernel",),
+                "select_pack": ("select_pack_kernel", "keep_scan_kernel"),
                 "residual": ("select_pack_residual_kernel",),
                 "actor": ("actor_gate_kernel", "actor_decode_kernel"),
                 "pl": ("pl_kernel",),
@@ -118,14 +126,49 @@ def _kernel_key(name: str):
     return None
 
 
-def summarize_profile(d: str, workload: str, traffic_json: str, calib_mib: int) -> int:
+class PhaseLog:
+    """Launch counts per kernel key for each timed phase, in launch order, so
+    that a rocprofv3 kernel trace of the same run can be split by phase (one
+    stream, phases separated by synchronisation)."""
+
+    def __init__(self):
+        self.phases = []   # [name, {key: count}]
+
+    def start(self, name: str):
+        self.phases.append([name, collections.Counter()])
+
+    def count(self, *keys):
+        if not self.phases:
+            self.start("setup")
+        for k in keys:
+            self.phases[-1][1][k] += 1
+
+    def dump(self, path: str):
+        with open(path, "w") as fh:
+            json.dump([[n, dict(c)] for n, c in self.phases], fh, indent=0)
+
+
+def split_by_phase(dispatches: dict, phase_log: list) -> dict:
+    """dispatches: key -> durations (ns) in dispatch order.  Returns
+    phase -> key -> durations."""
+    pos = collections.defaultdict(int)
+    out = collections.defaultdict(dict)
+    for name, counts in phase_log:
+        for k, n in counts.items():
+            seq = dispatches.get(k, [])
+            out[name][k] = seq[pos[k]:pos[k] + n]
+            pos[k] += n
+    return out
+
+
+def summarize_profile(d: str, workload: str, traffic_json: str, calib_mib: int, phase_log: str = None) -> int:
     """Reads the rocprofv3 CSV output of three runs of this script under
     DIR/stats (--kernel-trace --stats), DIR/fetch (--pmc FETCH_SIZE) and
     DIR/write (--pmc WRITE_SIZE), each run with --calibrate-copy; scales the
     counters by what they read for the plain calibration copy; prints a
-    markdown summary and stores the per-launch bytes in the traffic file."""
+    markdown summary (with the kernel trace split by the bench's phases when
+    a phase log is given) and stores the per-launch bytes in the traffic file."""
     import csv
-    import collections
     lines = []
     stats = os.path.join(d, "stats", "run_kernel_stats.csv")
     if os.path.exists(stats):
@@ -134,6 +177,22 @@ def summarize_profile(d: str, workload: str, traffic_json: str, calib_mib: int) 
             name = r["Name"].replace("dora::(anonymous namespace)::", "").replace("void ", "").split("(")[0]
             lines.append(f"| {name} | {r['Calls']} | {float(r['AverageNs']):,.0f} | {int(r['MinNs']):,} | "
                          f"{int(r['MaxNs']):,} | {float(r['Percentage']):.1f} % |")
+        lines.append("")
+    trace = os.path.join(d, "stats", "run_kernel_trace.csv")
+    if phase_log and os.path.exists(trace) and os.path.exists(phase_log):
+        rows = sorted(csv.DictReader(open(trace)), key=lambda r: int(r["Dispatch_Id"]))
+        disp = collections.defaultdict(list)
+        for r in rows:
+            k = _kernel_key(r["Kernel_Name"])
+            if k is not None:
+                disp[k].append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+        per = split_by_phase(disp, json.load(open(phase_log)))
+        lines += ["Kernel trace split by the bench's phases (average duration per launch):", "",
+                  "| Phase | Kernel | Launches | Average (ns) |", "|---|---|---|---|"]
+        for name, ks in per.items():
+            for k, v in sorted(ks.items()):
+                if v:
+                    lines.append(f"| {name} | {k} | {len(v)} | {sum(v) / len(v):,.0f} |")
         lines.append("")
     calib_kib = calib_mib * 1024.0
     measured = collections.defaultdict(dict)
@@ -181,9 +240,10 @@ def summarize_profile(d: str, workload: str, traffic_json: str, calib_mib: int) 
             entry[k] = {"bytes_per_launch": total, "fetch_bytes": m["FETCH_SIZE"][1],
                         "write_bytes": m["WRITE_SIZE"][1], "source_sha": source_digest(KERNEL_SOURCES[k]),
                         "fetch_factor": factors["FETCH_SIZE"], "write_factor": factors["WRITE_SIZE"]}
-    with open(traffic_json, "w") as fh:
-        json.dump(allt, fh, indent=1, sort_keys=True)
-        fh.write("\n")
+    if measured:
+        with open(traffic_json, "w") as fh:
+            json.dump(allt, fh, indent=1, sort_keys=True)
+            fh.write("\n")
     print("\n".join(lines))
     return 0
 
@@ -201,7 +261,6 @@ def summarize_pmc(d: str, workload: str) -> int:
     LDS bank conflicts per LDS access cycle.  Averages are per dispatch, over
     the launches after the first two."""
     import csv
-    import collections
     w = W.WORKLOADS[workload]
     keep = W.generate(w, parts=("keep",))[0].keep
     alg = {"attn": attn_flops(w, keep)}
@@ -305,33 +364,263 @@ def cpu_model() -> str:
     return platform.processor() or "unknown"
 
 
-def run_cpu_baseline(w: W.Workload, r: W.RoundInputs, repeats: int = 9, repeats_1: int = 3) -> dict:
-    """The oracle as it stands, timed on this host's cores over the full batch:
-    the median of `repeats` passes on all the process's cores and of
-    `repeats_1` passes on one thread (about 8-12 s of CPU work at DeiT-B)."""
+def _median_rep(reps):
+    return sorted(reps, key=lambda x: x[0] if isinstance(x, tuple) else x)[len(reps) // 2]
+
+
+class ConfigRun:
+    """Device buffers and launches of one workload's step (all its rounds)."""
+
+    def __init__(self, w: W.Workload, torch, dora, stream, phases: PhaseLog):
+        self.w, self.torch, self.dora, self.stream, self.phases = w, torch, dora, stream, phases
+        self.rounds = W.generate(w)
+        self.R = len(self.rounds)
+        self.max_seqlen = [int(r.keep.max()) for r in self.rounds]
+        self.sum_keep = [r.total_keep for r in self.rounds]
+        self.sets = [self._buffers()]
+
+    def dev(self, a):
+        torch = self.torch
+        if a.dtype == np.uint16:
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+    def _buffers(self, src=None):
+        """Inputs (uploaded, or copied from the buffer set `src`) and outputs of
+        every round of one step."""
+        torch, dora, w = self.torch, self.dora, self.w
+        rounds = []
+        for i, r in enumerate(self.rounds):
+            b = {}
+            names = ("scores", "keep", "q", "k", "v") + (("tokens",) if i == 0 else ())
+            for name in names:
+                b[name] = src[i][name].clone() if src is not None else self.dev(getattr(r, name))
+            sk = r.total_keep
+            dt = rounds[0]["tokens"].dtype if i > 0 else b["tokens"].dtype
+            b["idx"] = torch.empty(sk, dtype=torch.int32, device="cuda")
+            b["cu"] = torch.empty(w.B + 1, dtype=torch.int32, device="cuda")
+            b["packed"] = torch.empty((sk, w.C), dtype=dt, device="cuda")
+            b["out"] = torch.empty_like(b["q"])
+            b["ws"] = dora.new_workspace(w.B, w.H, self.max_seqlen[i])
+            b["st"] = dora.new_status()
+            rounds.append(b)
+        return rounds
+
+    def launches(self, bs):
+        """The step's launches in order: (kernel key, round, callable)."""
+        dora, w, stream = self.dora, self.w, self.stream
+        out = []
+        for i in range(self.R):
+            b = bs[i]
+            prev = bs[i - 1] if i > 0 else None
+            sk, ms = self.sum_keep[i], self.max_seqlen[i]
+
+            def sp(b=b, prev=prev, sk=sk, ms=ms):
+                dora.dora_select_pack_plan(
+                    b["scores"], b["keep"], b["tokens"] if prev is None else prev["packed"], w.H, ms, sk, b["ws"],
+                    cu_in=None if prev is None else prev["cu"], N=None if prev is None else w.N,
+                    idx_out=b["idx"], cu_out=b["cu"], packed_out=b["packed"], cap_rows=sk, dev_status=b["st"],
+                    stream=stream)
+
+            def at(b=b, ms=ms):
+                dora.dora_varlen_attn_execute(b["q"], b["k"], b["v"], b["cu"], ms, b["ws"], out=b["out"],
+                                              dev_status=b["st"], stream=stream)
+
+            out += [("select_pack", i, sp), ("attn", i, at)]
+        return out
+
+    def step(self, bs, evs=None):
+        ls = self.launches(bs)
+        if evs is not None:
+            evs[0].record(self.stream)
+        for j, (key, _, fn) in enumerate(ls):
+            fn()
+            self.phases.count(key)
+            if evs is not None:
+                evs[j + 1].record(self.stream)
+
+    def check_status(self, sets=None):
+        for bs in sets or self.sets:
+            for b in bs:
+                st = int(b["st"].item())
+                assert st == 0, f"{self.w.name}: device status {st}"
+
+    def plan_items(self, i: int) -> tuple:
+        """(items, queries per item) of round i's plan, read from the plan header."""
+        hdr = self.sets[0][i]["ws"][:32].view(self.torch.int32).cpu().numpy()
+        return int(hdr[2]), int(hdr[7])
+
+    def host_outputs(self):
+        torch = self.torch
+        res = []
+        for b in self.sets[0]:
+            def bits(t):
+                return t.view(torch.int16).cpu().numpy().view(np.uint16) if t.dtype == torch.bfloat16 \
+                    else t.cpu().numpy()
+            res.append({"idx": b["idx"].cpu().numpy(), "cu": b["cu"].cpu().numpy(),
+                        "packed": bits(b["packed"]), "out": bits(b["out"])})
+        return res
+
+
+def time_steps(run: ConfigRun, sets, args, tag: str):
+    """Median over repeats of the step time (ms) and of each launch's duration
+    (ms, HIP events around every kernel).  Step i uses sets[i % len(sets)].
+    Each repeat times K steps twice: bare (events only at the two ends) and
+    with events around every kernel (an event between two kernels adds a few
+    microseconds of dispatch latency to the interval, so these are upper
+    bounds)."""
+    torch, stream, phases = run.torch, run.stream, run.phases
+    phases.start(f"{run.w.name}:{tag}:warmup")
+    for i in range(args.warmup):
+        run.step(sets[i % len(sets)])
+    torch.cuda.synchronize()
+    n = 2 * run.R
+    reps = []
+    for rep in range(args.repeats):
+        phases.start(f"{run.w.name}:{tag}:bare")
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0.record(stream)
+        for i in range(args.steps):
+            run.step(sets[i % len(sets)])
+        t1.record(stream)
+        torch.cuda.synchronize()
+        step_ms = t0.elapsed_time(t1) / args.steps
+        phases.start(f"{run.w.name}:{tag}:events")
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n + 1)] for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        for i in range(args.steps):
+            run.step(sets[i % len(sets)], evs[i])
+        torch.cuda.synchronize()
+        per = [float(np.mean([e[j].elapsed_time(e[j + 1]) for e in evs])) for j in range(n)]
+        reps.append((step_ms, per))
+        print(f"[bench] {run.w.name} {tag} repeat {rep}: {step_ms * 1e3:.1f} us/step (per kernel with events: "
+              + ", ".join(f"{k}{r} {p * 1e3:.1f}" for (k, r, _), p in zip(run.launches(sets[0]), per)) + ")",
+              file=sys.stderr, flush=True)
+    run.check_status(sets)
+    return _median_rep(reps)
+
+
+def time_calls(torch, stream, fn, args, phases=None, tag=None, keys=()):
+    """Median over repeats of the mean time (ms) of `steps` back-to-back calls
+    of fn (after `warmup` calls), HIP events at the two ends."""
+    if phases is not None:
+        phases.start(f"{tag}:warmup")
+    for _ in range(args.warmup):
+        fn()
+        if phases is not None:
+            phases.count(*keys)
+    reps = []
+    for _ in range(args.repeats):
+        if phases is not None:
+            phases.start(f"{tag}:timed")
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            fn()
+            if phases is not None:
+                phases.count(*keys)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        reps.append(e0.elapsed_time(e1) / args.steps)
+    return sorted(reps)[len(reps) // 2]
+
+
+def bench_config(run: ConfigRun, args) -> dict:
+    """Step timing (bare and per kernel), each kernel alone back to back on
+    the same buffers, and the rates, for every round of one workload."""
+    torch, stream, w = run.torch, run.stream, run.w
+    step_ms, per = time_steps(run, run.sets, args, "warm")
+    ls = run.launches(run.sets[0])
+    alone = []
+    for key, i, fn in ls:
+        alone.append(time_calls(torch, stream, fn, args, run.phases, f"{w.name}:alone:{key}{i}", (key,)))
+    run.check_status()
+    peak = MFMA_PEAK_TFLOPS[w.dtype]
+    rec = {"B": w.B, "N": w.N, "H": w.H, "C": w.C, "dtype": w.dtype, "rounds": run.R,
+           "sum_keep": run.sum_keep, "max_seqlen": run.max_seqlen,
+           "sum_keep_sq": [int(np.sum(r.keep.astype(np.int64) ** 2)) for r in run.rounds],
+           "us_per_step": step_ms * 1e3, "packed_tokens_per_s": sum(run.sum_keep) / (step_ms * 1e-3),
+           "select_pack": [], "attention": []}
+    for i, r in enumerate(run.rounds):
+        n_items, q_tile = run.plan_items(i)
+        sp_b = select_pack_bytes(w, r.keep, r.n_in, n_items, packed_in=i > 0)
+        sp_in, sp_al = per[2 * i], alone[2 * i]
+        rec["select_pack"].append({
+            "algorithmic_bytes": sp_b, "us_in_step_events": sp_in * 1e3, "us_alone": sp_al * 1e3,
+            "GBs_alone": sp_b / (sp_al * 1e-3) / 1e9, "hbm_frac_alone": sp_b / (sp_al * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "GBs_in_step": sp_b / (sp_in * 1e-3) / 1e9,
+            "tokens_per_s_alone": r.total_keep / (sp_al * 1e-3), "plan_items": n_items, "q_tile": q_tile})
+        fl, ab = attn_flops(w, r.keep), attn_bytes(w, r.keep)
+        at_in, at_al = per[2 * i + 1], alone[2 * i + 1]
+        rec["attention"].append({
+            "flops": fl, "algorithmic_bytes": ab, "us_in_step_events": at_in * 1e3, "us_alone": at_al * 1e3,
+            "tflops_in_step": fl / (at_in * 1e-3) / 1e12, "mfma_frac_in_step": fl / (at_in * 1e-3) / 1e12 / peak,
+            "tflops_alone": fl / (at_al * 1e-3) / 1e12, "mfma_frac_alone": fl / (at_al * 1e-3) / 1e12 / peak,
+            "GBs_in_step": ab / (at_in * 1e-3) / 1e9, "GBs_alone": ab / (at_al * 1e-3) / 1e9,
+            "attainable_tflops": min(peak, fl / ab * HBM_PEAK_GBS / 1e3)})
+    print(f"[bench] {w.name}: {step_ms * 1e3:.1f} us/step; alone: "
+          + ", ".join(f"{k}{i} {a * 1e3:.1f} us" for (k, i, _), a in zip(ls, alone)), file=sys.stderr, flush=True)
+    return rec
+
+
+def attn_errors(got_bits: np.ndarray, want: np.ndarray, dtype: str):
+    got = (W.bf16_bits_to_f32(got_bits) if dtype == "bf16" else got_bits).astype(np.float64)
+    d = np.abs(got - want)
+    return float(d.max()) if d.size else 0.0, float(d.mean()) if d.size else 0.0, bool(np.all(np.isfinite(got)))
+
+
+def oracle_leg(run_rounds, gpu_out, w: W.Workload, passes: int, threads: int):
+    """The oracle as it stands, on this host's cores, over the whole step
+    (every round): select/pack and attention timed separately (median of
+    `passes`), and its outputs compared with the GPU outputs of the timed
+    step: idx, cu_seqlens and the packed rows bit for bit, attention within
+    the stated tolerance over every element."""
     import oracle
-    threads = len(os.sched_getaffinity(0))
-    times = []
-    for _ in range(repeats):
-        t0 = time.perf_counter()
-        idx, cu, packed, st = oracle.select_pack(r.scores, r.keep, r.tokens)
-        oracle.varlen_attn(r.q, r.k, r.v, cu, w.dtype, threads=threads)
-        times.append(time.perf_counter() - t0)
-        assert st == 0
-    t = statistics.median(times)
-    times_1 = []
-    for _ in range(repeats_1):
-        t0 = time.perf_counter()
-        idx, cu, packed, st = oracle.select_pack(r.scores, r.keep, r.tokens)
-        oracle.varlen_attn(r.q, r.k, r.v, cu, w.dtype, threads=1)
-        times_1.append(time.perf_counter() - t0)
-    t1 = statistics.median(times_1)
-    return {"value": r.total_keep / t, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "value_1_thread": r.total_keep / t1,
-            "sample": f"full {w.name} batch (B={w.B}, sum keep={r.total_keep}), select+pack+attention, "
-                      f"median of {repeats} passes on {threads} threads ({t:.3f} s each) and of "
-                      f"{repeats_1} on one thread ({t1:.3f} s each), "
-                      f"{repeats * t + repeats_1 * t1:.1f} s of CPU work in all, CPU: {cpu_model()}"}
+    t_sp, t_at = [], []
+    outs = None
+    for p in range(passes):
+        res = []
+        tok, cu_prev = None, None
+        a_sp = a_at = 0.0
+        for i, r in enumerate(run_rounds):
+            t0 = time.perf_counter()
+            if i == 0:
+                idx, cu, packed, st = oracle.select_pack(r.scores, r.keep, r.tokens)
+            else:
+                idx, cu, packed, st = oracle.select_pack(r.scores, r.keep, tok, cu_in=cu_prev, N=w.N)
+            t1 = time.perf_counter()
+            o = oracle.varlen_attn(r.q, r.k, r.v, cu, w.dtype, threads=threads)
+            t2 = time.perf_counter()
+            assert st == 0
+            a_sp += t1 - t0
+            a_at += t2 - t1
+            res.append((idx, cu, packed, o))
+            tok, cu_prev = packed, cu
+        t_sp.append(a_sp)
+        t_at.append(a_at)
+        outs = res
+    parity = {"ok": True, "rounds": []}
+    for i, ((idx, cu, packed, o), g) in enumerate(zip(outs, gpu_out)):
+        mx, mean, finite = attn_errors(g["out"], o, w.dtype)
+        tol = (mx <= BF16_MAX_ABS and mean <= BF16_MEAN_ABS) if w.dtype == "bf16" else mx <= F32_MAX_ABS
+        rp = {"idx_bit_exact": bool(np.array_equal(g["idx"], idx)), "cu_bit_exact": bool(np.array_equal(g["cu"], cu)),
+              "packed_bit_exact": bool(np.array_equal(g["packed"], packed)),
+              "attn_max_abs": mx, "attn_mean_abs": mean, "attn_elements": int(o.size),
+              "attn_within_tolerance": bool(tol and finite)}
+        rp["ok"] = rp["idx_bit_exact"] and rp["cu_bit_exact"] and rp["packed_bit_exact"] and rp["attn_within_tolerance"]
+        parity["ok"] = parity["ok"] and rp["ok"]
+        parity["rounds"].append(rp)
+    parity["tolerance"] = ({"attn_max_abs": BF16_MAX_ABS, "attn_mean_abs": BF16_MEAN_ABS} if w.dtype == "bf16"
+                           else {"attn_max_abs": F32_MAX_ABS})
+    sp, at = statistics.median(t_sp), statistics.median(t_at)
+    sk = sum(r.total_keep for r in run_rounds)
+    fl = sum(attn_flops(w, r.keep) for r in run_rounds)
+    cpu = {"value": sk / (sp + at), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+           "select_pack_s": sp, "select_pack_tokens_per_s": sk / sp, "attn_s": at, "attn_gflops": fl / at / 1e9,
+           "passes": passes}
+    return cpu, parity
 
 
 def main() -> int:
@@ -341,32 +630,31 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--repeats", type=int, default=5)
     ap.add_argument("--workload", default=W.HEADLINE, choices=sorted(W.WORKLOADS))
-    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip the oracle leg (CPU baseline and parity of the timed outputs)")
+    ap.add_argument("--no-configs", action="store_true", help="time the headline workload only")
     ap.add_argument("--cold-sets", type=int, default=3,
                     help="also time the step rotating through this many buffer sets (cold MALL); <= 1: off")
     ap.add_argument("--no-peaks", action="store_true", help="skip measuring the copy and MFMA peaks")
-    ap.add_argument("--no-actor", action="store_true", help="skip timing the actor decode (outside the step)")
-    ap.add_argument("--no-pl", action="store_true", help="skip timing the Plackett-Luce draw (outside the step)")
-    ap.add_argument("--no-lc1", action="store_true", help="skip timing the LC1 readout input (outside the step)")
-    ap.add_argument("--no-flops", action="store_true", help="skip timing the trajectory FLOP count (outside the step)")
-    ap.add_argument("--no-residual", action="store_true",
-                    help="skip timing select/pack after the attention residual (outside the step)")
+    ap.add_argument("--no-adjacent", action="store_true",
+                    help="skip the adjacent entry points (residual, actor, LC1, FLOPs, Plackett-Luce)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="before timing, run one plain device copy of MIB MiB (a reference dispatch "
                          "for scaling hardware byte counters)")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM bytes per launch (from rocprofv3 counters), if present")
+    ap.add_argument("--phase-log", metavar="FILE", help="write the launch counts of every timed phase here")
     ap.add_argument("--summarize-pmc", metavar="DIR",
                     help="print matrix-unit / LDS counter summaries from rocprofv3 --pmc runs under DIR/*/")
     ap.add_argument("--summarize-profile", metavar="DIR",
                     help="no benchmark: summarise rocprofv3 output under DIR/{stats,fetch,write} "
-                         "for --workload and update --traffic-json")
+                         "for --workload and update --traffic-json (kernel trace split by --phase-log)")
     args = ap.parse_args()
     if args.summarize_pmc:
         return summarize_pmc(args.summarize_pmc, args.workload)
     if args.summarize_profile:
         return summarize_profile(args.summarize_profile, args.workload, args.traffic_json,
-                                 args.calibrate_copy or 256)
+                                 args.calibrate_copy or 256, args.phase_log)
 
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -379,87 +667,14 @@ def main() -> int:
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dora.load_library()
     torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    phases = PhaseLog()
     w = W.WORKLOADS[args.workload]
-    r = W.generate(w)[0]
+    head = ConfigRun(w, torch, dora, stream, phases)
+    r = head.rounds[0]
     print(f"[bench] {w.name}: B={w.B} N={w.N} H={w.H} C={w.C} {w.dtype} sum_keep={r.total_keep}",
           file=sys.stderr, flush=True)
-
-    def dev(a):
-        if a.dtype == np.uint16:
-            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
-        return torch.from_numpy(np.ascontiguousarray(a)).cuda()
-
-    sk = r.total_keep
-    max_seqlen = int(r.keep.max())
-    stream = torch.cuda.current_stream()
-
-    def buffer_set(src=None):
-        """Inputs (copied from `src`, or uploaded) and outputs of one step."""
-        b = {}
-        if src is None:
-            b["scores"], b["keep"], b["tokens"] = dev(r.scores), dev(r.keep), dev(r.tokens)
-            b["q"], b["k"], b["v"] = dev(r.q), dev(r.k), dev(r.v)
-        else:
-            for name in ("scores", "keep", "tokens", "q", "k", "v"):
-                b[name] = src[name].clone()
-        b["idx"] = torch.empty(sk, dtype=torch.int32, device="cuda")
-        b["cu"] = torch.empty(w.B + 1, dtype=torch.int32, device="cuda")
-        b["packed"] = torch.empty((sk, w.C), dtype=b["tokens"].dtype, device="cuda")
-        b["out"] = torch.empty_like(b["q"])
-        b["ws"] = dora.new_workspace(w.B, w.H, max_seqlen)
-        b["st"] = dora.new_status()
-        return b
-
-    def step(b, ev=None):
-        if ev is not None:
-            ev[0].record(stream)
-        dora.dora_select_pack_plan(b["scores"], b["keep"], b["tokens"], w.H, max_seqlen, sk, b["ws"],
-                                   idx_out=b["idx"], cu_out=b["cu"], packed_out=b["packed"], cap_rows=sk,
-                                   dev_status=b["st"], stream=stream)
-        if ev is not None:
-            ev[1].record(stream)
-        dora.dora_varlen_attn_execute(b["q"], b["k"], b["v"], b["cu"], max_seqlen, b["ws"], out=b["out"],
-                                      dev_status=b["st"], stream=stream)
-        if ev is not None:
-            ev[2].record(stream)
-
-    def timed(sets, tag):
-        """Median over repeats of (step time, select/pack+plan time, attention
-        time) in ms; step i uses sets[i % len(sets)].  Each repeat times K steps
-        twice: once bare (events only at the two ends) and once with events
-        around every kernel (per-kernel durations; an event between two kernels
-        adds a few microseconds of dispatch latency to the interval, so these
-        are upper bounds)."""
-        for i in range(args.warmup):
-            step(sets[i % len(sets)])
-        torch.cuda.synchronize()
-        reps = []
-        for rep in range(args.repeats):
-            t_start = torch.cuda.Event(enable_timing=True)
-            t_end = torch.cuda.Event(enable_timing=True)
-            torch.cuda.synchronize()
-            t_start.record(stream)
-            for i in range(args.steps):
-                step(sets[i % len(sets)])
-            t_end.record(stream)
-            torch.cuda.synchronize()
-            total_ms = t_start.elapsed_time(t_end)
-            evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
-            torch.cuda.synchronize()
-            for i in range(args.steps):
-                step(sets[i % len(sets)], evs[i])
-            torch.cuda.synchronize()
-            sel = np.mean([e[0].elapsed_time(e[1]) for e in evs])
-            attn = np.mean([e[1].elapsed_time(e[2]) for e in evs])
-            reps.append((total_ms / args.steps, sel, attn))
-            print(f"[bench] {tag} repeat {rep}: {total_ms / args.steps * 1e3:.1f} us/step "
-                  f"(per kernel with events: select_pack+plan {sel * 1e3:.1f}, "
-                  f"attention {attn * 1e3:.1f})", file=sys.stderr, flush=True)
-        for b in sets:
-            assert int(b["st"].item()) == 0, f"device status {int(b['st'].item())}"
-        return sorted(reps, key=lambda x: x[0])[len(reps) // 2]
-
-    main_set = buffer_set()
+    sk = sum(head.sum_keep)
     if args.calibrate_copy > 0:
         src = torch.ones(args.calibrate_copy * 2 ** 20, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -469,229 +684,94 @@ def main() -> int:
         del src, dst
 
     # Warm: the same buffers every step, as in deployment, where the producing
-    # kernel has just written the inputs.
-    ms_step, ms_sel, ms_attn = timed([main_set], "warm")
+    # kernel has just written the inputs; then each kernel alone, back to back
+    # (attention alone: Q/K/V/O resident in the MALL).
+    rec = bench_config(head, args)
+    head_out = head.host_outputs()
+    ms_step = rec["us_per_step"] * 1e-3
+    sp0, at0 = rec["select_pack"][0], rec["attention"][0]
+
     # Cold: rotate through enough buffer sets that one rotation exceeds twice
     # the 256 MB MALL, so every step's inputs come from HBM.
     cold = None
-    if args.cold_sets > 1:
-        set_bytes = sum(t.numel() * t.element_size() for t in main_set.values())
-        cold_sets = [main_set] + [buffer_set(main_set) for _ in range(args.cold_sets - 1)]
-        c_step, c_sel, c_attn = timed(cold_sets, "cold")
+    if args.cold_sets > 1 and head.R == 1:
+        set_bytes = sum(t.numel() * t.element_size() for t in head.sets[0][0].values())
+        cold_sets = [head.sets[0]] + [head._buffers(head.sets[0]) for _ in range(args.cold_sets - 1)]
+        c_step, c_per = time_steps(head, cold_sets, args, "cold")
+        c_sel, c_attn = c_per[0], c_per[1]
         cold = {"sets": args.cold_sets, "bytes_per_set": set_bytes, "ms_per_step": c_step,
                 "value": sk / (c_step * 1e-3),
-                "us": {"select_pack_plan": c_sel * 1e3, "attention": c_attn * 1e3, "step": c_step * 1e3}}
-
-    # Beside the path: deletion after the attention residual (the kept rows of
-    # tokens + attention output) on the same batch, timed on its own, warm and,
-    # with a second attention-output buffer per set, cold.
-    residual = None
-    if not args.no_residual:
-        a_host = W.generate(w, parts=("keep", "attn_out"))[0].attn_out
-        a_main = dev(a_host)
-
-        def res_launch(b, a):
-            dora.dora_select_pack_residual(b["scores"], b["keep"], b["tokens"], a, idx_out=b["idx"],
-                                           cu_out=b["cu"], packed_out=b["packed"], cap_rows=sk,
-                                           dev_status=b["st"], stream=stream)
-
-        def res_timed(pairs, tag):
-            for i in range(args.warmup):
-                res_launch(*pairs[i % len(pairs)])
-            reps = []
-            for rep in range(args.repeats):
-                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                torch.cuda.synchronize()
-                e0.record(stream)
-                for i in range(args.steps):
-                    res_launch(*pairs[i % len(pairs)])
-                e1.record(stream)
-                torch.cuda.synchronize()
-                reps.append(e0.elapsed_time(e1) / args.steps)
-                print(f"[bench] residual {tag} repeat {rep}: {reps[-1] * 1e3:.1f} us/launch",
-                      file=sys.stderr, flush=True)
-            for b, _ in pairs:
-                assert int(b["st"].item()) == 0, f"device status {int(b['st'].item())}"
-            return sorted(reps)[len(reps) // 2]
-
-        rb = residual_bytes(w, r.keep, r.n_in)
-        ms_res = res_timed([(main_set, a_main)], "warm")
-        residual = {"entry": "dora_select_pack_residual", "kernel": "select_pack_residual_kernel",
-                    "bound": "hbm", "us": ms_res * 1e3, "achieved": rb / (ms_res * 1e-3) / 1e9,
-                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "algorithmic_bytes": rb,
-                    "tokens_per_s": sk / (ms_res * 1e-3), "regime": "warm"}
-        residual["frac"] = residual["achieved"] / HBM_PEAK_GBS
-        if args.cold_sets > 1:
-            pairs = [(main_set, a_main)] + [(b, a_main.clone()) for b in cold_sets[1:]]
-            ms_c = res_timed(pairs, "cold")
-            residual["cold"] = {"us": ms_c * 1e3, "achieved": rb / (ms_c * 1e-3) / 1e9,
-                                "frac": rb / (ms_c * 1e-3) / 1e9 / HBM_PEAK_GBS}
-            del pairs
-        del a_main
-    if args.cold_sets > 1:
-        del cold_sets
-
-    def time_calls(fn):
-        """Median over repeats of the mean time of `steps` back-to-back calls
-        of fn (after `warmup` calls), HIP events at the two ends, in ms."""
-        for _ in range(args.warmup):
-            fn()
-        reps = []
-        for _ in range(args.repeats):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            torch.cuda.synchronize()
-            e0.record(stream)
-            for _ in range(args.steps):
-                fn()
-            e1.record(stream)
-            torch.cuda.synchronize()
-            reps.append(e0.elapsed_time(e1) / args.steps)
-        return sorted(reps)[len(reps) // 2]
-
-    # Beside the path: the deterministic actor's decode that produces its
-    # inputs (gate + compaction, then budget argmax, keep counts and
-    # keep-scores), timed as a pair of launches.
-    actor = None
-    if not args.no_actor:
-        M = W.budget_outputs(w)
-        p_h, logits_h, removal_h = W.actor_outputs(w)
-        p_d, logits_d, removal_d = dev(p_h), dev(logits_h), dev(removal_h)
-        on_rank = torch.empty(w.B, dtype=torch.int32, device="cuda")
-        on_list = torch.empty_like(on_rank)
-        n_on = torch.empty(1, dtype=torch.int32, device="cuda")
-        keep_d = torch.empty_like(on_rank)
-        ks_d = torch.empty_like(removal_d)
-        st_a = dora.new_status()
-
-        def actor_pair():
-            dora.dora_actor_gate(p_d, M, w.N, on_rank=on_rank, on_list=on_list, n_on=n_on, dev_status=st_a,
-                                 stream=stream)
-            dora.dora_actor_decode(logits_d, on_rank, w.N, removal_scores=removal_d, keep_out=keep_d,
-                                   scores_out=ks_d, dev_status=st_a, stream=stream)
-
-        ms_actor = time_calls(actor_pair)
-        assert int(st_a.item()) == 0, f"device status {int(st_a.item())}"
-        actor = {"entries": ["dora_actor_gate", "dora_actor_decode"], "bound": "latency",
-                 "us_per_pair": ms_actor * 1e3, "gate_on": int(n_on.item()), "M": M,
-                 "note": "two small launches back to back; the cost is launch and dependency latency"}
-        print(f"[bench] actor decode: {ms_actor * 1e3:.1f} us per gate+decode pair, "
-              f"{actor['gate_on']} of {w.B} gates open", file=sys.stderr, flush=True)
-
-    # Beside the path: the LC1 readout input (LayerNorm + segmented mean over
-    # the packed rows of the same batch), an HBM-bound segmented reduction.
-    lc1 = None
-    if not args.no_lc1:
-        x_h, gamma_h, beta_h = W.readout_rows(w, r.keep)
-        cu_h = np.concatenate([[0], np.cumsum(r.keep)]).astype(np.int32)
-        x_d, cu_d, gamma_d, beta_d = dev(x_h), dev(cu_h), dev(gamma_h), dev(beta_h)
-        out_d = torch.empty((w.B, 2 * w.C), dtype=torch.float32, device="cuda")
-        st_l = dora.new_status()
-        ws_l = dora.new_lc1_workspace(w.B, w.C)
-
-        def lc1_call():
-            dora.dora_lc1_readout(x_d, cu_d, gamma_d, beta_d, 1e-6, out=out_d, workspace=ws_l, dev_status=st_l,
-                                  stream=stream)
-
-        ms_lc1 = time_calls(lc1_call)
-        assert int(st_l.item()) == 0, f"device status {int(st_l.item())}"
-        lb = lc1_bytes(w, r.keep)
-        lc1 = {"entry": "dora_lc1_readout", "kernel": "lc1_readout_kernel (+ lc1_combine_kernel when split)",
-               "bound": "hbm", "us": ms_lc1 * 1e3,
-               "achieved": lb / (ms_lc1 * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-               "frac": lb / (ms_lc1 * 1e-3) / 1e9 / HBM_PEAK_GBS, "algorithmic_bytes": lb, "regime": "warm"}
-        print(f"[bench] lc1 readout: {ms_lc1 * 1e3:.1f} us per launch ({lc1['achieved']:.0f} GB/s)",
-              file=sys.stderr, flush=True)
-        del x_d
-
-    # Beside the path: FLOP accounting of the batch's realised trajectories
-    # over a 12-block backbone (pruning at block 0 with this batch's keep
-    # counts, then none): one small latency-bound launch.
-    traj = None
-    if not args.no_flops:
-        L_blocks = 12
-        T = np.vstack([np.full((1, w.B), w.N, np.int32), np.tile(r.keep.astype(np.int32), (L_blocks, 1))])
-        T_d = dev(np.ascontiguousarray(T))
-        f_d = torch.empty(w.B, dtype=torch.int64, device="cuda")
-        tot_d = torch.empty(1, dtype=torch.int64, device="cuda")
-        st_f = dora.new_status()
-
-        def flops_call():
-            dora.dora_trajectory_flops(T_d, w.C, w.N - 1, 16, flops_out=f_d, total_out=tot_d, dev_status=st_f,
-                                       stream=stream)
-
-        ms_fl = time_calls(flops_call)
-        assert int(st_f.item()) == 0, f"device status {int(st_f.item())}"
-        traj = {"entry": "dora_trajectory_flops", "kernel": "trajectory_flops_kernel", "bound": "latency",
-                 "us": ms_fl * 1e3, "images": w.B, "blocks": L_blocks,
-                 "gflops_per_image": int(tot_d.item()) / w.B / 1e9}
-        print(f"[bench] trajectory flops: {ms_fl * 1e3:.1f} us per launch", file=sys.stderr, flush=True)
-
-    # Beside the path: the training-time draw (Gumbel-top-k Plackett-Luce
-    # deletion of n - keep tokens per image, with its ordered log-probability).
-    pl = None
-    if not args.no_pl:
-        k_h = (r.n_in - r.keep).astype(np.int32)
-        g_h = W.gumbel_noise(w)
-        s_d, g_d, k_d = dev(r.scores), dev(g_h), dev(k_h)
-        order = torch.empty(int(k_h.sum()) + 1, dtype=torch.int32, device="cuda")
-        cu_o = torch.empty(w.B + 1, dtype=torch.int32, device="cuda")
-        lp_d = torch.empty(w.B, dtype=torch.float32, device="cuda")
-        st_p = dora.new_status()
-
-        def pl_call():
-            dora.dora_pl_sample(s_d, g_d, k_d, order_out=order, cu_order_out=cu_o, logprob_out=lp_d,
-                                dev_status=st_p, stream=stream)
-
-        ms_pl = time_calls(pl_call)
-        assert int(st_p.item()) == 0, f"device status {int(st_p.item())}"
-        pl = {"entry": "dora_pl_sample", "kernel": "pl_kernel", "bound": "latency", "us": ms_pl * 1e3,
-              "draws": int(k_h.sum()), "images": w.B,
-              "note": "one workgroup per image: LDS bitonic sort of the visual keys and a block scan"}
-        print(f"[bench] pl sample: {ms_pl * 1e3:.1f} us per launch ({int(k_h.sum())} draws)",
-              file=sys.stderr, flush=True)
-
-    flops = attn_flops(w, r.keep)
-    sp_bytes = select_pack_bytes(w, r.keep, r.n_in)
-    a_bytes = attn_bytes(w, r.keep)
-    attn_tflops = flops / (ms_attn * 1e-3) / 1e12
-    sp_gbs = sp_bytes / (ms_sel * 1e-3) / 1e9
-    peak = MFMA_PEAK_TFLOPS[w.dtype]
-
-    traffic = load_traffic(args.traffic_json, w.name)
-
-    # The attention roofline is the lower of the two ceilings at its
-    # arithmetic intensity (flops per algorithmic byte): below the ridge point
-    # (peak flops / peak bandwidth) the kernel is bound by HBM.
-    intensity = flops / a_bytes
-    attn_gbs = a_bytes / (ms_attn * 1e-3) / 1e9
-    kname = "attn_fwd_bf16_kernel" if w.dtype == "bf16" else "attn_fwd_f32_kernel"
-    common = {"kernel": kname, "traffic": traffic.get("attn"), "algorithmic_bytes": a_bytes, "flops": flops,
-              "intensity_flop_per_byte": intensity, "ridge_flop_per_byte": peak * 1e3 / HBM_PEAK_GBS,
-              "tflops": attn_tflops, "mfma_peak_tflops": peak, "mfma_frac": attn_tflops / peak}
-    if intensity < peak * 1e3 / HBM_PEAK_GBS:
-        attn_roofline = {"bound": "hbm", "achieved": attn_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                         "frac": attn_gbs / HBM_PEAK_GBS, **common}
+                "us": {"select_pack_plan": c_sel * 1e3, "attention": c_attn * 1e3, "step": c_step * 1e3},
+                "attn_GBs": at0["algorithmic_bytes"] / (c_attn * 1e-3) / 1e9,
+                "attn_tflops": at0["flops"] / (c_attn * 1e-3) / 1e12,
+                "select_pack_GBs": sp0["algorithmic_bytes"] / (c_sel * 1e-3) / 1e9}
+        cold["attn_mfma_frac"] = cold["attn_tflops"] / MFMA_PEAK_TFLOPS[w.dtype]
+        cold["select_pack_hbm_frac"] = cold["select_pack_GBs"] / HBM_PEAK_GBS
+        # The cold sets stay for the residual leg below.
     else:
-        attn_roofline = {"bound": "mfma", "achieved": attn_tflops, "peak": peak, "unit": "TFLOP/s",
-                         "frac": attn_tflops / peak, **common}
+        cold_sets = None
+
+    extras = {} if args.no_adjacent else adjacent_legs(head, cold_sets, args, torch, dora, stream, phases)
+    del cold_sets
+    main_bufs = head.sets
+    head.sets = None
+    del main_bufs
+    torch.cuda.empty_cache()
+
+    # The other workloads, each with a record of its own.
+    configs, runs = {}, {}
+    if not args.no_configs:
+        for name in CONFIG_ORDER:
+            if name == w.name:
+                continue
+            cr = ConfigRun(W.WORKLOADS[name], torch, dora, stream, phases)
+            configs[name] = bench_config(cr, args)
+            runs[name] = (cr.rounds, cr.host_outputs())
+            cr.sets = None
+            del cr
+            torch.cuda.empty_cache()
 
     peaks = {} if args.no_peaks else measure_peaks(torch, stream)
-    attn_roofline["attainable_tflops"] = min(peak, intensity * HBM_PEAK_GBS / 1e3)
+    traffic = load_traffic(args.traffic_json, w.name)
+    peak = MFMA_PEAK_TFLOPS[w.dtype]
+
+    # The dominant kernel (attention) on the matrix-unit roofline, at its
+    # in-step duration; the HBM view and the MALL-resident timing beside it.
+    fl, ab = at0["flops"], at0["algorithmic_bytes"]
+    at_in = at0["us_in_step_events"] * 1e-6
+    intensity = fl / ab
+    roofline = {"bound": "mfma", "achieved": fl / at_in / 1e12, "peak": peak, "unit": "TFLOP/s",
+                "frac": fl / at_in / 1e12 / peak,
+                "kernel": "attn_fwd_bf16_kernel" if w.dtype == "bf16" else "attn_fwd_f32_kernel",
+                "traffic": traffic.get("attn"), "flops": fl, "algorithmic_bytes": ab,
+                "duration_us": at0["us_in_step_events"],
+                "duration_source": "HIP events around the kernel inside the step (an upper bound: includes "
+                                   "the dispatch gap after the preceding event)",
+                "intensity_flop_per_byte": intensity, "ridge_flop_per_byte": peak * 1e3 / HBM_PEAK_GBS,
+                "attainable_tflops": at0["attainable_tflops"],
+                "frac_of_attainable": fl / at_in / 1e12 / at0["attainable_tflops"],
+                "hbm_view": {"achieved": ab / at_in / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                             "frac": ab / at_in / 1e9 / HBM_PEAK_GBS},
+                "resident": {"regime": "attention alone, back to back on one Q/K/V/O set resident in the MALL",
+                             "us": at0["us_alone"], "tflops": at0["tflops_alone"], "mfma_frac": at0["mfma_frac_alone"],
+                             "GBs": at0["GBs_alone"]}}
     if "copy_GBs" in peaks:
-        attn_roofline["frac_of_measured_copy"] = attn_gbs / peaks["copy_GBs"]
+        roofline["hbm_view"]["frac_of_measured_copy"] = roofline["hbm_view"]["achieved"] / peaks["copy_GBs"]
     if "mfma_bf16_TFLOPs" in peaks and w.dtype == "bf16":
-        attn_roofline["frac_of_measured_mfma"] = attn_tflops / peaks["mfma_bf16_TFLOPs"]
-    if cold is not None:
-        c_attn, c_sel = cold["us"]["attention"] * 1e-6, cold["us"]["select_pack_plan"] * 1e-6
-        cold["attn_GBs"] = a_bytes / c_attn / 1e9
-        cold["attn_hbm_frac"] = cold["attn_GBs"] / HBM_PEAK_GBS
-        cold["attn_tflops"] = flops / c_attn / 1e12
-        cold["select_pack_GBs"] = sp_bytes / c_sel / 1e9
-        cold["select_pack_hbm_frac"] = cold["select_pack_GBs"] / HBM_PEAK_GBS
+        roofline["frac_of_measured_mfma"] = roofline["achieved"] / peaks["mfma_bf16_TFLOPs"]
+    sp_b, sp_al = sp0["algorithmic_bytes"], sp0["us_alone"] * 1e-6
+    roofline_sp = {"bound": "hbm", "kernel": "select_pack_kernel", "achieved": sp_b / sp_al / 1e9,
+                   "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": sp_b / sp_al / 1e9 / HBM_PEAK_GBS,
+                   "traffic": traffic.get("select_pack"), "algorithmic_bytes": sp_b, "duration_us": sp0["us_alone"],
+                   "duration_source": "dora_select_pack_plan alone, back to back on the same buffers",
+                   "in_step_events": {"us": sp0["us_in_step_events"], "GBs": sp0["GBs_in_step"],
+                                      "frac": sp0["GBs_in_step"] / HBM_PEAK_GBS}}
+    if "copy_GBs" in peaks:
+        roofline_sp["frac_of_measured_copy"] = roofline_sp["achieved"] / peaks["copy_GBs"]
 
     result = {
         "metric": METRIC,
-        "value": sk / (ms_step * 1e-3),
+        "value": sk / ms_step * 1e3,
         "unit": "packed tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -703,43 +783,192 @@ def main() -> int:
         "dtype": w.dtype,
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "N": w.N, "H": w.H, "head_dim": W.HEAD_DIM, "C": w.C,
-                   "sum_keep": sk, "sum_keep_sq": int(np.sum(r.keep.astype(np.int64) ** 2)),
-                   "max_seqlen": max_seqlen},
-        "roofline": attn_roofline,
-        "roofline_select_pack": {"bound": "hbm", "kernel": "select_pack_kernel", "achieved": sp_gbs,
-                                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": sp_gbs / HBM_PEAK_GBS,
-                                 "traffic": traffic.get("select_pack"), "algorithmic_bytes": sp_bytes},
-        "select_pack_tokens_per_s": sk / (ms_sel * 1e-3),
-        "attn_tflops": attn_tflops,
-        "us": {"select_pack_plan": ms_sel * 1e3, "attention": ms_attn * 1e3, "step": ms_step * 1e3},
+                   "rounds": head.R, "sum_keep": rec["sum_keep"][0] if head.R == 1 else rec["sum_keep"],
+                   "sum_keep_sq": rec["sum_keep_sq"][0] if head.R == 1 else rec["sum_keep_sq"],
+                   "max_seqlen": rec["max_seqlen"][0] if head.R == 1 else rec["max_seqlen"]},
+        "roofline": roofline,
+        "roofline_select_pack": roofline_sp,
+        "select_pack_tokens_per_s": sp0["tokens_per_s_alone"],
+        "attn_tflops": roofline["achieved"],
+        "us": {"select_pack_plan_in_step": sp0["us_in_step_events"], "attention_in_step": at0["us_in_step_events"],
+               "select_pack_plan_alone": sp0["us_alone"], "attention_alone": at0["us_alone"],
+               "step": ms_step * 1e3},
         "repeats": args.repeats,
         "regime": "warm: the same input buffers every step",
         "cold": cold,
         "measured_peaks": peaks,
+        "parity": None,
     }
-    if "copy_GBs" in peaks:
-        result["roofline_select_pack"]["frac_of_measured_copy"] = sp_gbs / peaks["copy_GBs"]
-    if residual is not None:
-        residual["traffic"] = traffic.get("residual")
-        if "copy_GBs" in peaks:
-            residual["frac_of_measured_copy"] = residual["achieved"] / peaks["copy_GBs"]
-        result["residual_select_pack"] = residual
-    if lc1 is not None:
-        lc1["traffic"] = traffic.get("lc1")
-        if "copy_GBs" in peaks:
-            lc1["frac_of_measured_copy"] = lc1["achieved"] / peaks["copy_GBs"]
-        result["lc1_readout"] = lc1
-    if actor is not None:
-        result["actor_decode"] = actor
-    if pl is not None:
-        result["pl_sample"] = pl
-    if traj is not None:
-        result["trajectory_flops"] = traj
+    result.update(extras)
+    for k in ("residual_select_pack", "lc1_readout"):
+        if k in result:
+            result[k]["traffic"] = traffic.get("residual" if k.startswith("residual") else "lc1")
+            if "copy_GBs" in peaks:
+                result[k]["frac_of_measured_copy"] = result[k]["achieved"] / peaks["copy_GBs"]
+
     if not args.no_cpu_baseline:
-        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
-        result["cpu_baseline"] = run_cpu_baseline(w, r)
+        threads = len(os.sched_getaffinity(0))
+        print("[bench] oracle leg: CPU baseline and parity of the timed outputs", file=sys.stderr, flush=True)
+        cpu, parity = oracle_leg(head.rounds, head_out, w, 5, threads)
+        # one thread, for scale
+        import oracle
+        t1 = []
+        for _ in range(2):
+            t0 = time.perf_counter()
+            idx, cu, _, _ = oracle.select_pack(r.scores, r.keep, r.tokens)
+            oracle.varlen_attn(r.q, r.k, r.v, cu, w.dtype, threads=1)
+            t1.append(time.perf_counter() - t0)
+        cpu["value_1_thread"] = sk / statistics.median(t1)
+        cpu["sample"] = (f"full {w.name} batch (B={w.B}, sum keep={sk}), select+pack+attention, median of 5 passes "
+                         f"on {threads} threads ({cpu['select_pack_s'] + cpu['attn_s']:.3f} s each) and of 2 on one "
+                         f"thread ({statistics.median(t1):.3f} s each); CPU: {cpu_model()}")
+        result["cpu_baseline"] = cpu
+        result["parity"] = parity
+        for name, (rounds, outs) in runs.items():
+            c, p = oracle_leg(rounds, outs, W.WORKLOADS[name], 3, threads)
+            configs[name]["cpu_baseline"] = c
+            configs[name]["parity"] = p
+        print(f"[bench] parity: {w.name} {'ok' if parity['ok'] else 'FAILED'}; "
+              + ", ".join(f"{n} {'ok' if c['parity']['ok'] else 'FAILED'}" for n, c in configs.items()),
+              file=sys.stderr, flush=True)
+    result["configs"] = configs
+    if args.phase_log:
+        phases.dump(args.phase_log)
     print(json.dumps(result), flush=True)
     return 0
+
+
+def adjacent_legs(head: ConfigRun, cold_sets, args, torch, dora, stream, phases) -> dict:
+    """The entry points beside the path, on the headline batch, each timed on
+    its own (events at the two ends of back-to-back calls)."""
+    w, r = head.w, head.rounds[0]
+    b0 = head.sets[0][0]
+    sk = r.total_keep
+    out = {}
+
+    # Deletion after the attention residual (the kept rows of tokens +
+    # attention output), warm and, with a second attention-output buffer per
+    # set, cold.
+    a_main = head.dev(W.generate(w, parts=("keep", "attn_out"))[0].attn_out)
+
+    def res_launch(b, a):
+        dora.dora_select_pack_residual(b["scores"], b["keep"], b["tokens"], a, idx_out=b["idx"], cu_out=b["cu"],
+                                       packed_out=b["packed"], cap_rows=sk, dev_status=b["st"], stream=stream)
+
+    rb = residual_bytes(w, r.keep, r.n_in)
+    ms_res = time_calls(torch, stream, lambda: res_launch(b0, a_main), args, phases, "residual:warm", ("residual",))
+    res = {"entry": "dora_select_pack_residual", "kernel": "select_pack_residual_kernel", "bound": "hbm",
+           "us": ms_res * 1e3, "achieved": rb / (ms_res * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+           "algorithmic_bytes": rb, "tokens_per_s": sk / (ms_res * 1e-3), "regime": "warm"}
+    res["frac"] = res["achieved"] / HBM_PEAK_GBS
+    if cold_sets is not None:
+        pairs = [(cold_sets[0][0], a_main)] + [(s[0], a_main.clone()) for s in cold_sets[1:]]
+        it = [0]
+
+        def rot():
+            b, a = pairs[it[0] % len(pairs)]
+            it[0] += 1
+            res_launch(b, a)
+
+        ms_c = time_calls(torch, stream, rot, args, phases, "residual:cold", ("residual",))
+        res["cold"] = {"us": ms_c * 1e3, "achieved": rb / (ms_c * 1e-3) / 1e9,
+                       "frac": rb / (ms_c * 1e-3) / 1e9 / HBM_PEAK_GBS}
+        del pairs
+    head.check_status(cold_sets)
+    out["residual_select_pack"] = res
+    print(f"[bench] residual select/pack: {ms_res * 1e3:.1f} us warm", file=sys.stderr, flush=True)
+    del a_main
+
+    # The deterministic actor's decode that produces the path's inputs (gate +
+    # compaction, then budget argmax, keep counts and keep-scores), timed as a
+    # pair of launches.
+    M = W.budget_outputs(w)
+    p_h, logits_h, removal_h = W.actor_outputs(w)
+    p_d, logits_d, removal_d = head.dev(p_h), head.dev(logits_h), head.dev(removal_h)
+    on_rank = torch.empty(w.B, dtype=torch.int32, device="cuda")
+    on_list = torch.empty_like(on_rank)
+    n_on = torch.empty(1, dtype=torch.int32, device="cuda")
+    keep_d = torch.empty_like(on_rank)
+    ks_d = torch.empty_like(removal_d)
+    st_a = dora.new_status()
+
+    def actor_pair():
+        dora.dora_actor_gate(p_d, M, w.N, on_rank=on_rank, on_list=on_list, n_on=n_on, dev_status=st_a,
+                             stream=stream)
+        dora.dora_actor_decode(logits_d, on_rank, w.N, removal_scores=removal_d, keep_out=keep_d,
+                               scores_out=ks_d, dev_status=st_a, stream=stream)
+
+    ms_actor = time_calls(torch, stream, actor_pair, args, phases, "actor", ("actor", "actor"))
+    assert int(st_a.item()) == 0, f"device status {int(st_a.item())}"
+    out["actor_decode"] = {"entries": ["dora_actor_gate", "dora_actor_decode"], "bound": "latency",
+                           "us_per_pair": ms_actor * 1e3, "gate_on": int(n_on.item()), "M": M,
+                           "note": "two small launches back to back; the cost is launch and dependency latency"}
+    print(f"[bench] actor decode: {ms_actor * 1e3:.1f} us per gate+decode pair", file=sys.stderr, flush=True)
+
+    # The LC1 readout input (LayerNorm + segmented mean over the packed rows of
+    # the same batch), an HBM-bound segmented reduction.
+    x_h, gamma_h, beta_h = W.readout_rows(w, r.keep)
+    cu_h = np.concatenate([[0], np.cumsum(r.keep)]).astype(np.int32)
+    x_d, cu_d, gamma_d, beta_d = head.dev(x_h), head.dev(cu_h), head.dev(gamma_h), head.dev(beta_h)
+    out_d = torch.empty((w.B, 2 * w.C), dtype=torch.float32, device="cuda")
+    st_l = dora.new_status()
+    ws_l = dora.new_lc1_workspace(w.B, w.C)
+
+    def lc1_call():
+        dora.dora_lc1_readout(x_d, cu_d, gamma_d, beta_d, 1e-6, out=out_d, workspace=ws_l, dev_status=st_l,
+                              stream=stream)
+
+    ms_lc1 = time_calls(torch, stream, lc1_call, args, phases, "lc1", ("lc1",))
+    assert int(st_l.item()) == 0, f"device status {int(st_l.item())}"
+    lb = lc1_bytes(w, r.keep)
+    out["lc1_readout"] = {"entry": "dora_lc1_readout", "kernel": "lc1_readout_kernel (+ lc1_combine_kernel when split)",
+                          "bound": "hbm", "us": ms_lc1 * 1e3, "achieved": lb / (ms_lc1 * 1e-3) / 1e9,
+                          "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": lb / (ms_lc1 * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                          "algorithmic_bytes": lb, "regime": "warm"}
+    print(f"[bench] lc1 readout: {ms_lc1 * 1e3:.1f} us per launch", file=sys.stderr, flush=True)
+    del x_d
+
+    # FLOP accounting of the batch's realised trajectories over a 12-block
+    # backbone (pruning at block 0 with this batch's keep counts, then none).
+    L_blocks = 12
+    T = np.vstack([np.full((1, w.B), w.N, np.int32), np.tile(r.keep.astype(np.int32), (L_blocks, 1))])
+    T_d = head.dev(np.ascontiguousarray(T))
+    f_d = torch.empty(w.B, dtype=torch.int64, device="cuda")
+    tot_d = torch.empty(1, dtype=torch.int64, device="cuda")
+    st_f = dora.new_status()
+
+    def flops_call():
+        dora.dora_trajectory_flops(T_d, w.C, w.N - 1, 16, flops_out=f_d, total_out=tot_d, dev_status=st_f,
+                                   stream=stream)
+
+    ms_fl = time_calls(torch, stream, flops_call, args, phases, "flops", ("flops",))
+    assert int(st_f.item()) == 0, f"device status {int(st_f.item())}"
+    out["trajectory_flops"] = {"entry": "dora_trajectory_flops", "kernel": "trajectory_flops_kernel",
+                               "bound": "latency", "us": ms_fl * 1e3, "images": w.B, "blocks": L_blocks,
+                               "gflops_per_image": int(tot_d.item()) / w.B / 1e9}
+
+    # The training-time draw (Gumbel-top-k Plackett-Luce deletion of n - keep
+    # tokens per image, with its ordered log-probability).
+    k_h = (r.n_in - r.keep).astype(np.int32)
+    g_h = W.gumbel_noise(w)
+    s_d, g_d, k_d = head.dev(r.scores), head.dev(g_h), head.dev(k_h)
+    order = torch.empty(int(k_h.sum()) + 1, dtype=torch.int32, device="cuda")
+    cu_o = torch.empty(w.B + 1, dtype=torch.int32, device="cuda")
+    lp_d = torch.empty(w.B, dtype=torch.float32, device="cuda")
+    st_p = dora.new_status()
+
+    def pl_call():
+        dora.dora_pl_sample(s_d, g_d, k_d, order_out=order, cu_order_out=cu_o, logprob_out=lp_d,
+                            dev_status=st_p, stream=stream)
+
+    ms_pl = time_calls(torch, stream, pl_call, args, phases, "pl", ("pl",))
+    assert int(st_p.item()) == 0, f"device status {int(st_p.item())}"
+    out["pl_sample"] = {"entry": "dora_pl_sample", "kernel": "pl_kernel", "bound": "latency", "us": ms_pl * 1e3,
+                        "draws": int(k_h.sum()), "images": w.B,
+                        "note": "one workgroup per image: LDS bitonic sort of the visual keys and a block scan"}
+    print(f"[bench] trajectory flops {ms_fl * 1e3:.1f} us, pl sample {ms_pl * 1e3:.1f} us",
+          file=sys.stderr, flush=True)
+    return out
 
 
 if __name__ == "__main__":
