@@ -56,7 +56,8 @@ typedef enum {
   DORA_ERR_UNSUPPORTED = -5, /* valid request outside what this library implements  */
   DORA_ERR_CAPACITY = -6,    /* an output capacity cannot be represented            */
   DORA_ERR_HIP = -7,         /* the HIP runtime reported an error at launch         */
-  DORA_ERR_WORKSPACE = -8    /* workspace NULL, misaligned or smaller than required */
+  DORA_ERR_WORKSPACE = -8,   /* workspace NULL, misaligned or smaller than required */
+  DORA_ERR_STATIC_LIMIT = -9 /* sizes need more than the library's static workspace */
 } dora_status;
 
 /* Bits OR-ed into *dev_status by the kernels. */
@@ -425,6 +426,37 @@ int dora_varlen_attn(const void* q, const void* k, const void* v, const int32_t*
                      int32_t B, int32_t H, int32_t D, int32_t max_seqlen, int64_t total,
                      float softmax_scale, dora_dtype dtype, void* out, void* workspace,
                      size_t workspace_bytes, int32_t* dev_status, void* stream);
+
+/*
+ * dora_varlen_attn_noalloc -- dora_varlen_attn for callers that cannot
+ * allocate device memory (code under HIP graph capture, serving loops or
+ * harnesses that forbid allocation).  The plan and work queue live in a
+ * library-owned static device array of DORA_NOALLOC_WORKSPACE_BYTES instead
+ * of a caller workspace; every GPU the library runs on holds its own copy
+ * until the process ends.  The call allocates nothing (no hipMalloc, no
+ * allocating library routine); the caller still passes inputs and outputs.
+ *
+ * Arguments, results and dev_status bits are those of dora_varlen_attn
+ * without workspace / workspace_bytes.  Outputs are bit-identical to
+ * dora_varlen_attn's (the same two kernels run; the plan kernel rewrites
+ * the whole header, counters included, on every call, so nothing of an
+ * earlier call's contents is used).
+ *
+ * Limit: dora_varlen_attn_workspace_size(B, H, max_seqlen) must not exceed
+ * DORA_NOALLOC_WORKSPACE_BYTES (4 MiB: about 524,000 (sequence, head,
+ * query chunk) items), else DORA_ERR_STATIC_LIMIT before anything is
+ * enqueued.
+ * Concurrency: every call on one GPU shares that GPU's array, so calls that
+ * overlap in time on one GPU (several streams or host threads) race and
+ * give undefined results; calls must be serialised, e.g. on one stream.
+ * The first call on each device looks up the array's device address
+ * (hipGetSymbolAddress) and keeps it; DORA_ERR_HIP if that fails.
+ */
+#define DORA_NOALLOC_WORKSPACE_BYTES (4u << 20)
+int dora_varlen_attn_noalloc(const void* q, const void* k, const void* v, const int32_t* cu_seqlens,
+                             int32_t B, int32_t H, int32_t D, int32_t max_seqlen, int64_t total,
+                             float softmax_scale, dora_dtype dtype, void* out, int32_t* dev_status,
+                             void* stream);
 
 /* Human-readable name of a dora_status value (static string). */
 const char* dora_status_string(int status);

@@ -36,6 +36,7 @@ DORA_ERR_UNSUPPORTED = -5
 DORA_ERR_CAPACITY = -6
 DORA_ERR_HIP = -7
 DORA_ERR_WORKSPACE = -8
+DORA_ERR_STATIC_LIMIT = -9
 
 DORA_DEV_KEEP_RANGE = 0x1
 DORA_DEV_CAPACITY = 0x2
@@ -47,6 +48,7 @@ DORA_DEV_ACTOR = 0x20
 DORA_MAX_ROW_TOKENS = 2048
 DORA_MAX_SEQLEN = 16384
 DORA_HEAD_DIM = 64
+DORA_NOALLOC_WORKSPACE_BYTES = 4 << 20
 
 EXPORTS = (
     "dora_select_pack",
@@ -63,6 +65,7 @@ EXPORTS = (
     "dora_varlen_attn_plan",
     "dora_varlen_attn_execute",
     "dora_varlen_attn",
+    "dora_varlen_attn_noalloc",
     "dora_status_string",
 )
 
@@ -125,6 +128,8 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
                                              ctypes.c_float, ctypes.c_int, vp, vp, sz, vp, vp]
     lib.dora_varlen_attn.restype = ctypes.c_int
     lib.dora_varlen_attn.argtypes = lib.dora_varlen_attn_execute.argtypes
+    lib.dora_varlen_attn_noalloc.restype = ctypes.c_int
+    lib.dora_varlen_attn_noalloc.argtypes = lib.dora_varlen_attn_execute.argtypes[:12] + [vp, vp]
     lib.dora_status_string.restype = ctypes.c_char_p
     lib.dora_status_string.argtypes = [ctypes.c_int]
     if path is None:
@@ -550,4 +555,23 @@ def dora_varlen_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, cu_seqle
         _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
         _dev(dev_status, "dev_status", torch.int32), _stream(stream))
     _check("dora_varlen_attn", rc)
+    return out
+
+
+def dora_varlen_attn_noalloc(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, cu_seqlens: torch.Tensor,
+                             max_seqlen: int, out: torch.Tensor, softmax_scale: float = 0.0,
+                             dev_status: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """dora_varlen_attn with the library's static per-GPU workspace: no device
+    allocation in the call (out and dev_status must be given).  Calls that
+    overlap in time on one GPU race on that workspace."""
+    if out is None or dev_status is None:
+        raise ValueError("dora_varlen_attn_noalloc allocates nothing: pass out and dev_status")
+    lib = load_library()
+    total, H, D, out = _attn_args(q, k, v, cu_seqlens, out)
+    B = int(cu_seqlens.shape[0]) - 1
+    rc = lib.dora_varlen_attn_noalloc(
+        _dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(cu_seqlens, "cu_seqlens", torch.int32),
+        B, H, D, int(max_seqlen), total, float(softmax_scale), _dtype_code(q), _dev(out, "out"),
+        _dev(dev_status, "dev_status", torch.int32), _stream(stream))
+    _check("dora_varlen_attn_noalloc", rc)
     return out

@@ -1146,6 +1146,56 @@ extern "C" int dora_varlen_attn(const void* q, const void* k, const void* v,
                                   dtype, out, workspace, workspace_bytes, dev_status, stream);
 }
 
+// Workspace of dora_varlen_attn_noalloc: one per GPU, for the life of the
+// process.  Host code never passes the array's name to a kernel (on the host
+// it is a stand-in, not a device address); it uses the address that
+// hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) uint8_t scratch[DORA_NOALLOC_WORKSPACE_BYTES];
+
+namespace dora {
+namespace {
+
+// Device address of `scratch` on the current device, looked up on the first
+// call there and kept (a per-device atomic: concurrent first calls store the
+// same address).
+int noalloc_workspace(void** out) {
+  static std::atomic<void*> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return DORA_ERR_HIP;
+  void* ptr = cache[dev].load(std::memory_order_acquire);
+  if (ptr == nullptr) {
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return DORA_ERR_HIP;
+    cache[dev].store(ptr, std::memory_order_release);
+  }
+  *out = ptr;
+  return DORA_OK;
+}
+
+}  // namespace
+}  // namespace dora
+
+extern "C" int dora_varlen_attn_noalloc(const void* q, const void* k, const void* v,
+                                        const int32_t* cu_seqlens, int32_t B, int32_t H, int32_t D,
+                                        int32_t max_seqlen, int64_t total, float softmax_scale,
+                                        dora_dtype dtype, void* out, int32_t* dev_status, void* stream) {
+  using namespace dora;
+  if (!q || !k || !v || !cu_seqlens || !out || !dev_status) return DORA_ERR_NULL;
+  if (dtype != DORA_F32 && dtype != DORA_BF16) return DORA_ERR_DTYPE;
+  if (D != DORA_HEAD_DIM) return DORA_ERR_SHAPE;
+  const int sz = check_attn_sizes(B, H, max_seqlen, total);
+  if (sz != DORA_OK) return sz;
+  if ((reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(k) | reinterpret_cast<uintptr_t>(v) |
+       reinterpret_cast<uintptr_t>(out)) & 15u)
+    return DORA_ERR_ALIGN;
+  const size_t need = attn_workspace_layout(B, H, max_seqlen).bytes;
+  if (need > DORA_NOALLOC_WORKSPACE_BYTES) return DORA_ERR_STATIC_LIMIT;
+  void* ws = nullptr;
+  const int rc = noalloc_workspace(&ws);
+  if (rc != DORA_OK) return rc;
+  return dora_varlen_attn(q, k, v, cu_seqlens, B, H, D, max_seqlen, total, softmax_scale, dtype, out, ws,
+                          DORA_NOALLOC_WORKSPACE_BYTES, dev_status, stream);
+}
+
 extern "C" const char* dora_status_string(int status) {
   switch (status) {
     case DORA_OK: return "DORA_OK";
@@ -1157,6 +1207,7 @@ extern "C" const char* dora_status_string(int status) {
     case DORA_ERR_CAPACITY: return "DORA_ERR_CAPACITY: output capacity out of range";
     case DORA_ERR_HIP: return "DORA_ERR_HIP: HIP runtime error at launch";
     case DORA_ERR_WORKSPACE: return "DORA_ERR_WORKSPACE: workspace missing, misaligned or too small";
+    case DORA_ERR_STATIC_LIMIT: return "DORA_ERR_STATIC_LIMIT: sizes need more than the library's static workspace";
     default: return "unknown dora status";
   }
 }

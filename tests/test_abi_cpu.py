@@ -35,13 +35,13 @@ def test_constants_match_header():
                  "DORA_DEV_PLAN", "DORA_DEV_ACTOR", "DORA_MAX_ROW_TOKENS", "DORA_MAX_SEQLEN", "DORA_HEAD_DIM"]:
         m = re.search(r"#define\s+%s\s+(0x[0-9a-fA-F]+|\d+)" % name, text)
         assert m and int(m.group(1), 0) == getattr(dora, name), name
-    for name, val in re.findall(r"(DORA_(?:OK|ERR_[A-Z]+))\s*=\s*(-?\d+)", text):
+    for name, val in re.findall(r"(DORA_(?:OK|ERR_[A-Z_]+))\s*=\s*(-?\d+)", text):
         assert getattr(dora, name) == int(val), name
 
 
 def test_status_strings():
     assert dora.dora_status_string(0) == "DORA_OK"
-    for code in range(-8, 0):
+    for code in range(-9, 0):
         assert dora.dora_status_string(code).startswith("DORA_ERR_")
     assert "unknown" in dora.dora_status_string(-99)
 
@@ -259,6 +259,34 @@ def test_attention_host_validation():
     assert ex(total=-1) == (dora.DORA_ERR_SHAPE,) * 2
     assert lib.dora_varlen_attn_plan(None, 4, 3, 197, 100, FAKE, ws, FAKE, None) == dora.DORA_ERR_NULL
     assert lib.dora_varlen_attn_plan(FAKE, 4, 3, 197, 100, None, ws, FAKE, None) == dora.DORA_ERR_WORKSPACE
+
+
+def test_noalloc_host_validation():
+    """dora_varlen_attn_noalloc rejects bad arguments, and sizes whose plan
+    would not fit the static workspace, before any device call."""
+    lib = dora.load_library()
+    m = re.search(r"#define\s+DORA_NOALLOC_WORKSPACE_BYTES\s+\((\d+)u\s*<<\s*(\d+)\)", open(HEADER).read())
+    assert m and int(m.group(1)) << int(m.group(2)) == dora.DORA_NOALLOC_WORKSPACE_BYTES
+
+    def na(**kw):
+        a = dict(q=FAKE, k=FAKE, v=FAKE, cu=FAKE, B=4, H=3, D=64, max_seqlen=197, total=100, scale=0.0,
+                 dtype=1, out=FAKE, status=FAKE, stream=None)
+        a.update(kw)
+        return lib.dora_varlen_attn_noalloc(a["q"], a["k"], a["v"], a["cu"], a["B"], a["H"], a["D"],
+                                            a["max_seqlen"], a["total"], a["scale"], a["dtype"], a["out"],
+                                            a["status"], a["stream"])
+
+    assert na(q=None) == dora.DORA_ERR_NULL
+    assert na(status=None) == dora.DORA_ERR_NULL
+    assert na(dtype=5) == dora.DORA_ERR_DTYPE
+    assert na(D=128) == dora.DORA_ERR_SHAPE
+    assert na(B=0) == dora.DORA_ERR_SHAPE
+    assert na(out=FAKE + 8) == dora.DORA_ERR_ALIGN
+    # 4094 x 128 one-chunk items fill the 4 MiB array exactly; one more sequence does not fit
+    assert dora.dora_varlen_attn_workspace_size(4094, 128, 192) == dora.DORA_NOALLOC_WORKSPACE_BYTES
+    assert dora.dora_varlen_attn_workspace_size(4095, 128, 192) > dora.DORA_NOALLOC_WORKSPACE_BYTES
+    assert na(B=4095, H=128, max_seqlen=192) == dora.DORA_ERR_STATIC_LIMIT
+    assert na(B=8192, H=64, max_seqlen=dora.DORA_MAX_SEQLEN) == dora.DORA_ERR_STATIC_LIMIT
 
 
 def test_product_package_does_not_touch_the_oracle():
