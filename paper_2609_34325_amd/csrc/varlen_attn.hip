@@ -419,14 +419,15 @@ __device__ __forceinline__ void q_read(const uint16_t* Qs, const LdsOffsets& lo,
   }
 }
 
-// S^T[key][query] for keys kb .. kb+63 of the staged block: 4 key tiles of 16
-// against query tile 0 (and tile 1 when ACT1).
-template <bool ACT1>
+// S^T[key][query] for keys kb .. kb+63 of the staged block (kb .. kb+31 for a
+// HALF block, the last block of a sequence when at most 32 keys remain): 4 (2)
+// key tiles of 16 against query tile 0 (and tile 1 when ACT1).
+template <bool ACT1, bool HALF>
 __device__ __forceinline__ void qk_block(const LanePtrs& lp, int kb, const bf16x8 (&qf)[2][2],
                                          floatx4 (&s)[2][4]) {
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int kt = 0; kt < 4; ++kt) {
+  for (int kt = 0; kt < (HALF ? 2 : 4); ++kt) {
     const int off = (kb + kt * 16) * kRowBytes;
     const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(lp.k0 + off);
     const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(lp.k1 + off);
@@ -454,27 +455,30 @@ __device__ __forceinline__ float row_group_max(float m) {
   return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
-// Online softmax of one 64-key block followed by O^T += V^T P^T.  FIRST marks
-// an item's first block: the running max starts at the block max and the
-// accumulators start from zero.  In a partial block (kvalid < 64) the keys
-// past the end are copies of the last key, with zero V rows: they leave every
-// block maximum unchanged and add nothing to O, and the denominators skip
-// them (their row of the ones operand is zero).
-template <bool ACT1, bool FIRST>
+// Online softmax of one 64-key block (32 keys when HALF) followed by
+// O^T += V^T P^T.  FIRST marks an item's first block: the running max starts
+// at the block max and the accumulators start from zero.  In a partial block
+// (kvalid < 64, or < 32 when HALF) the keys past the end are copies of the
+// last key, with zero V rows: they leave every block maximum unchanged and add
+// nothing to O, and the denominators skip them (their row of the ones operand
+// is zero).
+template <bool ACT1, bool FIRST, bool HALF>
 __device__ __forceinline__ void softmax_pv_block(const LanePtrs& lp, int kb, int kvalid, float scale_log2,
                                                  const bf16x8& ones, floatx4 (&s)[2][4],
                                                  SoftmaxState& st) {
   constexpr int kTiles = ACT1 ? 2 : 1;
+  constexpr int kKt = HALF ? 2 : 4;  // 16-key tiles in the block
+  constexpr int kKs = HALF ? 1 : 2;  // 32-key P.V steps in the block
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4;
-  // The lane's maximum over its 16 scores (raw units; the scale is positive).
+  // The lane's maximum over its 16 (8) scores (raw units; the scale is positive).
   float lm[2];
 #pragma unroll
   for (int j = 0; j < kTiles; ++j) {
     float m = fmaxf(fmaxf(s[j][0][0], s[j][0][1]), s[j][0][2]);
     m = fmaxf(fmaxf(m, s[j][0][3]), s[j][1][0]);
 #pragma unroll
-    for (int kt = 1; kt < 4; ++kt) {
+    for (int kt = 1; kt < kKt; ++kt) {
       const int i0 = kt == 1 ? 1 : 0;
 #pragma unroll
       for (int i = i0; i < 4; ++i) m = fmaxf(m, s[j][kt][i]);
@@ -509,12 +513,12 @@ __device__ __forceinline__ void softmax_pv_block(const LanePtrs& lp, int kb, int
   for (int j = 0; j < kTiles; ++j) {
     const float neg_m = -st.m[j];
 #pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
+    for (int kt = 0; kt < kKt; ++kt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) s[j][kt][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[j][kt][i], scale_log2, neg_m));
     // PV step ks, B operand k = 8g + e <-> key ks*32 + (e < 4 ? 4g + e : 16 + 4g + e - 4).
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
+    for (int ks = 0; ks < kKs; ++ks)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         pb[j][ks][e] = static_cast<__bf16>(s[j][2 * ks][e]);
@@ -527,7 +531,7 @@ __device__ __forceinline__ void softmax_pv_block(const LanePtrs& lp, int kb, int
   // lane group g stands for the key of P^T's element e.
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int ks = 0; ks < 2; ++ks) {
+  for (int ks = 0; ks < kKs; ++ks) {
     const bool init = FIRST && ks == 0;
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) {
@@ -541,14 +545,17 @@ __device__ __forceinline__ void softmax_pv_block(const LanePtrs& lp, int kb, int
         st.o[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[j][ks], init ? zero : st.o[j][dt], 0, 0, 0);
     }
   }
-  if (kvalid < 64) {
+  if (kvalid < kKs * 32) {
+    // Key of element e = ks*32 + 4g + (e < 4 ? e : 12 + e): compared as
+    // 4g < kvalid - (the rest), one lane value against scalars.
+    const int g4 = 4 * g;
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
+    for (int ks = 0; ks < kKs; ++ks) {
       bf16x8 on;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const int key = ks * 32 + (e < 4 ? 4 * g + e : 12 + 4 * g + e);
-        on[e] = key < kvalid ? ones[e] : static_cast<__bf16>(0.0f);
+        const int rest = ks * 32 + (e < 4 ? e : 12 + e);
+        on[e] = g4 < kvalid - rest ? ones[e] : static_cast<__bf16>(0.0f);
       }
 #pragma unroll
       for (int j = 0; j < kTiles; ++j)
@@ -556,30 +563,41 @@ __device__ __forceinline__ void softmax_pv_block(const LanePtrs& lp, int kb, int
     }
   } else {
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
+    for (int ks = 0; ks < kKs; ++ks)
 #pragma unroll
       for (int j = 0; j < kTiles; ++j)
         st.l[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[j][ks], FIRST && ks == 0 ? zero : st.l[j], 0, 0, 0);
   }
 }
 
-// All key blocks of one stage (nk >= 1 keys in LDS).  Two key blocks are in
-// flight: the MFMAs of block kb+64 are issued before the softmax of block kb,
-// so the matrix unit and the VALU overlap.
+// All key blocks of one stage (nk >= 1 keys in LDS): 64-key blocks, except
+// that a last block of at most 32 keys runs as a 32-key half block after the
+// others.  Two key blocks are in flight: the MFMAs of block kb+64 are issued
+// before the softmax of block kb, so the matrix unit and the VALU overlap.
 template <bool ACT1>
 __device__ __forceinline__ void attend_stage(const LanePtrs& lp, int nk, bool first, float scale_log2,
                                              const bf16x8& ones, const bf16x8 (&qf)[2][2], SoftmaxState& sm) {
-  floatx4 sa[2][4], sbk[2][4];
-  qk_block<ACT1>(lp, 0, qf, sa);
-  if (nk > 64) qk_block<ACT1>(lp, 64, qf, sbk);
-  if (first) softmax_pv_block<ACT1, true>(lp, 0, nk, scale_log2, ones, sa, sm);
-  else softmax_pv_block<ACT1, false>(lp, 0, nk, scale_log2, ones, sa, sm);
-  for (int kb = 64; kb < nk; kb += 128) {
-    if (kb + 64 < nk) qk_block<ACT1>(lp, kb + 64, qf, sa);
-    softmax_pv_block<ACT1, false>(lp, kb, nk - kb, scale_log2, ones, sbk, sm);
-    if (kb + 64 >= nk) break;
-    if (kb + 128 < nk) qk_block<ACT1>(lp, kb + 128, qf, sbk);
-    softmax_pv_block<ACT1, false>(lp, kb + 64, nk - kb - 64, scale_log2, ones, sa, sm);
+  const int tail = nk & 63;
+  const int nm = tail != 0 && tail <= 32 ? nk - tail : nk;  // keys of the 64-key blocks
+  if (nm > 0) {
+    floatx4 sa[2][4], sbk[2][4];
+    qk_block<ACT1, false>(lp, 0, qf, sa);
+    if (nm > 64) qk_block<ACT1, false>(lp, 64, qf, sbk);
+    if (first) softmax_pv_block<ACT1, true, false>(lp, 0, nm, scale_log2, ones, sa, sm);
+    else softmax_pv_block<ACT1, false, false>(lp, 0, nm, scale_log2, ones, sa, sm);
+    for (int kb = 64; kb < nm; kb += 128) {
+      if (kb + 64 < nm) qk_block<ACT1, false>(lp, kb + 64, qf, sa);
+      softmax_pv_block<ACT1, false, false>(lp, kb, nm - kb, scale_log2, ones, sbk, sm);
+      if (kb + 64 >= nm) break;
+      if (kb + 128 < nm) qk_block<ACT1, false>(lp, kb + 128, qf, sbk);
+      softmax_pv_block<ACT1, false, false>(lp, kb + 64, nm - kb - 64, scale_log2, ones, sa, sm);
+    }
+  }
+  if (nm < nk) {
+    floatx4 st[2][4];
+    qk_block<ACT1, true>(lp, nm, qf, st);
+    if (first && nm == 0) softmax_pv_block<ACT1, true, true>(lp, nm, nk - nm, scale_log2, ones, st, sm);
+    else softmax_pv_block<ACT1, false, true>(lp, nm, nk - nm, scale_log2, ones, st, sm);
   }
 }
 
