@@ -84,7 +84,8 @@ KERNEL_SOURCES = {"lc1": "paper_2609_34325_amd/csrc/lc1_readout.hip",
                   "select_pack": "paper_2609_34325_amd/csrc/select_pack.hip",
                   "residual": "paper_2609_34325_amd/csrc/select_pack.hip"}
 KERNEL_NAMES = {"attn": ("attn_fwd_bf16_kernel", "attn_fwd_f32_kernel"),
-                "select_pack": ("select_pack_kernel", "keep_scan_kernel"),
+                "select_pack": ("select_pack_kernel",),
+                "scan": ("keep_scan_kernel",),
                 "residual": ("select_pack_residual_kernel",),
                 "actor": ("actor_gate_kernel", "actor_decode_kernel"),
                 "pl": ("pl_kernel",),
@@ -968,6 +969,43 @@ def adjacent_legs(head: ConfigRun, cold_sets, args, torch, dora, stream, phases)
                         "note": "one workgroup per image: LDS bitonic sort of the visual keys and a block scan"}
     print(f"[bench] trajectory flops {ms_fl * 1e3:.1f} us, pl sample {ms_pl * 1e3:.1f} us",
           file=sys.stderr, flush=True)
+    del s_d, g_d
+
+    # Large batches: past 2048 images a block scan writes cu_seqlens before
+    # the gather (DeiT-B's keep rule; scores and keep counts from the seeded
+    # host streams, token rows filled on the device from a seeded generator).
+    large = []
+    for Bl, C in ((8192, 768), (65536, 192)):
+        wl = W.Workload(f"{w.name}_B{Bl}", w.seed, Bl, w.N, C // W.HEAD_DIM, w.dtype, w.keep_rule)
+        rl = W.generate(wl, parts=("keep", "scores"))[0]
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(wl.seed)
+        tok = torch.randint(-2 ** 15, 2 ** 15, (Bl, w.N, C), dtype=torch.int16, device="cuda",
+                            generator=gen).view(torch.bfloat16)
+        sc, kp = head.dev(rl.scores), head.dev(rl.keep)
+        skl = rl.total_keep
+        idx_l = torch.empty(skl, dtype=torch.int32, device="cuda")
+        cu_l = torch.empty(Bl + 1, dtype=torch.int32, device="cuda")
+        pk_l = torch.empty((skl, C), dtype=torch.bfloat16, device="cuda")
+        st_l2 = dora.new_status()
+
+        def big_call():
+            dora.dora_select_pack(sc, kp, tok, idx_out=idx_l, cu_out=cu_l, packed_out=pk_l, cap_rows=skl,
+                                  dev_status=st_l2, stream=stream)
+
+        ms_b = time_calls(torch, stream, big_call, args, phases, f"select_pack:B{Bl}", ("scan", "select_pack"))
+        assert int(st_l2.item()) == 0, f"device status {int(st_l2.item())}"
+        bl = 2 * skl * C * 2 + 4 * (Bl * w.N + skl + 2 * Bl + 1)
+        large.append({"B": Bl, "N": w.N, "C": C, "sum_keep": skl, "us": ms_b * 1e3, "algorithmic_bytes": bl,
+                      "GBs": bl / (ms_b * 1e-3) / 1e9, "hbm_frac": bl / (ms_b * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                      "tokens_per_s": skl / (ms_b * 1e-3)})
+        print(f"[bench] select/pack B={Bl} C={C}: {ms_b * 1e3:.1f} us ({large[-1]['GBs']:.0f} GB/s)",
+              file=sys.stderr, flush=True)
+        del tok, pk_l, idx_l, sc, kp
+        torch.cuda.empty_cache()
+    out["large_batch_select_pack"] = {"entry": "dora_select_pack", "kernels": ["keep_scan_kernel", "select_pack_kernel"],
+                                      "note": "past 2048 images one workgroup scans the keep counts first",
+                                      "runs": large}
     return out
 
 

@@ -111,7 +111,12 @@ typedef enum {
  *   cap_rows   rows available in idx_out / packed_out, 1 .. 2^31-1.
  *   dev_status int32 device word, see DORA_DEV_*.
  *
- * Returns DORA_OK or a negative dora_status; enqueues one kernel.
+ * cu_out is the running total of the keep counts.  Up to 2048 images each
+ * workgroup sums the counts before its own image; past 2048 images one
+ * workgroup first scans all counts into cu_out, in a launch of its own.
+ *
+ * Returns DORA_OK or a negative dora_status; enqueues one kernel (two past
+ * 2048 images).
  */
 int dora_select_pack(const float* scores, const int32_t* keep, const void* tokens,
                      const int32_t* cu_in, int64_t total_in, int32_t B, int32_t N, int32_t C,
@@ -157,9 +162,13 @@ int dora_varlen_attn_plan(const int32_t* cu_seqlens, int32_t B, int32_t H, int32
  * The select/pack arguments and results are those of dora_select_pack.  The
  * plan written into `workspace` serves dora_varlen_attn_execute with
  * cu_seqlens = cu_out and the same B, H, max_seqlen and total, exactly as a
- * dora_varlen_attn_plan call on cu_out would (its items are ordered by
- * decreasing keep count, then by image); the plan depends on the keep
- * counts only, so it is built while the rows are copied instead of after.
+ * dora_varlen_attn_plan call on cu_out would.  Up to 2048 images it is built
+ * in the select/pack launch while the rows are copied (it depends on the
+ * keep counts only), its items ordered by decreasing keep count, then by
+ * image.  Past 2048 images the keep counts are first scanned into cu_out by
+ * a one-workgroup launch and the plan is made from cu_out as
+ * dora_varlen_attn_plan makes it (decreasing length, equal lengths in an
+ * unspecified order); attention results do not depend on that order.
  *
  *   H, max_seqlen, total  as for dora_varlen_attn_plan; total is the row
  *              count of the Q/K/V buffers that execute will read.
@@ -169,7 +178,8 @@ int dora_varlen_attn_plan(const int32_t* cu_seqlens, int32_t B, int32_t H, int32
  *              keep[b] is outside [1, max_seqlen] or sum(keep) > total (the
  *              plan is then empty and execute writes nothing).
  *
- * Returns DORA_OK or a negative dora_status; enqueues one kernel.
+ * Returns DORA_OK or a negative dora_status; enqueues one kernel (three
+ * past 2048 images).
  */
 int dora_select_pack_plan(const float* scores, const int32_t* keep, const void* tokens,
                           const int32_t* cu_in, int64_t total_in, int32_t B, int32_t N, int32_t C,
@@ -197,7 +207,8 @@ int dora_select_pack_plan(const float* scores, const int32_t* keep, const void* 
  * dora_select_pack.  packed_out must not overlap h or a.
  *
  * Returns DORA_OK or a negative dora_status (DORA_ERR_NULL for a NULL a,
- * DORA_ERR_ALIGN for a misaligned one); enqueues one kernel.
+ * DORA_ERR_ALIGN for a misaligned one); enqueues one kernel (two past 2048
+ * images, as dora_select_pack).
  */
 int dora_select_pack_residual(const float* scores, const int32_t* keep, const void* h, const void* a,
                               const int32_t* cu_in, int64_t total_in, int32_t B, int32_t N, int32_t C,

@@ -15,6 +15,13 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 // Number of compute units of the current device (cached per device id).
 int device_cu_count(int* device_out);
 
+// Enqueues the attention plan kernel: items of the layout cu[0..B] into the
+// workspace (sizes already checked by the caller).  Sequences shorter than
+// min_len, longer than max_seqlen or past total make the plan empty and set
+// DORA_DEV_CU_SEQLENS.
+int launch_attn_plan(const int32_t* cu, int32_t B, int32_t H, int32_t max_seqlen, int64_t total, int32_t min_len,
+                     void* workspace, int32_t* dev_status, void* stream);
+
 // 16-byte stores at system scope (sc1), non-temporal (nt): written through
 // the L2 and not kept there, so no line is left dirty (a bulk output written
 // with plain stores leaves up to the L2's capacity dirty: several

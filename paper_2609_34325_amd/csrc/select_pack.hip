@@ -37,6 +37,12 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kDigitSelectSlots = 8;  // rows of more than 256 tokens select by 8-bit digits
 constexpr int kCopyUnroll = 2;  // loads in flight per lane: few, so stores start early (measured best)
+// Up to this many images each workgroup sums keep[0..b) itself (at most 8 KB
+// of keep counts from the L2, cheaper than a second launch); above it one
+// workgroup scans the keep counts into cu_out first.
+constexpr int kFusedScanMaxB = 2048;
+constexpr int kScanThreads = 1024;
+constexpr int kScanPer = 8;  // keep counts per thread and tile
 
 struct SelectPackParams {
   const float* scores;
@@ -56,6 +62,9 @@ struct SelectPackParams {
   int2* plan_items;
   int32_t H, max_seqlen, max_items;
   int64_t plan_total;
+  // cu_out was written by keep_scan_kernel before this launch (batches of
+  // more than kFusedScanMaxB images): each workgroup reads its offset there.
+  int32_t cu_ready;
 };
 
 // Order-preserving key: larger key = preferred for keeping.  -0 and +0 map
@@ -188,6 +197,22 @@ __device__ __forceinline__ void select_pack_body(const SelectPackParams& p) {
     n = p.N;
   }
   const int kb = p.keep[b];
+  const long long cu_b = p.cu_ready ? static_cast<long long>(p.cu_out[b]) : 0;
+  // Wave 0's score loads go out before the keep count is checked: they
+  // depend on the segment only, so they overlap the keep count's load instead
+  // of following it.  All SLOTS loads are issued before the first is used:
+  // positions past the segment read its last score (they are not
+  // candidates), and the empty asm consumes every loaded value, so the
+  // compiler cannot sink a load into the branch of its only use, where each
+  // would wait alone.
+  float x[SLOTS];
+  if (wave == 0 && seg_ok) {
+    const long long last = off_in + n - 1;
+#pragma unroll
+    for (int r = 0; r < SLOTS; ++r) x[r] = p.scores[min(off_in + r * 64 + lane, last)];
+#pragma unroll
+    for (int r = 0; r < SLOTS; ++r) asm volatile("" : "+v"(x[r]));
+  }
   const bool img_ok = seg_ok && kb >= 1 && kb <= n;
   // With a plan, workgroup (b, 0) writes image b's attention items and
   // workgroup (0, 0) the plan header.
@@ -195,57 +220,50 @@ __device__ __forceinline__ void select_pack_body(const SelectPackParams& p) {
   const bool plan_head = p.plan_hdr != nullptr && blockIdx.x == 0;
 
   if (wave != 0) {
-    // Output offset of image b: keep[0] + ... + keep[b-1].  For the plan, the
-    // items of the sequences that precede b in the queue order (longer
-    // first, then lower index) give the position of b's first item.
-    long long part = 0, before = 0, items = 0, kept = 0;
-    int bad = 0;
-    const int jend = plan_img ? p.B : b;
-    for (int j = tid - 64; j < jend; j += kThreads - 64) {
-      const int kj = p.keep[j];
-      if (j < b) part += kj;
-      if (plan_img) {
-        const bool fits = kj >= 1 && kj <= p.max_seqlen;
-        const int cj = fits ? p.H * attn_chunks(kj) : 0;
-        if (kj > kb || (kj == kb && j < b)) before += cj;
-        if (plan_head) {
-          items += cj;
-          kept += kj;
-          bad |= !fits;
+    if (!p.cu_ready) {
+      // Output offset of image b: keep[0] + ... + keep[b-1].  For the plan,
+      // the items of the sequences that precede b in the queue order (longer
+      // first, then lower index) give the position of b's first item.
+      long long part = 0, before = 0, items = 0, kept = 0;
+      int bad = 0;
+      const int jend = plan_img ? p.B : b;
+      for (int j = tid - 64; j < jend; j += kThreads - 64) {
+        const int kj = p.keep[j];
+        if (j < b) part += kj;
+        if (plan_img) {
+          const bool fits = kj >= 1 && kj <= p.max_seqlen;
+          const int cj = fits ? p.H * attn_chunks(kj) : 0;
+          if (kj > kb || (kj == kb && j < b)) before += cj;
+          if (plan_head) {
+            items += cj;
+            kept += kj;
+            bad |= !fits;
+          }
         }
       }
-    }
-    part = wave_sum(part);
-    if (lane == 0) s_part[wave] = part;
-    if (plan_img) {
-      before = wave_sum(before);
-      if (lane == 0) s_before[wave] = before;
-    }
-    if (plan_head) {
-      items = wave_sum(items);
-      kept = wave_sum(kept);
-      bad = __ballot(bad != 0) != 0ull;
-      if (lane == 0) {
-        s_items[wave] = items;
-        s_kept[wave] = kept;
-        s_bad[wave] = bad;
+      part = wave_sum(part);
+      if (lane == 0) s_part[wave] = part;
+      if (plan_img) {
+        before = wave_sum(before);
+        if (lane == 0) s_before[wave] = before;
+      }
+      if (plan_head) {
+        items = wave_sum(items);
+        kept = wave_sum(kept);
+        bad = __ballot(bad != 0) != 0ull;
+        if (lane == 0) {
+          s_items[wave] = items;
+          s_kept[wave] = kept;
+          s_bad[wave] = bad;
+        }
       }
     }
   } else if (img_ok) {
     // Candidates are positions 1..n-1 (CLS, position 0, is not a candidate).
-    // Position pos = r*64 + lane lives in key[r] of that lane.
-    // All SLOTS loads are issued before the first is used: positions past
-    // the segment read its last score (they are not candidates), and the
-    // empty asm consumes every loaded value, so the compiler cannot sink a
-    // load into the branch of its only use, where each would wait alone.
+    // Position pos = r*64 + lane lives in key[r] of that lane (score x[r],
+    // loaded above).
     uint32_t key[SLOTS];
     uint64_t valid[SLOTS];
-    float x[SLOTS];
-    const long long last = off_in + n - 1;
-#pragma unroll
-    for (int r = 0; r < SLOTS; ++r) x[r] = p.scores[min(off_in + r * 64 + lane, last)];
-#pragma unroll
-    for (int r = 0; r < SLOTS; ++r) asm volatile("" : "+v"(x[r]));
 #pragma unroll
     for (int r = 0; r < SLOTS; ++r) {
       const int pos = r * 64 + lane;
@@ -291,7 +309,7 @@ __device__ __forceinline__ void select_pack_body(const SelectPackParams& p) {
     }
   }
   __syncthreads();
-  const long long off_out = s_part[1] + s_part[2] + s_part[3];
+  const long long off_out = p.cu_ready ? cu_b : s_part[1] + s_part[2] + s_part[3];
 
   if (plan_img && kb >= 1 && kb <= p.max_seqlen) {
     // Items (b, h, c) for head h and query chunk c, head-major.
@@ -319,8 +337,10 @@ __device__ __forceinline__ void select_pack_body(const SelectPackParams& p) {
   if (s == 0) {
     if (tid == 0) {
       if (off_out + kb > p.cap_rows) atomicOr(p.status, DORA_DEV_CAPACITY);
-      p.cu_out[b + 1] = static_cast<int32_t>(off_out + kb);
-      if (b == 0) p.cu_out[0] = 0;
+      if (!p.cu_ready) {
+        p.cu_out[b + 1] = static_cast<int32_t>(off_out + kb);
+        if (b == 0) p.cu_out[0] = 0;
+      }
     }
     for (int i = tid; i < kb; i += kThreads) {
       const long long row = off_out + i;
@@ -380,6 +400,61 @@ __global__ __launch_bounds__(kThreads) void select_pack_residual_kernel(SelectPa
   select_pack_body<SLOTS, MODE>(p);
 }
 
+__device__ __forceinline__ long long wave_inclusive_scan64(long long v, int lane) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const long long t = __shfl_up(v, off, 64);
+    if (lane >= off) v += t;
+  }
+  return v;
+}
+
+// Running total of the keep counts (Sec. 3.5 "Inference": the boundaries of
+// the packed buffer): cu_out[0] = 0, cu_out[b+1] = keep[0] + ... + keep[b],
+// held at the int32 range (a total past it is a capacity error either way).
+// One workgroup walks the counts in tiles of kScanThreads * kScanPer: each
+// thread sums its kScanPer counts, a block scan of those sums gives every
+// thread's starting total, and a carry joins the tiles.
+__global__ __launch_bounds__(kScanThreads) void keep_scan_kernel(const int32_t* keep, int32_t B, int32_t* cu_out) {
+  __shared__ long long s_wave[kScanThreads / 64];
+  __shared__ long long s_carry;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid == 0) {
+    s_carry = 0;
+    cu_out[0] = 0;
+  }
+  __syncthreads();
+  for (long long base = 0; base < B; base += static_cast<long long>(kScanThreads) * kScanPer) {
+    const long long first = base + static_cast<long long>(tid) * kScanPer;
+    long long v[kScanPer];
+    long long sum = 0;
+#pragma unroll
+    for (int i = 0; i < kScanPer; ++i) {
+      v[i] = first + i < B ? keep[first + i] : 0;
+      sum += v[i];
+    }
+    const long long incl = wave_inclusive_scan64(sum, lane);
+    if (lane == 63) s_wave[wave] = incl;
+    __syncthreads();
+    if (wave == 0) {
+      const long long x = lane < kScanThreads / 64 ? s_wave[lane] : 0;
+      const long long xi = wave_inclusive_scan64(x, lane);
+      if (lane < kScanThreads / 64) s_wave[lane] = xi - x;
+    }
+    __syncthreads();
+    long long run = s_carry + s_wave[wave] + incl - sum;
+#pragma unroll
+    for (int i = 0; i < kScanPer; ++i) {
+      run += v[i];
+      if (first + i < B) cu_out[first + i + 1] = static_cast<int32_t>(max(min(run, static_cast<long long>(INT_MAX)),
+                                                                             static_cast<long long>(INT_MIN)));
+    }
+    __syncthreads();
+    if (tid == kScanThreads - 1) s_carry = run;
+    __syncthreads();
+  }
+}
+
 template <int SLOTS>
 hipError_t launch(const SelectPackParams& p, int mode, hipStream_t stream) {
   const dim3 grid(p.B * p.split), block(kThreads);
@@ -434,12 +509,26 @@ int prepare(const float* scores, const int32_t* keep, const void* tokens, const 
   p->plan_items = nullptr;
   p->H = p->max_seqlen = p->max_items = 0;
   p->plan_total = 0;
+  p->cu_ready = 0;
   return DORA_OK;
 }
 
-int launch_select_pack(const SelectPackParams& p, void* stream, int mode = kCopy) {
+int launch_select_pack(SelectPackParams p, void* stream, int mode = kCopy) {
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t err;
+  if (p.B > kFusedScanMaxB) {
+    // Large batch: the block scan writes cu_out first; a plan is then built
+    // from cu_out by the attention plan kernel (sequences of at least one row).
+    hipLaunchKernelGGL(keep_scan_kernel, dim3(1), dim3(kScanThreads), 0, st, p.keep, p.B, p.cu_out);
+    if (hipGetLastError() != hipSuccess) return DORA_ERR_HIP;
+    if (p.plan_hdr != nullptr) {
+      const int rc = launch_attn_plan(p.cu_out, p.B, p.H, p.max_seqlen, p.plan_total, 1, p.plan_hdr, p.status, stream);
+      if (rc != DORA_OK) return rc;
+      p.plan_hdr = nullptr;
+      p.plan_items = nullptr;
+    }
+    p.cu_ready = 1;
+  }
   if (p.N <= 64) err = launch<1>(p, mode, st);
   else if (p.N <= 128) err = launch<2>(p, mode, st);
   else if (p.N <= 256) err = launch<4>(p, mode, st);

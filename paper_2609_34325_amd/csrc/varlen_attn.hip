@@ -63,6 +63,7 @@ constexpr float kLog2e = 1.4426950408889634f;
 struct PlanParams {
   const int32_t* cu;
   int32_t B, H, max_seqlen;
+  int32_t min_len;  // shortest valid sequence (0; 1 for the plan of a select/pack output)
   int64_t total;
   AttnPlanHeader* hdr;
   int2* items;
@@ -133,7 +134,7 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanParams p) {
   for (int b = tid; b < p.B; b += kPlanThreads) {
     const long long a = s_cu[b], e = s_cu[b + 1];
     const long long len = e - a;
-    if (a < 0 || e > p.total || len < 0 || len > p.max_seqlen || (b == 0 && a != 0)) s_bad = 1;
+    if (a < 0 || e > p.total || len < p.min_len || len > p.max_seqlen || (b == 0 && a != 0)) s_bad = 1;
     else atomicAdd(&hist[static_cast<int>(len) >> shift], 1);
   }
   __syncthreads();
@@ -1070,6 +1071,23 @@ int device_cu_count(int* device_out) {
   return n;
 }
 
+int launch_attn_plan(const int32_t* cu, int32_t B, int32_t H, int32_t max_seqlen, int64_t total, int32_t min_len,
+                     void* workspace, int32_t* dev_status, void* stream) {
+  const AttnWorkspaceLayout L = attn_workspace_layout(B, H, max_seqlen);
+  PlanParams p;
+  p.cu = cu;
+  p.B = B;
+  p.H = H;
+  p.max_seqlen = max_seqlen;
+  p.min_len = min_len;
+  p.total = total;
+  p.status = dev_status;
+  p.hdr = static_cast<AttnPlanHeader*>(workspace);
+  p.items = reinterpret_cast<int2*>(static_cast<char*>(workspace) + L.items_off);
+  hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(kPlanThreads), 0, static_cast<hipStream_t>(stream), p);
+  return hipGetLastError() == hipSuccess ? DORA_OK : DORA_ERR_HIP;
+}
+
 }  // namespace dora
 
 extern "C" size_t dora_varlen_attn_workspace_size(int32_t B, int32_t H, int32_t max_seqlen) {
@@ -1087,17 +1105,7 @@ extern "C" int dora_varlen_attn_plan(const int32_t* cu_seqlens, int32_t B, int32
   const AttnWorkspaceLayout L = attn_workspace_layout(B, H, max_seqlen);
   if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) || workspace_bytes < L.bytes)
     return DORA_ERR_WORKSPACE;
-  PlanParams p;
-  p.cu = cu_seqlens;
-  p.B = B;
-  p.H = H;
-  p.max_seqlen = max_seqlen;
-  p.total = total;
-  p.status = dev_status;
-  p.hdr = static_cast<AttnPlanHeader*>(workspace);
-  p.items = reinterpret_cast<int2*>(static_cast<char*>(workspace) + L.items_off);
-  hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(kPlanThreads), 0, static_cast<hipStream_t>(stream), p);
-  return hipGetLastError() == hipSuccess ? DORA_OK : DORA_ERR_HIP;
+  return launch_attn_plan(cu_seqlens, B, H, max_seqlen, total, 0, workspace, dev_status, stream);
 }
 
 extern "C" int dora_varlen_attn_execute(const void* q, const void* k, const void* v,

@@ -155,3 +155,69 @@ def test_fused_plan_errors_leave_an_empty_plan(gpu, case):
     torch.cuda.synchronize()
     assert int(st_t.item()) == 0
     assert np.all(to_host_bits(out) == 0x1234)
+
+
+def test_fused_plan_large_batch(gpu):
+    """8192 images: the keep counts are scanned first and the plan kernel
+    builds the plan from cu_seqlens.  Select/pack stays bit-exact; the plan
+    holds exactly the documented items, longer sequences first (equal
+    lengths in any order); attention on it equals attention on a separately
+    made plan bit for bit, and the oracle on every element."""
+    rng = np.random.default_rng(8192)
+    B, N, H = 8192, 64, 2
+
+    class R:
+        pass
+    r = R()
+    r.keep = rng.integers(1, N + 1, size=B).astype(np.int32)
+    r.scores = rng.standard_normal((B, N)).astype(np.float32)
+    r.tokens = rng.integers(0, 2 ** 16, size=(B, N, 8)).astype(np.uint16)
+    total = int(r.keep.sum())
+    idx, cu, packed, ws, st = fused(gpu, r, H, N, total)
+    assert st == 0
+    idx_o, cu_o, packed_o, st_o = oracle.select_pack(r.scores, r.keep, r.tokens)
+    assert st_o == 0
+    assert np.array_equal(cu.cpu().numpy(), cu_o)
+    assert np.array_equal(idx[:total].cpu().numpy(), idx_o)
+    assert np.array_equal(to_host_bits(packed[:total]), packed_o)
+    hdr, n, items = read_plan(ws)
+    want = expected_items(r.keep, H, N)
+    assert n == len(want)
+    lens = items[:, 1] >> 17
+    assert np.all(np.diff(lens) <= 0)
+    assert sorted(map(tuple, items.tolist())) == sorted(map(tuple, want.tolist()))
+    q, k, v = W.random_qkv(rng, r.keep, H, "bf16")
+    tq, tk, tv = to_dev(q), to_dev(k), to_dev(v)
+    st_t = torch.zeros(1, dtype=torch.int32, device="cuda")
+    out_fused = gpu.dora_varlen_attn_execute(tq, tk, tv, cu, N, ws, dev_status=st_t)
+    ws2 = gpu.new_workspace(B, H, N)
+    gpu.dora_varlen_attn_plan(cu, H, N, total, ws2, st_t)
+    out_sep = gpu.dora_varlen_attn_execute(tq, tk, tv, cu, N, ws2, dev_status=st_t)
+    torch.cuda.synchronize()
+    assert int(st_t.item()) == 0
+    assert np.array_equal(to_host_bits(out_fused), to_host_bits(out_sep))
+    assert_attn_close(widen(out_fused), oracle.varlen_attn(q, k, v, cu_o, "bf16"), "bf16", "8192 images")
+
+
+@pytest.mark.parametrize("case", ["keep_zero", "keep_above_max_seqlen"])
+def test_fused_plan_large_batch_errors(gpu, case):
+    """The same error contract past 2048 images: an empty plan and the bits."""
+    rng = np.random.default_rng(4099)
+    B, N, H = 4096, 40, 2
+
+    class R:
+        pass
+    r = R()
+    r.keep = np.full(B, 10, np.int32)
+    r.scores = rng.standard_normal((B, N)).astype(np.float32)
+    r.tokens = rng.integers(0, 2 ** 16, size=(B, N, 8)).astype(np.uint16)
+    max_seqlen, want_bits = N, gpu.DORA_DEV_CU_SEQLENS
+    if case == "keep_zero":
+        r.keep[2222] = 0
+        want_bits |= gpu.DORA_DEV_KEEP_RANGE
+    else:
+        max_seqlen = 9
+    _, _, _, ws, st = fused(gpu, r, H, max_seqlen, int(r.keep.sum()))
+    assert st & want_bits == want_bits
+    _, n, _ = read_plan(ws)
+    assert n == 0

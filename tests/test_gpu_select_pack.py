@@ -192,3 +192,49 @@ def test_digit_prefix_ties_every_keep_count(gpu, n):
     tokens = rng.integers(0, 2 ** 16, size=(n, n, 8)).astype(np.uint16)
     print(f"[select_pack] digit prefix ties n={n}", flush=True)
     check_round(gpu, scores, keep, tokens)
+
+
+@pytest.mark.parametrize("B", [2049, 8192, 65536])
+def test_large_batch_block_scan(gpu, B):
+    """Past 2048 images one workgroup scans the keep counts into cu_seqlens
+    before the gather (Sec. 3.5 "Inference": the packed buffer's
+    boundaries); the results stay bit-exact."""
+    rng = np.random.default_rng(B)
+    n = 197
+    scores = rng.standard_normal((B, n)).astype(np.float32)
+    keep = rng.integers(1, n + 1, size=B).astype(np.int32)
+    tokens = rng.integers(0, 2 ** 16, size=(B, n, 8)).astype(np.uint16)
+    print(f"[select_pack] large batch B={B} sum_keep={int(keep.sum())}", flush=True)
+    check_round(gpu, scores, keep, tokens)
+
+
+def test_large_batch_packed_input_rounds(gpu):
+    """Two chained rounds on packed input with 8192 images."""
+    rng = np.random.default_rng(8193)
+    B, n = 8192, 100
+    scores = rng.standard_normal((B, n)).astype(np.float32)
+    keep = rng.integers(1, n + 1, size=B).astype(np.int32)
+    tokens = rng.integers(0, 2 ** 16, size=(B, n, 8)).astype(np.uint16)
+    idx, cu, packed = check_round(gpu, scores, keep, tokens)
+    keep2 = np.maximum(1, (keep * rng.uniform(0.3, 1.0, B)).astype(np.int32))
+    scores2 = rng.standard_normal(int(keep.sum())).astype(np.float32)
+    check_round(gpu, scores2, keep2, packed, cu_in=cu, N=n)
+
+
+def test_large_batch_errors_write_nothing_past_cap(gpu):
+    """The scanned path keeps the error contract: a bad keep count sets its
+    bit, and nothing lands past the capacity."""
+    rng = np.random.default_rng(4097)
+    B, n = 4096, 40
+    scores = rng.standard_normal((B, n)).astype(np.float32)
+    tokens = rng.integers(0, 2 ** 16, size=(B, n, 8)).astype(np.uint16)
+    keep = np.full(B, 10, np.int32)
+    keep[3000] = 0
+    *_, st, canary = run_gpu(gpu, scores, keep, tokens, cap=B * 10, guard=8)
+    assert st & gpu.DORA_DEV_KEEP_RANGE and canary
+    keep = np.full(B, 30, np.int32)
+    idx, cu, packed, st, canary = run_gpu(gpu, scores, keep, tokens, cap=1000, guard=16)
+    assert st & gpu.DORA_DEV_CAPACITY and canary
+    idx_o, cu_o, packed_o, _ = oracle.select_pack(scores, keep, tokens)
+    assert np.array_equal(idx, idx_o[:1000]) and np.array_equal(packed, packed_o[:1000])
+    assert np.array_equal(cu, cu_o)
