@@ -58,10 +58,15 @@ __device__ __forceinline__ int lanes_below(uint64_t mask) {
 //   [2048, ...)   items[max_items]: int2 {x = first row of the sequence,
 //                 y = len << 17 | head << 9 | query chunk}
 //
-// A work item is one (sequence, head, chunk of kAttnQTile queries); items are
-// ordered by decreasing sequence length.  Item i belongs to sub-queue
-// i % kSubQueues, so each sub-queue is itself longest-first and the
-// sub-queues carry near-equal work.
+// A work item is one (sequence, head, chunk of at most kAttnQTile queries);
+// items are ordered by decreasing sequence length.  Item i belongs to
+// sub-queue i % kSubQueues, so each sub-queue is itself longest-first and the
+// sub-queues carry near-equal work.  Sequences with the same number of
+// chunks form a contiguous class; inside it, full blocks of kSubQueues
+// (sequence, head) groups place the chunks of group j at stride kSubQueues
+// (attn_item_slot), so every chunk of a (sequence, head) is in one sub-queue,
+// at consecutive tickets: the workgroups of one XCD take them together and
+// read that head's K/V through one L2.
 // ---------------------------------------------------------------------------
 constexpr int32_t kPlanMagic = 0x444F5241;  // "DORA"
 constexpr int kAttnQTile = 192;             // queries per work item (12 tiles of 16, one per wave)
@@ -115,6 +120,28 @@ inline int check_attn_sizes(int32_t B, int32_t H, int32_t max_seqlen, int64_t to
 
 // Query chunks of a sequence of `len` tokens (len >= 0).
 __host__ __device__ __forceinline__ int attn_chunks(int len) { return (len + kAttnQTile - 1) / kAttnQTile; }
+
+// Queries per chunk: the chunks share the sequence evenly, rounded up to
+// whole 16-query tiles (at most kAttnQTile; the last chunk takes the rest and
+// is never empty).
+__host__ __device__ __forceinline__ int attn_chunk_size(int len) {
+  if (len <= kAttnQTile) return (len + 15) & ~15;  // one chunk: no division on the common path
+  const int ch = attn_chunks(len);
+  return ((len + ch - 1) / ch + 15) & ~15;
+}
+
+// Item slot of chunk c of group gi (the sequence's rank inside its class
+// times H, plus the head) in a class of `groups` groups of ch chunks whose
+// items start at slot `base`.  Full blocks of kSubQueues groups put group j's
+// chunks at slots base + block * ch * kSubQueues + c * kSubQueues + j; the
+// groups past the last full block follow chunk after chunk.
+__host__ __device__ __forceinline__ long long attn_item_slot(long long base, int groups, int ch, int gi, int c) {
+  const int full = groups / kSubQueues * kSubQueues;
+  if (gi < full)
+    return base + static_cast<long long>(ch) * (gi / kSubQueues) * kSubQueues +
+           static_cast<long long>(c) * kSubQueues + gi % kSubQueues;
+  return base + static_cast<long long>(ch) * full + static_cast<long long>(gi - full) * ch + c;
+}
 
 // Item descriptor of chunk c of head h of the sequence at rows [seq0, seq0 + len).
 __device__ __forceinline__ int2 encode_item(int seq0, int len, int h, int c) {

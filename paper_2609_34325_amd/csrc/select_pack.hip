@@ -173,7 +173,9 @@ __device__ __forceinline__ void select_pack_body(const SelectPackParams& p) {
   __shared__ int32_t s_idx[SLOTS * 64];
   __shared__ __align__(16) uint32_t s_hist[SLOTS >= kDigitSelectSlots ? 256 : 1];  // digit histogram of the long-row select
   __shared__ long long s_part[kThreads / 64];
-  __shared__ long long s_before[kThreads / 64];  // plan items of the sequences ordered before b
+  __shared__ long long s_before[kThreads / 64];  // plan items of the sequences with more chunks than b
+  __shared__ int s_rank[kThreads / 64];          // sequences of b's chunk count ordered before b
+  __shared__ int s_members[kThreads / 64];       // sequences of b's chunk count
   __shared__ long long s_items[kThreads / 64];   // plan items of all sequences
   __shared__ long long s_kept[kThreads / 64];    // sum of all keep counts
   __shared__ int s_bad[kThreads / 64];           // some keep count outside [1, max_seqlen]
@@ -221,21 +223,28 @@ __device__ __forceinline__ void select_pack_body(const SelectPackParams& p) {
 
   if (wave != 0) {
     if (!p.cu_ready) {
-      // Output offset of image b: keep[0] + ... + keep[b-1].  For the plan,
-      // the items of the sequences that precede b in the queue order (longer
-      // first, then lower index) give the position of b's first item.
+      // Output offset of image b: keep[0] + ... + keep[b-1].  For the plan
+      // (queue order: longer sequences first, then lower index), b's class
+      // of sequences with its chunk count starts after the items of every
+      // sequence with more chunks; inside the class b's rank is the number of
+      // class members ordered before it.
       long long part = 0, before = 0, items = 0, kept = 0;
-      int bad = 0;
+      int rank = 0, members = 0, bad = 0;
+      const int chb = kb >= 1 && kb <= p.max_seqlen ? attn_chunks(kb) : 0;
       const int jend = plan_img ? p.B : b;
       for (int j = tid - 64; j < jend; j += kThreads - 64) {
         const int kj = p.keep[j];
         if (j < b) part += kj;
         if (plan_img) {
           const bool fits = kj >= 1 && kj <= p.max_seqlen;
-          const int cj = fits ? p.H * attn_chunks(kj) : 0;
-          if (kj > kb || (kj == kb && j < b)) before += cj;
+          const int chj = fits ? attn_chunks(kj) : 0;
+          if (chj > chb) before += p.H * chj;
+          if (fits && chj == chb) {
+            ++members;
+            rank += kj > kb || (kj == kb && j < b);
+          }
           if (plan_head) {
-            items += cj;
+            items += p.H * chj;
             kept += kj;
             bad |= !fits;
           }
@@ -245,7 +254,13 @@ __device__ __forceinline__ void select_pack_body(const SelectPackParams& p) {
       if (lane == 0) s_part[wave] = part;
       if (plan_img) {
         before = wave_sum(before);
-        if (lane == 0) s_before[wave] = before;
+        const long long rk = wave_sum(static_cast<long long>(rank));
+        const long long mb = wave_sum(static_cast<long long>(members));
+        if (lane == 0) {
+          s_before[wave] = before;
+          s_rank[wave] = static_cast<int>(rk);
+          s_members[wave] = static_cast<int>(mb);
+        }
       }
       if (plan_head) {
         items = wave_sum(items);
@@ -312,12 +327,16 @@ __device__ __forceinline__ void select_pack_body(const SelectPackParams& p) {
   const long long off_out = p.cu_ready ? cu_b : s_part[1] + s_part[2] + s_part[3];
 
   if (plan_img && kb >= 1 && kb <= p.max_seqlen) {
-    // Items (b, h, c) for head h and query chunk c, head-major.
-    const long long first = s_before[1] + s_before[2] + s_before[3];
+    // Items (b, h, c) for head h and query chunk c, each in its slot of the
+    // class (attn_item_slot).
+    const long long cls_base = s_before[1] + s_before[2] + s_before[3];
+    const int rank = s_rank[1] + s_rank[2] + s_rank[3];
+    const int groups = (s_members[1] + s_members[2] + s_members[3]) * p.H;
     const int ch = attn_chunks(kb);
     for (int i = tid; i < p.H * ch; i += kThreads) {
-      const int h = i / ch;
-      if (first + i < p.max_items) p.plan_items[first + i] = encode_item(static_cast<int>(off_out), kb, h, i - h * ch);
+      const int h = i / ch, c = i - h * ch;
+      const long long slot = attn_item_slot(cls_base, groups, ch, rank * p.H + h, c);
+      if (slot < p.max_items) p.plan_items[slot] = encode_item(static_cast<int>(off_out), kb, h, c);
     }
   }
   if (plan_head) {

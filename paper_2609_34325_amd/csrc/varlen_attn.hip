@@ -124,8 +124,13 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanParams p) {
   __shared__ int wave_sums[kPlanThreads / 64 + 1];
   __shared__ int s_bad;
   const int tid = threadIdx.x;
+  // Length bins: bin 0 for empty sequences, then (len - 1) >> shift + 1.
+  // The smallest shift that fits is at most 5 (max_seqlen <= 16384), and
+  // 2^shift divides kAttnQTile, so a bin never straddles a chunk boundary and
+  // the sequences of equal chunk count stay contiguous in the sorted order.
   int shift = 0;
-  while ((p.max_seqlen >> shift) >= kPlanBins) ++shift;
+  while (((p.max_seqlen - 1) >> shift) + 1 >= kPlanBins) ++shift;
+  auto bin_of = [shift](int len) { return len == 0 ? 0 : ((len - 1) >> shift) + 1; };
 
   for (int i = tid; i < kPlanBins; i += kPlanThreads) hist[i] = 0;
   for (int i = tid; i <= p.B; i += kPlanThreads) s_cu[i] = p.cu[i];
@@ -135,7 +140,7 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanParams p) {
     const long long a = s_cu[b], e = s_cu[b + 1];
     const long long len = e - a;
     if (a < 0 || e > p.total || len < p.min_len || len > p.max_seqlen || (b == 0 && a != 0)) s_bad = 1;
-    else atomicAdd(&hist[static_cast<int>(len) >> shift], 1);
+    else atomicAdd(&hist[bin_of(static_cast<int>(len))], 1);
   }
   __syncthreads();
   if (s_bad) {
@@ -156,7 +161,7 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanParams p) {
   __syncthreads();
   for (int b = tid; b < p.B; b += kPlanThreads) {
     const int len = s_cu[b + 1] - s_cu[b];
-    const int pos = atomicAdd(&hist[len >> shift], 1);
+    const int pos = atomicAdd(&hist[bin_of(len)], 1);
     order[pos] = static_cast<uint32_t>(b) | (static_cast<uint32_t>(len) << 13);
   }
   __syncthreads();
@@ -180,7 +185,10 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanParams p) {
   if (tid == 0) base[p.B] = n_items;
   __syncthreads();
 
-  // Emit: item t belongs to the last sorted position whose first item <= t.
+  // Emit: the t-th item in (position, head, chunk) order belongs to the last
+  // sorted position whose first item <= t; it goes to its slot in the class
+  // of sequences with its chunk count (attn_item_slot).
+  auto chunks_at = [&](int pos) { return attn_chunks(static_cast<int>(order[pos] >> 13)); };
   for (int t = tid; t < n_items; t += kPlanThreads) {
     int lo = 0, hi = p.B - 1;
     while (lo < hi) {
@@ -194,7 +202,21 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanParams p) {
     const int chunks = attn_chunks(len);
     const int li = t - base[lo];
     const int h = li / chunks, c = li - h * chunks;
-    p.items[t] = encode_item(s_cu[b], len, h, c);
+    // The class: positions [c0, c1) with this chunk count (counts fall with position).
+    int c0 = 0, c1 = lo;
+    while (c0 < c1) {
+      const int mid = (c0 + c1) >> 1;
+      if (chunks_at(mid) > chunks) c0 = mid + 1;
+      else c1 = mid;
+    }
+    int e0 = lo + 1, e1 = p.B;
+    while (e0 < e1) {
+      const int mid = (e0 + e1) >> 1;
+      if (chunks_at(mid) >= chunks) e0 = mid + 1;
+      else e1 = mid;
+    }
+    const long long slot = attn_item_slot(base[c0], (e0 - c0) * p.H, chunks, (lo - c0) * p.H + h, c);
+    p.items[slot] = encode_item(s_cu[b], len, h, c);
   }
   if (tid < 32) p.hdr->zero_row[tid] = 0u;
   if (tid == 0) write_plan_header(p.hdr, n_items, p.B, p.H, p.max_seqlen, p.total);
@@ -223,7 +245,7 @@ __device__ __forceinline__ Item decode_item(const AttnParams& p, int2 raw) {
   it.chunk = static_cast<int>(y & 0x1FFu);
   const bool ok = raw.x >= 0 && it.len <= p.max_seqlen &&
                   static_cast<long long>(raw.x) + it.len <= p.total && it.h < p.H &&
-                  it.chunk * kAttnQTile < it.len;
+                  it.chunk < attn_chunks(it.len);
   if (!ok) {
     if (threadIdx.x == 0) atomicOr(p.status, DORA_DEV_CU_SEQLENS);
     it.seq0 = 0;
@@ -400,8 +422,9 @@ __device__ __forceinline__ void q_dma(const char* qbase, int nq, uint32_t row_by
 // The queries of an item's chunk into the query buffer (nothing for an empty item).
 __device__ __forceinline__ void q_chunk_dma(const AttnParams& p, const Item& it, long long row_elems,
                                             uint32_t row_bytes, uint16_t* Qd) {
-  const int q0 = it.chunk * kAttnQTile;
-  const int nq = min(kAttnQTile, it.len - q0);
+  const int cs = attn_chunk_size(it.len);
+  const int q0 = it.chunk * cs;
+  const int nq = min(cs, it.len - q0);
   if (nq > 0) q_dma(head_base(p.q, static_cast<long long>(it.seq0) + q0, row_elems, it.h), nq, row_bytes, Qd);
 }
 
@@ -702,8 +725,9 @@ __device__ __forceinline__ bool attn_stage(const KernelCtx& c, Sched& s, const c
   const Item cur = s.cur;
   const int kb0 = s.sb * kKRes;
   const int nk = min(kKRes, cur.len - kb0);
-  const int q0 = cur.chunk * kAttnQTile;
-  const int nq = min(kAttnQTile, cur.len - q0);
+  const int cs = attn_chunk_size(cur.len);
+  const int q0 = cur.chunk * cs;
+  const int nq = min(cs, cur.len - q0);
   const bool act0 = tile_q(wave, 0) < nq;
   const bool act1 = kTilesPerWave > 1 && tile_q(wave, 1) < nq;
   if (s.sb == 0) {
@@ -916,8 +940,9 @@ __global__ __launch_bounds__(kF32Threads) void attn_fwd_f32_kernel(AttnParams p)
     const Item it = decode_item(p, p.items[ticket]);
     const long long seq0 = it.seq0;
     const int len = it.len;
-    const int q0 = it.chunk * kAttnQTile + wave * 32;
-    const int qend = min(len, (it.chunk + 1) * kAttnQTile);  // this item's queries end here
+    const int cs = attn_chunk_size(len);
+    const int q0 = it.chunk * cs + wave * 32;
+    const int qend = min(len, (it.chunk + 1) * cs);  // this item's queries end here
     const bool active = q0 < qend;
 
     float qf[2][16];

@@ -26,19 +26,65 @@ ITEMS_OFF = HDR_BYTES
 QUEUE_INTS = [64 + 32 * q for q in range(8)]   # one counter per 128-byte line
 
 
+SUB_QUEUES = 8      # item i is served by sub-queue i % 8
+
+
+def n_chunks(k):
+    return (int(k) + Q_TILE - 1) // Q_TILE
+
+
+def item_slot(base, groups, ch, gi, c):
+    """Slot of chunk c of group gi in a class of `groups` (sequence, head)
+    groups of ch chunks starting at `base`: full blocks of 8 groups put a
+    group's chunks 8 slots apart (one sub-queue, consecutive tickets), the
+    groups past the last full block follow chunk after chunk."""
+    full = groups // SUB_QUEUES * SUB_QUEUES
+    if gi < full:
+        return base + ch * (gi // SUB_QUEUES) * SUB_QUEUES + c * SUB_QUEUES + gi % SUB_QUEUES
+    return base + ch * full + (gi - full) * ch + c
+
+
 def expected_items(keep, H, max_seqlen):
-    """Plan items in queue order as int2 pairs (first row, len << 17 | h << 9 | chunk)."""
+    """Plan items in slot order as int2 pairs (first row, len << 17 | h << 9 | chunk):
+    sequences in queue order (longer first, then lower index), grouped in
+    classes of equal chunk count, each (sequence, head) group's chunks placed
+    by item_slot."""
     keep = np.asarray(keep, np.int64)
     cu = np.concatenate([[0], np.cumsum(keep)])
     order = sorted(range(len(keep)), key=lambda b: (-keep[b], b))
-    rows = []
-    for b in order:
-        k = int(keep[b])
-        ch = (k + Q_TILE - 1) // Q_TILE
-        for h in range(H):
-            for c in range(ch):
-                rows.append((int(cu[b]), (k << 17) | (h << 9) | c))
-    return np.array(rows, np.int64).reshape(-1, 2)
+    total = H * sum(n_chunks(k) for k in keep)
+    out = np.full((total, 2), -1, np.int64)
+    base = 0
+    for ch in sorted({n_chunks(k) for k in keep}, reverse=True):
+        members = [b for b in order if n_chunks(keep[b]) == ch]
+        groups = len(members) * H
+        for rank, b in enumerate(members):
+            k = int(keep[b])
+            for h in range(H):
+                for c in range(ch):
+                    out[item_slot(base, groups, ch, rank * H + h, c)] = (int(cu[b]), (k << 17) | (h << 9) | c)
+        base += groups * ch
+    assert np.all(out >= 0)
+    return out
+
+
+def assert_groups_share_a_subqueue(items):
+    """Every (sequence, head) group's chunks sit in one sub-queue at
+    consecutive tickets (slots 8 apart), except at most 7 groups per class
+    past its last full block of 8, whose chunks are adjacent."""
+    slots = {}
+    for i, (row, y) in enumerate(items.tolist()):
+        slots.setdefault((row, (y >> 9) & 0xFF), []).append((y & 0x1FF, i))
+    tail = {}
+    for (row, h), v in slots.items():
+        idx = [i for _, i in sorted(v)]
+        if len(idx) == 1:
+            continue
+        steps = set(np.diff(idx).tolist())
+        assert steps in ({SUB_QUEUES}, {1}), (row, h, idx)
+        if steps == {1}:
+            tail[len(idx)] = tail.get(len(idx), 0) + 1
+    assert all(n < SUB_QUEUES for n in tail.values()), tail
 
 
 def read_plan(ws):
@@ -78,6 +124,7 @@ def test_fused_plan_matches_oracle_and_separate_plan(gpu, name):
 
     hdr, n, items = read_plan(ws)
     assert np.array_equal(items, expected_items(r.keep, w.H, w.N))
+    assert_groups_share_a_subqueue(items)
 
     q, k, v = (to_dev(a) for a in (r.q, r.k, r.v))
     st_t = torch.zeros(1, dtype=torch.int32, device="cuda")
@@ -88,6 +135,11 @@ def test_fused_plan_matches_oracle_and_separate_plan(gpu, name):
     torch.cuda.synchronize()
     assert int(st_t.item()) == 0
     assert np.array_equal(to_host_bits(out_fused), to_host_bits(out_sep))
+    # the plan kernel's plan: the same items, the same class and sub-queue placement
+    _, n2, items2 = read_plan(ws2)
+    assert n2 == n and sorted(map(tuple, items2.tolist())) == sorted(map(tuple, items.tolist()))
+    assert np.all(np.diff([n_chunks(k) for k in (items2[:, 1] >> 17)]) <= 0)
+    assert_groups_share_a_subqueue(items2)
     # and against the oracle, every element
     want = oracle.varlen_attn(r.q, r.k, r.v, cu_o, w.dtype)
     assert_attn_close(widen(out_fused), want, w.dtype, name)
@@ -183,9 +235,10 @@ def test_fused_plan_large_batch(gpu):
     hdr, n, items = read_plan(ws)
     want = expected_items(r.keep, H, N)
     assert n == len(want)
-    lens = items[:, 1] >> 17
-    assert np.all(np.diff(lens) <= 0)
+    chunks = [n_chunks(k) for k in (items[:, 1] >> 17)]
+    assert np.all(np.diff(chunks) <= 0)                       # classes of equal chunk count, longest first
     assert sorted(map(tuple, items.tolist())) == sorted(map(tuple, want.tolist()))
+    assert_groups_share_a_subqueue(items)
     q, k, v = W.random_qkv(rng, r.keep, H, "bf16")
     tq, tk, tv = to_dev(q), to_dev(k), to_dev(v)
     st_t = torch.zeros(1, dtype=torch.int32, device="cuda")
