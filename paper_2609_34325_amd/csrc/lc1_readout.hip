@@ -6,19 +6,20 @@
 // fused with the backbone's final LayerNorm, so each packed row is read once
 // and only B x 2C values are written.
 //
-// One workgroup per image (16 waves; 8 for the widest rows).  Wave w takes
-// rows r0 + w, r0 + w + 16, ..., two per step (one for wide rows), with the
-// next step's rows in flight while it reduces the current ones.  Loads are
-// unconditional from clamped, in-bounds addresses and the loop body is one
-// basic block, so the compiler counts the loads in order instead of waiting
-// for all of them; values past the sequence or the row are masked where they
-// are used.  A lane holds up to VPL 16-byte pieces of a row; the row's mean
-// and biased variance come from two wave reductions (DPP butterflies and row
-// swaps; the variance from centred values).  CLS leaves the loop normalised,
-// (x - mean) / sqrt(var + eps), into LDS; for the other rows each lane
-// accumulates the same quantity.  The waves' sums meet in LDS in two rounds
-// and are added in wave order (the result does not depend on timing); then
-// gamma * sum / (n - 1) + beta is the mean of the normalised rows and
+// One workgroup of 8 waves per image.  A row of P 16-byte pieces is held by
+// a group of L = 16, 32 or 64 lanes, up to 4 pieces a lane, the shape that
+// leaves the fewest lanes idle (768 bf16 channels: 32 lanes of 3 pieces, two
+// rows per wave).  The groups are row slots taking every (slots)-th row, with
+// the next row in flight while they reduce the current one.  Loads are
+// unconditional from clamped, in-bounds addresses; a row past the end gets
+// weight 0.  A row's sum comes from bf16 dot products with (1, 1) on the
+// packed values, its mean and biased variance (from centred values) from
+// group reductions (DPP butterflies and row swaps), and 1 / sqrt(var + eps)
+// from the hardware reciprocal square root.  CLS is normalised apart, into
+// LDS; for the other rows each lane accumulates (x - mean) / sqrt(var + eps).
+// The groups' sums are merged by row swaps and the waves' sums meet in LDS
+// in two rounds, added in wave order (the result does not depend on timing);
+// then gamma * sum / (n - 1) + beta is the mean of the normalised rows and
 // gamma * cls + beta the normalised CLS.
 //
 // Small batches (a caller workspace given): the rows of an image are split
@@ -35,7 +36,7 @@
 namespace dora {
 namespace {
 
-constexpr int kLCCombine = 8;  // waves whose partial sums meet in LDS (LDS holds kLCCombine x C floats)
+constexpr int kLCCombine = 4;  // waves whose partial sums meet in LDS (LDS holds kLCCombine x C floats)
 constexpr int kLCMaxRowBytes = 4096;  // 64 lanes x 4 pieces of 16 bytes
 constexpr int kLCMaxSplit = 8;        // workgroups per image with a workspace
 constexpr int32_t kLCMaxB = 1 << 24;  // images per call (B x kLCMaxSplit workgroups fit a grid)
@@ -79,42 +80,93 @@ struct Piece<false> {
   }
 };
 
-// Sum over the wave, every lane receiving the same value: butterflies inside
-// each 16-lane row by DPP (quad permutes, half-row and row mirrors), then the
-// row swaps v_permlane16_swap and v_permlane32_swap.  Each step adds two
-// values that every lane of the pair sees in the same two operands, so all
-// lanes agree bit for bit.
-__device__ __forceinline__ float wave_total(float v) {
+// Sum over a group of L lanes (16, 32 or 64), every lane of the group
+// receiving the same value: butterflies inside each 16-lane row by DPP
+// (quad permutes, half-row and row mirrors), then for wider groups the row
+// swaps v_permlane16_swap and v_permlane32_swap.  Each step adds two values
+// that every lane of the pair sees in the same two operands, so all lanes of
+// a group agree bit for bit.
+template <int L>
+__device__ __forceinline__ float group_total(float v) {
   v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
   v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
   v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x141, 0xF, 0xF, false));  // row_half_mirror
   v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x140, 0xF, 0xF, false));  // row_mirror
-  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-  const auto c = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return __uint_as_float(c[0]) + __uint_as_float(c[1]);
+  if constexpr (L >= 32) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  }
+  if constexpr (L >= 64) {
+    const auto c = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(c[0]) + __uint_as_float(c[1]);
+  }
+  return v;
 }
 
-// Shape of the work of one workgroup for rows of VPL pieces of E values per
-// lane: two rows per step on 16 waves, or one on 8 waves for the widest rows
-// (within the register budget of the occupancy).
-template <int VPL, int E>
-struct Flight {
-  static constexpr int kRows = VPL * E > 16 || VPL >= 4 ? 1 : 2;
-  static constexpr int kWaves = VPL * E > 16 || VPL >= 4 ? 8 : 16;
-};
+// Sum of the value a lane holds and the values the lanes at the same place
+// in the wave's other L-lane groups hold (the same channels of other rows).
+template <int L>
+__device__ __forceinline__ float merge_groups(float v) {
+  if constexpr (L <= 16) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  }
+  if constexpr (L <= 32) {
+    const auto c = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(c[0]) + __uint_as_float(c[1]);
+  }
+  return v;
+}
 
-template <int VPL, bool BF16>
-__global__ __launch_bounds__((Flight<VPL, Piece<BF16>::kElems>::kWaves * 64)) void lc1_readout_kernel(LCParams p) {
+constexpr int kLCWaves = 8;
+constexpr int kLCThreads = kLCWaves * 64;
+static_assert(kLCWaves == 2 * kLCCombine, "two combine rounds");
+constexpr int kLCChanPerThread = 4;  // output channels per thread
+static_assert(kLCMaxRowBytes / 2 <= kLCChanPerThread * kLCThreads, "every channel has a thread");
+
+// LDS slot of element e of piece v (channel v * E + e) in a partial-sum
+// buffer of C = P * E floats: the elements are stored in 16-byte quads, quad
+// e / 4 of every piece first, so the lanes of a group, which hold consecutive
+// pieces, store and load consecutive quads (no bank conflicts).
+template <int E>
+__device__ __forceinline__ int quad_slot(int P, int v, int e) {
+  return ((e >> 2) * P + v) * 4 + (e & 3);
+}
+
+// Sum of the 2 E bf16 or E fp32 values of a piece, before unpacking: one
+// dot product with (1, 1) per pair of bf16 values.
+template <bool BF16>
+__device__ __forceinline__ float piece_sum(uint4 v, float s) {
+  if constexpr (BF16) {
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    const bf16x2 one = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, v.x), one, s, false);
+    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, v.y), one, s, false);
+    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, v.z), one, s, false);
+    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, v.w), one, s, false);
+    return s;
+  } else {
+    return s + __uint_as_float(v.x) + __uint_as_float(v.y) + __uint_as_float(v.z) + __uint_as_float(v.w);
+  }
+}
+
+// One workgroup per image part (8 waves).  A row of P 16-byte pieces is held
+// by a group of L lanes, VPL pieces a lane (L * VPL >= P, chosen by the host
+// to leave few lanes idle: 96-piece rows, DeiT-B and DINOv2-B in bf16, are two
+// rows per wave on 32-lane groups with three pieces a lane); PAD says that
+// some lanes' last piece lies past the row's end.  The 64 / L groups of the
+// 8 waves are the row slots: slot g takes rows r0 + g, r0 + g + slots, ...,
+// with its next row in flight while it reduces the current one.
+template <int L, int VPL, bool PAD, bool BF16>
+__global__ __launch_bounds__(kLCThreads) void lc1_readout_kernel(LCParams p) {
   constexpr int E = Piece<BF16>::kElems;
-  constexpr int R = Flight<VPL, E>::kRows;
-  constexpr int kLCWaves = Flight<VPL, E>::kWaves;
-  constexpr int kLCThreads = kLCWaves * 64;
-  static_assert(kLCWaves == kLCCombine || kLCWaves == 2 * kLCCombine, "two combine rounds at most");
+  constexpr int kGroups = 64 / L;
+  constexpr int kSlots = kLCWaves * kGroups;  // rows per step
   extern __shared__ float s_acc[];  // [kLCCombine][C], then the normalised CLS row [C]
   float* s_cls = s_acc + kLCCombine * p.C;
   const int b = blockIdx.x / p.split, part_id = blockIdx.x - b * p.split;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int grp = lane / L, t = lane % L;
   const int lo = p.cu[b], hi = p.cu[b + 1];
   if (!(lo >= 0 && hi > lo && hi <= p.total && (b > 0 || lo == 0))) {
     if (threadIdx.x == 0 && part_id == 0) {
@@ -126,7 +178,52 @@ __global__ __launch_bounds__((Flight<VPL, Piece<BF16>::kElems>::kWaves * 64)) vo
   // This workgroup's rows [rlo, rhi) of the image; CLS (row lo) falls in part 0.
   const int per_part = (hi - lo + p.split - 1) / p.split;
   const int rlo = min(hi, lo + part_id * per_part), rhi = min(hi, rlo + per_part);
-  // Per lane: the sum over this wave's visual rows of (x - mean) * rstd for
+  const float inv_c = 1.0f / static_cast<float>(p.C);
+  // Only a lane's last piece can lie past the row's end (L * (VPL - 1) < P):
+  // it reads the row's last piece and is masked to zero (PAD only).
+  const bool last_ok = !PAD || t + L * (VPL - 1) < p.vpr;
+  const uint32_t last_mask = last_ok ? ~0u : 0u;
+  const int last_piece = PAD ? min(t + L * (VPL - 1), p.vpr - 1) : t + L * (VPL - 1);
+  // Loads are unconditional from clamped (in-bounds) addresses, so the
+  // compiler counts them in order instead of waiting for all of them.  A row
+  // past this part's end reads the part's last row and is given weight 0.  An
+  // empty part (rlo == rhi == hi) reads the image's last row.
+  const int last_row = min(max(rhi, rlo + 1), hi) - 1;
+  auto load = [&](int r, uint4 (&dst)[VPL]) {
+    const uint4* row = p.x + static_cast<int64_t>(min(r, last_row)) * p.vpr;
+#pragma unroll
+    for (int i = 0; i < VPL; ++i) dst[i] = row[i + 1 < VPL ? t + L * i : last_piece];
+  };
+  // (x - mean) of the row's values this lane holds, and the row's
+  // 1 / sqrt(var + eps) (biased variance from the centred values).
+  auto normalise = [&](uint4 (&src)[VPL], float (&d)[VPL][E]) {
+    if constexpr (PAD) {
+      uint4& w = src[VPL - 1];
+      w = make_uint4(w.x & last_mask, w.y & last_mask, w.z & last_mask, w.w & last_mask);
+    }
+    float s = 0.0f;
+#pragma unroll
+    for (int i = 0; i < VPL; ++i) s = piece_sum<BF16>(src[i], s);
+    const float mu = group_total<L>(s) * inv_c;
+    float ss = 0.0f;
+#pragma unroll
+    for (int i = 0; i < VPL; ++i) {
+      Piece<BF16>::unpack(src[i], d[i]);
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        d[i][e] -= mu;
+        if (!PAD || i + 1 < VPL) ss += d[i][e] * d[i][e];
+      }
+    }
+    if constexpr (PAD) {
+      float sl = 0.0f;
+#pragma unroll
+      for (int e = 0; e < E; ++e) sl += d[VPL - 1][e] * d[VPL - 1][e];
+      ss += last_ok ? sl : 0.0f;
+    }
+    return __builtin_amdgcn_rsqf(group_total<L>(ss) * inv_c + p.eps);
+  };
+  // Per lane: the sum over this slot's visual rows of (x - mean) * rstd for
   // its channels; gamma and beta are applied once at the end (the affine map
   // commutes with the mean).
   float acc[VPL][E];
@@ -134,137 +231,114 @@ __global__ __launch_bounds__((Flight<VPL, Piece<BF16>::kElems>::kWaves * 64)) vo
   for (int i = 0; i < VPL; ++i)
 #pragma unroll
     for (int e = 0; e < E; ++e) acc[i][e] = 0.0f;
-  const float inv_c = 1.0f / static_cast<float>(p.C);
-  // Wave w takes rows lo + w + j * kLCWaves, R of them per step, with two
-  // buffers: the next step's rows are in flight while the current ones are
-  // reduced.  Loads are unconditional from clamped (in-bounds) addresses, so
-  // the compiler can count them in order instead of waiting for all of them;
-  // values past the sequence or the row are masked to zero where they are used.
-  constexpr int kStep = R * kLCWaves;
-  // An empty range (rlo == rhi == hi) reads the image's last row, masked.
-  const int last_row = min(max(rhi, rlo + 1), hi) - 1, last_vec = p.vpr - 1;
-  auto load = [&](int r0, uint4 (&dst)[R][VPL]) {
+  auto process = [&](int r, uint4 (&src)[VPL]) {
+    float d[VPL][E];
+    const float rs = normalise(src, d);
+    const float w = r < rhi ? rs : 0.0f;
 #pragma unroll
-    for (int q = 0; q < R; ++q)
+    for (int i = 0; i < VPL; ++i)
 #pragma unroll
-      for (int i = 0; i < VPL; ++i) {
-        const int r = min(r0 + q * kLCWaves, last_row), v = min(lane + 64 * i, last_vec);
-        dst[q][i] = p.x[static_cast<int64_t>(r) * p.vpr + v];
-      }
+      for (int e = 0; e < E; ++e) acc[i][e] += d[i][e] * w;
   };
-  auto process = [&](int r0, const uint4 (&src)[R][VPL]) {
-    float x[R][VPL][E], s[R], ss[R];
+  // The loop takes the visual rows, from lo + 1 in part 0.
+  const int r0 = part_id == 0 ? lo + 1 : rlo;
+  // Rounds of two steps; the loop runs on the wave's first row (uniform), and
+  // the second step of a round is skipped when no row of the wave is left.
+  // The empty asm statements, memory barriers to the compiler, keep loads
+  // where they are written instead of next to their use.
+  uint4 buf_a[VPL], buf_b[VPL];
+  int rw = r0 + wave * kGroups;
+  load(rw + grp, buf_a);
+  // gamma and beta of this thread's output channels (c = tid + 512 k),
+  // loaded now so that their latency overlaps the rows' loads.
+  float gam[kLCChanPerThread], bet[kLCChanPerThread];
 #pragma unroll
-    for (int q = 0; q < R; ++q) {
-      s[q] = 0.0f;
-      const bool row_in = r0 + q * kLCWaves < rhi;
-#pragma unroll
-      for (int i = 0; i < VPL; ++i) {
-        const uint32_t mk = (row_in && lane + 64 * i < p.vpr) ? ~0u : 0u;
-        const uint4 t = src[q][i];
-        Piece<BF16>::unpack(make_uint4(t.x & mk, t.y & mk, t.z & mk, t.w & mk), x[q][i]);
-#pragma unroll
-        for (int e = 0; e < E; ++e) s[q] += x[q][i][e];
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < R; ++q) s[q] = wave_total(s[q]);
-#pragma unroll
-    for (int q = 0; q < R; ++q) {
-      const float mu = s[q] * inv_c;
-      ss[q] = 0.0f;
-#pragma unroll
-      for (int i = 0; i < VPL; ++i) {
-        const float keep = lane + 64 * i < p.vpr ? 1.0f : 0.0f;
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-          const float d = (x[q][i][e] - mu) * keep;
-          x[q][i][e] = d;
-          ss[q] += d * d;
-        }
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < R; ++q) ss[q] = wave_total(ss[q]);
-#pragma unroll
-    for (int q = 0; q < R; ++q) {
-      // a row past the sequence has d = 0; its scale is kept finite (1) so it
-      // adds exactly nothing, without a branch
-      const int r = r0 + q * kLCWaves;
-      const float pad = r < rhi ? 0.0f : 1.0f;
-      const float rstd = 1.0f / sqrtf(ss[q] * inv_c + p.eps + pad);
-      if (r == lo) {  // CLS: kept in LDS, gamma and beta applied at the end
-#pragma unroll
-        for (int i = 0; i < VPL; ++i) {
-          const int v = lane + 64 * i;
-          if (v < p.vpr)
-#pragma unroll
-            for (int e = 0; e < E; ++e) s_cls[v * E + e] = x[q][i][e] * rstd;
-        }
-      } else {
-#pragma unroll
-        for (int i = 0; i < VPL; ++i)
-#pragma unroll
-          for (int e = 0; e < E; ++e) acc[i][e] += x[q][i][e] * rstd;
-      }
-    }
-  };
-  uint4 buf_a[R][VPL], buf_b[R][VPL];
-  int r0 = rlo + wave;
-  load(r0, buf_a);
-  // Whole rounds of two steps, one basic block (so no load is moved next to
-  // its use); a step past the sequence sees masked rows and adds nothing.
-  for (; r0 < rhi; r0 += 2 * kStep) {
-    load(r0 + kStep, buf_b);
-    process(r0, buf_a);
-    load(r0 + 2 * kStep, buf_a);
-    process(r0 + kStep, buf_b);
+  for (int k = 0; k < kLCChanPerThread; ++k) {
+    const int c = min(static_cast<int>(threadIdx.x) + k * kLCThreads, p.C - 1);
+    gam[k] = p.gamma[c];
+    bet[k] = p.beta[c];
   }
-  // Waves kLCCombine.. hand their sums to waves 0.., which add them to their
-  // own; the kLCCombine sums are then added in wave order.
-  float* mine = s_acc + (wave % kLCCombine) * p.C;
-  if (wave >= kLCCombine) {
+  asm volatile("" ::: "memory");
+  // CLS (part 0): normalised by wave 0 into LDS, its loads issued after the
+  // loop's first ones.
+  if (part_id == 0 && wave == 0) {
+    uint4 c[VPL];
+    load(lo, c);
+    float d[VPL][E];
+    const float rs = normalise(c, d);
+    if (grp == 0) {
 #pragma unroll
-    for (int i = 0; i < VPL; ++i) {
-      const int v = lane + 64 * i;
-      if (v < p.vpr)
+      for (int i = 0; i < VPL; ++i)
+        if (i + 1 < VPL || last_ok)
 #pragma unroll
-        for (int e = 0; e < E; ++e) mine[v * E + e] = acc[i][e];
+          for (int e = 0; e < E; ++e) s_cls[quad_slot<E>(p.vpr, t + L * i, e)] = d[i][e] * rs;
     }
+  }
+  for (; rw < rhi; rw += 2 * kSlots) {
+    load(rw + grp + kSlots, buf_b);
+    asm volatile("" ::: "memory");
+    process(rw + grp, buf_a);
+    load(rw + grp + 2 * kSlots, buf_a);
+    if (rw + kSlots < rhi) process(rw + grp + kSlots, buf_b);
+  }
+  // The wave's groups hold the same channels of different rows: merge them,
+  // then the waves' sums meet in LDS in two rounds and are added in wave
+  // order (the result does not depend on timing).
+#pragma unroll
+  for (int i = 0; i < VPL; ++i)
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[i][e] = merge_groups<L>(acc[i][e]);
+  float* mine = s_acc + (wave % kLCCombine) * p.C;
+  if (wave >= kLCCombine && grp == 0) {
+#pragma unroll
+    for (int i = 0; i < VPL; ++i)
+      if (i + 1 < VPL || last_ok)
+#pragma unroll
+        for (int e = 0; e < E; ++e) mine[quad_slot<E>(p.vpr, t + L * i, e)] = acc[i][e];
   }
   __syncthreads();
-  if (wave < kLCCombine) {
+  if (wave < kLCCombine && grp == 0) {
 #pragma unroll
-    for (int i = 0; i < VPL; ++i) {
-      const int v = lane + 64 * i;
-      if (v < p.vpr)
+    for (int i = 0; i < VPL; ++i)
+      if (i + 1 < VPL || last_ok)
 #pragma unroll
-        for (int e = 0; e < E; ++e) mine[v * E + e] = (kLCWaves > kLCCombine ? mine[v * E + e] : 0.0f) + acc[i][e];
-    }
+        for (int e = 0; e < E; ++e) {
+          const int q = quad_slot<E>(p.vpr, t + L * i, e);
+          mine[q] = mine[q] + acc[i][e];
+        }
   }
   __syncthreads();
   const float inv_n = 1.0f / static_cast<float>(hi - lo - 1);
   float* o = p.out + static_cast<int64_t>(b) * 2 * p.C + p.C;
+  // Channel c is element c % E of piece c / E.
+  auto slot_of = [&](int c) { return quad_slot<E>(p.vpr, c / E, c % E); };
   if (p.split == 1) {
-    for (int c = threadIdx.x; c < p.C; c += kLCThreads) {
-      float t = 0.0f;
 #pragma unroll
-      for (int w = 0; w < kLCCombine; ++w) t += s_acc[w * p.C + c];
-      const float gc = p.gamma[c], bc = p.beta[c];
-      o[c] = hi - lo > 1 ? t * inv_n * gc + bc : __builtin_nanf("");
-      o[c - p.C] = s_cls[c] * gc + bc;
+    for (int k = 0; k < kLCChanPerThread; ++k) {
+      const int c = threadIdx.x + k * kLCThreads;
+      if (c >= p.C) break;
+      const int q = slot_of(c);
+      float tsum = 0.0f;
+#pragma unroll
+      for (int w = 0; w < kLCCombine; ++w) tsum += s_acc[w * p.C + q];
+      o[c] = hi - lo > 1 ? tsum * inv_n * gam[k] + bet[k] : __builtin_nanf("");
+      o[c - p.C] = s_cls[q] * gam[k] + bet[k];
     }
     return;
   }
   // Several workgroups per image: each writes its sum, part 0 the CLS half;
   // lc1_combine_kernel, the next launch, adds the sums.
   float* mine_part = p.part + (static_cast<int64_t>(b) * p.split + part_id) * p.C;
-  for (int c = threadIdx.x; c < p.C; c += kLCThreads) {
-    float t = 0.0f;
 #pragma unroll
-    for (int w = 0; w < kLCCombine; ++w) t += s_acc[w * p.C + c];
-    mine_part[c] = t;
-    if (part_id == 0) o[c - p.C] = s_cls[c] * p.gamma[c] + p.beta[c];
+  for (int k = 0; k < kLCChanPerThread; ++k) {
+    const int c = threadIdx.x + k * kLCThreads;
+    if (c >= p.C) break;
+    const int q = slot_of(c);
+    float tsum = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kLCCombine; ++w) tsum += s_acc[w * p.C + q];
+    mine_part[c] = tsum;
+    if (part_id == 0) o[c - p.C] = s_cls[q] * gam[k] + bet[k];
   }
 }
 
@@ -292,15 +366,45 @@ __global__ __launch_bounds__(256) void lc1_combine_kernel(LCParams p) {
                                                                   : __builtin_nanf("");
 }
 
-template <int VPL, bool BF16>
+template <int L, int VPL, bool BF16>
 hipError_t launch_lc1(const LCParams& p, hipStream_t stream) {
   const size_t lds = static_cast<size_t>(kLCCombine + 1) * p.C * sizeof(float);
-  constexpr int threads = Flight<VPL, Piece<BF16>::kElems>::kWaves * 64;
-  hipLaunchKernelGGL((lc1_readout_kernel<VPL, BF16>), dim3(p.B * p.split), dim3(threads), lds, stream, p);
+  auto kernel = L * VPL == p.vpr ? lc1_readout_kernel<L, VPL, false, BF16> : lc1_readout_kernel<L, VPL, true, BF16>;
+  hipLaunchKernelGGL(kernel, dim3(p.B * p.split), dim3(kLCThreads), lds, stream, p);
   if (p.split > 1) hipLaunchKernelGGL(lc1_combine_kernel, dim3(p.B, (p.C + 255) / 256), dim3(256), 0, stream, p);
   return hipGetLastError();
 }
 
+// Lanes per row group and pieces per lane for rows of P pieces: the fewest
+// idle slots (L * VPL - P), then the widest group; at most 4 pieces a lane.
+void lc1_shape(int P, int* L_out, int* vpl_out) {
+  int best_l = 64, best_v = (P + 63) / 64, best_w = 1 << 30;
+  for (int L : {64, 32, 16}) {
+    const int v = (P + L - 1) / L;
+    if (v > 4) continue;
+    const int waste = L * v - P;
+    if (waste < best_w) {
+      best_w = waste;
+      best_l = L;
+      best_v = v;
+    }
+  }
+  *L_out = best_l;
+  *vpl_out = best_v;
+}
+
+template <bool BF16>
+hipError_t launch_lc1_shape(const LCParams& p, hipStream_t st) {
+  int L, v;
+  lc1_shape(p.vpr, &L, &v);
+#define DORA_LC1_CASE(LL, VV) \
+  if (L == LL && v == VV) return launch_lc1<LL, VV, BF16>(p, st);
+  DORA_LC1_CASE(64, 1) DORA_LC1_CASE(64, 2) DORA_LC1_CASE(64, 3) DORA_LC1_CASE(64, 4)
+  DORA_LC1_CASE(32, 1) DORA_LC1_CASE(32, 2) DORA_LC1_CASE(32, 3) DORA_LC1_CASE(32, 4)
+  DORA_LC1_CASE(16, 1) DORA_LC1_CASE(16, 2) DORA_LC1_CASE(16, 3) DORA_LC1_CASE(16, 4)
+#undef DORA_LC1_CASE
+  return hipErrorInvalidValue;
+}
 
 }  // namespace
 }  // namespace dora
@@ -333,13 +437,6 @@ extern "C" int dora_lc1_readout(const void* x, const int32_t* cu_seqlens, int64_
     p.part = static_cast<float*>(workspace);
   }
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const int vpl = (p.vpr + 63) / 64;
-  hipError_t err;
-  if (dtype == DORA_BF16) {
-    err = vpl <= 1 ? launch_lc1<1, true>(p, st) : vpl <= 2 ? launch_lc1<2, true>(p, st) : launch_lc1<4, true>(p, st);
-  } else {
-    err = vpl <= 1 ? launch_lc1<1, false>(p, st) : vpl <= 2 ? launch_lc1<2, false>(p, st)
-                                                          : launch_lc1<4, false>(p, st);
-  }
+  const hipError_t err = dtype == DORA_BF16 ? launch_lc1_shape<true>(p, st) : launch_lc1_shape<false>(p, st);
   return err == hipSuccess ? DORA_OK : DORA_ERR_HIP;
 }
