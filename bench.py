@@ -639,6 +639,9 @@ def main() -> int:
     ap.add_argument("--no-peaks", action="store_true", help="skip measuring the copy and MFMA peaks")
     ap.add_argument("--no-adjacent", action="store_true",
                     help="skip the adjacent entry points (residual, actor, LC1, FLOPs, Plackett-Luce)")
+    ap.add_argument("--no-large-batch", action="store_true",
+                    help="skip the select/pack runs at 8192 and 65536 images (their launches would mix "
+                         "into the per-launch counter averages of the headline select/pack)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="before timing, run one plain device copy of MIB MiB (a reference dispatch "
                          "for scaling hardware byte counters)")
@@ -975,7 +978,7 @@ def adjacent_legs(head: ConfigRun, cold_sets, args, torch, dora, stream, phases)
     # the gather (DeiT-B's keep rule; scores and keep counts from the seeded
     # host streams, token rows filled on the device from a seeded generator).
     large = []
-    for Bl, C in ((8192, 768), (65536, 192)):
+    for Bl, C in (() if args.no_large_batch else ((8192, 768), (65536, 192))):
         wl = W.Workload(f"{w.name}_B{Bl}", w.seed, Bl, w.N, C // W.HEAD_DIM, w.dtype, w.keep_rule)
         rl = W.generate(wl, parts=("keep", "scores"))[0]
         gen = torch.Generator(device="cuda")

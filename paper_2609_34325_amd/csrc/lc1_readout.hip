@@ -121,16 +121,14 @@ __device__ __forceinline__ float merge_groups(float v) {
 constexpr int kLCWaves = 8;
 constexpr int kLCThreads = kLCWaves * 64;
 static_assert(kLCWaves == 2 * kLCCombine, "two combine rounds");
-constexpr int kLCChanPerThread = 4;  // output channels per thread
-static_assert(kLCMaxRowBytes / 2 <= kLCChanPerThread * kLCThreads, "every channel has a thread");
+static_assert(kLCMaxRowBytes / 2 <= 4 * kLCThreads, "every quad of output channels has a thread");
 
-// LDS slot of element e of piece v (channel v * E + e) in a partial-sum
-// buffer of C = P * E floats: the elements are stored in 16-byte quads, quad
-// e / 4 of every piece first, so the lanes of a group, which hold consecutive
-// pieces, store and load consecutive quads (no bank conflicts).
-template <int E>
-__device__ __forceinline__ int quad_slot(int P, int v, int e) {
-  return ((e >> 2) * P + v) * 4 + (e & 3);
+// Partial-sum buffers of C = P * E floats in LDS hold 16-byte quads: quad h
+// (elements 4h .. 4h + 3) of piece v at quad index h * P + v.  The lanes of a
+// group, which hold consecutive pieces, store and load consecutive quads
+// (16-byte accesses without bank conflicts).
+__device__ __forceinline__ float4* lds_quad(float* base, int P, int v, int h) {
+  return reinterpret_cast<float4*>(base) + (h * P + v);
 }
 
 // Sum of the 2 E bf16 or E fp32 values of a piece, before unpacking: one
@@ -249,14 +247,15 @@ __global__ __launch_bounds__(kLCThreads) void lc1_readout_kernel(LCParams p) {
   uint4 buf_a[VPL], buf_b[VPL];
   int rw = r0 + wave * kGroups;
   load(rw + grp, buf_a);
-  // gamma and beta of this thread's output channels (c = tid + 512 k),
-  // loaded now so that their latency overlaps the rows' loads.
-  float gam[kLCChanPerThread], bet[kLCChanPerThread];
+  // gamma and beta of this thread's four output channels 4u .. 4u + 3
+  // (u = thread index; C is a multiple of 4), loaded now so that their
+  // latency overlaps the rows' loads.
+  const int u = threadIdx.x, cq = min(4 * u, p.C - 4);
+  float gam[4], bet[4];
 #pragma unroll
-  for (int k = 0; k < kLCChanPerThread; ++k) {
-    const int c = min(static_cast<int>(threadIdx.x) + k * kLCThreads, p.C - 1);
-    gam[k] = p.gamma[c];
-    bet[k] = p.beta[c];
+  for (int k = 0; k < 4; ++k) {
+    gam[k] = p.gamma[cq + k];
+    bet[k] = p.beta[cq + k];
   }
   asm volatile("" ::: "memory");
   // CLS (part 0): normalised by wave 0 into LDS, its loads issued after the
@@ -271,7 +270,9 @@ __global__ __launch_bounds__(kLCThreads) void lc1_readout_kernel(LCParams p) {
       for (int i = 0; i < VPL; ++i)
         if (i + 1 < VPL || last_ok)
 #pragma unroll
-          for (int e = 0; e < E; ++e) s_cls[quad_slot<E>(p.vpr, t + L * i, e)] = d[i][e] * rs;
+          for (int h = 0; h < E / 4; ++h)
+            *lds_quad(s_cls, p.vpr, t + L * i, h) =
+                make_float4(d[i][4 * h] * rs, d[i][4 * h + 1] * rs, d[i][4 * h + 2] * rs, d[i][4 * h + 3] * rs);
     }
   }
   for (; rw < rhi; rw += 2 * kSlots) {
@@ -294,7 +295,9 @@ __global__ __launch_bounds__(kLCThreads) void lc1_readout_kernel(LCParams p) {
     for (int i = 0; i < VPL; ++i)
       if (i + 1 < VPL || last_ok)
 #pragma unroll
-        for (int e = 0; e < E; ++e) mine[quad_slot<E>(p.vpr, t + L * i, e)] = acc[i][e];
+        for (int h = 0; h < E / 4; ++h)
+          *lds_quad(mine, p.vpr, t + L * i, h) =
+              make_float4(acc[i][4 * h], acc[i][4 * h + 1], acc[i][4 * h + 2], acc[i][4 * h + 3]);
   }
   __syncthreads();
   if (wave < kLCCombine && grp == 0) {
@@ -302,43 +305,43 @@ __global__ __launch_bounds__(kLCThreads) void lc1_readout_kernel(LCParams p) {
     for (int i = 0; i < VPL; ++i)
       if (i + 1 < VPL || last_ok)
 #pragma unroll
-        for (int e = 0; e < E; ++e) {
-          const int q = quad_slot<E>(p.vpr, t + L * i, e);
-          mine[q] = mine[q] + acc[i][e];
+        for (int h = 0; h < E / 4; ++h) {
+          float4* q = lds_quad(mine, p.vpr, t + L * i, h);
+          const float4 o = *q;
+          *q = make_float4(o.x + acc[i][4 * h], o.y + acc[i][4 * h + 1], o.z + acc[i][4 * h + 2],
+                           o.w + acc[i][4 * h + 3]);
         }
   }
   __syncthreads();
-  const float inv_n = 1.0f / static_cast<float>(hi - lo - 1);
-  float* o = p.out + static_cast<int64_t>(b) * 2 * p.C + p.C;
-  // Channel c is element c % E of piece c / E.
-  auto slot_of = [&](int c) { return quad_slot<E>(p.vpr, c / E, c % E); };
+  if (4 * u >= p.C) return;
+  // Quad u holds channels 4u .. 4u + 3: quad h of piece v.
+  const int v = 4 * u / E, h = (4 * u - v * E) / 4;
+  float4 tsum = *lds_quad(s_acc, p.vpr, v, h);
+#pragma unroll
+  for (int w = 1; w < kLCCombine; ++w) {
+    const float4 a = *lds_quad(s_acc + w * p.C, p.vpr, v, h);
+    tsum = make_float4(tsum.x + a.x, tsum.y + a.y, tsum.z + a.z, tsum.w + a.w);
+  }
+  const float ts[4] = {tsum.x, tsum.y, tsum.z, tsum.w};
+  const float4 cl = *lds_quad(s_cls, p.vpr, v, h);
+  const float cls[4] = {cl.x, cl.y, cl.z, cl.w};
+  float* o = p.out + static_cast<int64_t>(b) * 2 * p.C + 4 * u;  // CLS half; the mean half at + C
   if (p.split == 1) {
+    const float inv_n = 1.0f / static_cast<float>(hi - lo - 1);
 #pragma unroll
-    for (int k = 0; k < kLCChanPerThread; ++k) {
-      const int c = threadIdx.x + k * kLCThreads;
-      if (c >= p.C) break;
-      const int q = slot_of(c);
-      float tsum = 0.0f;
-#pragma unroll
-      for (int w = 0; w < kLCCombine; ++w) tsum += s_acc[w * p.C + q];
-      o[c] = hi - lo > 1 ? tsum * inv_n * gam[k] + bet[k] : __builtin_nanf("");
-      o[c - p.C] = s_cls[q] * gam[k] + bet[k];
+    for (int k = 0; k < 4; ++k) {
+      o[k] = cls[k] * gam[k] + bet[k];
+      o[p.C + k] = hi - lo > 1 ? ts[k] * inv_n * gam[k] + bet[k] : __builtin_nanf("");
     }
     return;
   }
   // Several workgroups per image: each writes its sum, part 0 the CLS half;
   // lc1_combine_kernel, the next launch, adds the sums.
-  float* mine_part = p.part + (static_cast<int64_t>(b) * p.split + part_id) * p.C;
+  float* mine_part = p.part + (static_cast<int64_t>(b) * p.split + part_id) * p.C + 4 * u;
 #pragma unroll
-  for (int k = 0; k < kLCChanPerThread; ++k) {
-    const int c = threadIdx.x + k * kLCThreads;
-    if (c >= p.C) break;
-    const int q = slot_of(c);
-    float tsum = 0.0f;
-#pragma unroll
-    for (int w = 0; w < kLCCombine; ++w) tsum += s_acc[w * p.C + q];
-    mine_part[c] = tsum;
-    if (part_id == 0) o[c - p.C] = s_cls[q] * gam[k] + bet[k];
+  for (int k = 0; k < 4; ++k) {
+    mine_part[k] = ts[k];
+    if (part_id == 0) o[k] = cls[k] * gam[k] + bet[k];
   }
 }
 

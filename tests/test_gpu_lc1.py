@@ -48,8 +48,12 @@ def compare(dora, x, cu, gamma, beta, dtype, eps=1e-6):
     return err.max()
 
 
+# Row shapes: 768/384/1024/2048 bf16 and 192/1024 f32 fill their lane groups
+# exactly; 64, 8, 200, 520 and 1000 bf16 and 100 f32 leave some lanes' last
+# piece past the row's end (16-, 32- and 64-lane groups, 1 to 3 pieces a lane).
 @pytest.mark.parametrize("C,dtype", [(768, "bf16"), (1024, "bf16"), (384, "bf16"), (192, "f32"), (64, "bf16"),
-                                     (2048, "bf16"), (1024, "f32"), (8, "bf16")])
+                                     (2048, "bf16"), (1024, "f32"), (8, "bf16"), (200, "bf16"), (520, "bf16"),
+                                     (1000, "bf16"), (100, "f32")])
 def test_ragged_sequences(gpu, C, dtype):
     rng = np.random.default_rng(C)
     lens = np.array([1, 2, 3, 8, 9, 16, 17, 31, 197, 257, 1000])
