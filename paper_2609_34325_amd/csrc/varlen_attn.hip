@@ -49,9 +49,13 @@ constexpr int kThreads = kWaves * 64;
 constexpr int kTilesPerWave = 1;  // 16-query tiles per wave (1 or 2)
 static_assert(kTilesPerWave == 1 || kTilesPerWave == 2, "tiles per wave");
 static_assert(kWaves * kTilesPerWave * 16 >= kAttnQTile && kAttnQTile % 16 == 0, "tile size");
-constexpr int kF32Waves = 8;  // fp32 kernel: 8 waves x 32 queries
+// fp32 kernel: a workgroup of 4 waves takes one part of 64 queries (a
+// 16-query tile per wave) of an item; an item is kF32Parts tickets, so a
+// short batch still spreads over many compute units.
+constexpr int kF32Waves = 4;
 constexpr int kF32Threads = kF32Waves * 64;
-static_assert(kF32Waves * 32 >= kAttnQTile, "fp32 tile size");
+constexpr int kF32PartQ = kF32Waves * 16;
+constexpr int kF32Parts = (kAttnQTile + kF32PartQ - 1) / kF32PartQ;
 constexpr int kKRes = 256;             // keys resident in LDS per stage (bf16)
 // Lane 0 of the last wave talks to the queue: the last wave holds the fewest
 // query tiles of an item, so the queue's latency lands where there is slack.
@@ -901,7 +905,8 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16_kernel(AttnParams p) {
 
 // ---------------------------------------------------------------------------
 // fp32 inputs, v_mfma_f32_16x16x4_f32 (true fp32 products, fp32 accumulate).
-// Same items; K/V streamed through LDS in blocks of 64 keys.
+// Same items, each taken as kF32Parts tickets of 64 queries; K/V streamed
+// through LDS in blocks of 64 keys.
 //
 // MFMA 16x16x4 f32 operand layout (lane l, g = l / 16, c = l % 16):
 //   A[16 x 4]: lane holds row c, k = g;  B[4 x 16]: lane holds column c, k = g
@@ -931,128 +936,132 @@ __global__ __launch_bounds__(kF32Threads) void attn_fwd_f32_kernel(AttnParams p)
   float* O = static_cast<float*>(p.out);
   const long long row_elems = static_cast<long long>(p.H) * kD;
 
+  // At most 8192 x 256 x 86 items (B, H, chunks of 16384 keys): the ticket
+  // count stays below 2^31.
+  const int n_tickets = n_items * kF32Parts;
   for (;;) {
     if (tid == 0) s_ticket = atomicAdd(&p.hdr->queue[0].ticket, 1);
     __syncthreads();
     const int ticket = s_ticket;
     __syncthreads();
-    if (ticket >= n_items) break;
-    const Item it = decode_item(p, p.items[ticket]);
+    if (ticket >= n_tickets) break;
+    const int part = ticket % kF32Parts;
+    const Item it = decode_item(p, p.items[ticket / kF32Parts]);
     const long long seq0 = it.seq0;
     const int len = it.len;
     const int cs = attn_chunk_size(len);
-    const int q0 = it.chunk * cs + wave * 32;
-    const int qend = min(len, (it.chunk + 1) * cs);  // this item's queries end here
+    const int qbeg = it.chunk * cs + part * kF32PartQ;  // this part's queries start here
+    const int qend = min(len, (it.chunk + 1) * cs);     // and the item's chunk ends here
+    if (qbeg >= qend) continue;                          // workgroup-uniform: an empty part
+    const int q0 = qbeg + wave * 16;
     const bool active = q0 < qend;
 
-    float qf[2][16];
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int qi = q0 + 16 * j + c16;
+    float qf[16];
+    {
+      const int qi = q0 + c16;
 #pragma unroll
       for (int ks = 0; ks < 16; ++ks)
-        qf[j][ks] = qi < qend ? Q[(seq0 + qi) * row_elems + it.h * kD + 4 * ks + g] : 0.f;
+        qf[ks] = qi < qend ? Q[(seq0 + qi) * row_elems + it.h * kD + 4 * ks + g] : 0.f;
     }
-    floatx4 o[2][4];
+    floatx4 o[4];
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt) o[j][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    float m_run[2] = {-INFINITY, -INFINITY};
-    float l_run[2] = {0.f, 0.f};
+    for (int dt = 0; dt < 4; ++dt) o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    float m_run = -INFINITY;
+    float l_run = 0.f;
 
+    // K/V of the next 64-key block are loaded into registers while the
+    // current block is computed, then stored to LDS between two barriers.
+    constexpr int kU = kBlockKeys * 16 / kF32Threads;  // float4 of K (and of V) per thread per block
+    float4 kn[kU], vn[kU];
+    auto fetch = [&](int kb0) {
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        const int e = tid + u * kF32Threads;  // 64 keys x 16 float4
+        const int key = e >> 4, dv = e & 15;
+        kn[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+        vn[u] = kn[u];
+        if (kb0 + key < len) {
+          const long long off = (seq0 + kb0 + key) * row_elems + it.h * kD + dv * 4;
+          kn[u] = *reinterpret_cast<const float4*>(K + off);
+          vn[u] = *reinterpret_cast<const float4*>(V + off);
+        }
+      }
+    };
+    fetch(0);
     for (int kb0 = 0; kb0 < len; kb0 += kBlockKeys) {
       __syncthreads();
 #pragma unroll
-      for (int u = 0; u < kBlockKeys * 16 / kF32Threads; ++u) {
-        const int e = tid + u * kF32Threads;  // 64 keys x 16 float4
+      for (int u = 0; u < kU; ++u) {
+        const int e = tid + u * kF32Threads;
         const int key = e >> 4, dv = e & 15;
-        float4 kv = make_float4(0.f, 0.f, 0.f, 0.f), vv = kv;
-        if (kb0 + key < len) {
-          const long long off = (seq0 + kb0 + key) * row_elems + it.h * kD + dv * 4;
-          kv = *reinterpret_cast<const float4*>(K + off);
-          vv = *reinterpret_cast<const float4*>(V + off);
-        }
-        *reinterpret_cast<float4*>(&Ks[key * kFStride + dv * 4]) = kv;
-        *reinterpret_cast<float4*>(&Vs[key * kFStride + dv * 4]) = vv;
+        *reinterpret_cast<float4*>(&Ks[key * kFStride + dv * 4]) = kn[u];
+        *reinterpret_cast<float4*>(&Vs[key * kFStride + dv * 4]) = vn[u];
       }
       __syncthreads();
+      if (kb0 + kBlockKeys < len) fetch(kb0 + kBlockKeys);
       if (!active) continue;
 
-      floatx4 s[2][4];
+      floatx4 s[4];
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) {
+        s[kt] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int j = 0; j < 2; ++j) s[j][kt] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < 16; ++ks) {
-          const float a = Ks[(kt * 16 + c16) * kFStride + 4 * ks + g];
-#pragma unroll
-          for (int j = 0; j < 2; ++j)
-            s[j][kt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, qf[j][ks], s[j][kt], 0, 0, 0);
-        }
+        for (int ks = 0; ks < 16; ++ks)
+          s[kt] = __builtin_amdgcn_mfma_f32_16x16x4f32(Ks[(kt * 16 + c16) * kFStride + 4 * ks + g], qf[ks], s[kt],
+                                                      0, 0, 0);
       }
       // The running max stays in raw score units and is subtracted before
       // scaling, so the terms near the max carry only a small rounding error.
       const int kvalid = len - kb0;
+      float mx = -INFINITY;
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        float mx = -INFINITY;
+      for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
+        for (int i = 0; i < 4; ++i) {
+          const int key = kt * 16 + 4 * g + i;
+          const float x = key < kvalid ? s[kt][i] : -INFINITY;
+          s[kt][i] = x;
+          mx = fmaxf(mx, x);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * p.scale_log2);
+      m_run = m_new;
+      float rs = 0.f;
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int key = kt * 16 + 4 * g + i;
-            const float x = key < kvalid ? s[j][kt][i] : -INFINITY;
-            s[j][kt][i] = x;
-            mx = fmaxf(mx, x);
-          }
-        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        const float m_new = fmaxf(m_run[j], mx);
-        const float alpha = __builtin_amdgcn_exp2f((m_run[j] - m_new) * p.scale_log2);
-        m_run[j] = m_new;
-        float rs = 0.f;
+      for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
+        for (int i = 0; i < 4; ++i) {
+          const float pv = __builtin_amdgcn_exp2f((s[kt][i] - m_new) * p.scale_log2);
+          s[kt][i] = pv;
+          rs += pv;
+        }
+      l_run = l_run * alpha + rs;
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float pv = __builtin_amdgcn_exp2f((s[j][kt][i] - m_new) * p.scale_log2);
-            s[j][kt][i] = pv;
-            rs += pv;
-          }
-        l_run[j] = l_run[j] * alpha + rs;
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt) o[j][dt] *= alpha;
-      }
+      for (int dt = 0; dt < 4; ++dt) o[dt] *= alpha;
       // O^T += V^T P^T, one 4-key step per (kt, i): MFMA k = g <-> key kt*16 + 4g + i.
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-          for (int dt = 0; dt < 4; ++dt) {
-            const float a = Vs[(kt * 16 + 4 * g + i) * kFStride + dt * 16 + c16];
-#pragma unroll
-            for (int j = 0; j < 2; ++j)
-              o[j][dt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, s[j][kt][i], o[j][dt], 0, 0, 0);
-          }
+          for (int dt = 0; dt < 4; ++dt)
+            o[dt] = __builtin_amdgcn_mfma_f32_16x16x4f32(Vs[(kt * 16 + 4 * g + i) * kFStride + dt * 16 + c16],
+                                                        s[kt][i], o[dt], 0, 0, 0);
     }
 
     if (active) {
+      float l = l_run + __shfl_xor(l_run, 16, 64);
+      l += __shfl_xor(l, 32, 64);
+      const float inv = 1.0f / l;
+      const int qi = q0 + c16;
+      if (qi < qend) {
+        float* dst = O + (seq0 + qi) * row_elems + it.h * kD + 4 * g;
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        float l = l_run[j] + __shfl_xor(l_run[j], 16, 64);
-        l += __shfl_xor(l, 32, 64);
-        const float inv = 1.0f / l;
-        const int qi = q0 + 16 * j + c16;
-        if (qi < qend) {
-          float* dst = O + (seq0 + qi) * row_elems + it.h * kD + 4 * g;
-#pragma unroll
-          for (int dt = 0; dt < 4; ++dt)
-            *reinterpret_cast<float4*>(dst + dt * 16) =
-                make_float4(o[j][dt][0] * inv, o[j][dt][1] * inv, o[j][dt][2] * inv, o[j][dt][3] * inv);
-        }
+        for (int dt = 0; dt < 4; ++dt)
+          *reinterpret_cast<float4*>(dst + dt * 16) =
+              make_float4(o[dt][0] * inv, o[dt][1] * inv, o[dt][2] * inv, o[dt][3] * inv);
       }
     }
   }
