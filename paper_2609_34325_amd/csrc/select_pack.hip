@@ -14,10 +14,14 @@
 // image each repeat the (cheap) selection and then copy a disjoint share of
 // the kept rows, so the HBM-bound copy is spread over many workgroups.
 //
-//   wave 0        radix select on order-preserving uint32 keys, one bit per
-//                 step, counting with wave ballots (keys live in VGPRs);
-//                 ordered compaction of the keep flags with ballot + mbcnt.
+//   wave 0        rows of at most 256 tokens: radix select on
+//                 order-preserving uint32 keys, one bit per step, counting
+//                 with wave ballots (keys live in VGPRs); ordered compaction
+//                 of the keep flags with ballot + mbcnt.
 //   waves 1..3    sum keep[0..b) -> this image's output offset (cu_out[b]).
+//   all waves     longer rows: the four waves each hold a quarter of the
+//                 positions and select by 8-bit digits together (LDS
+//                 histograms, a barrier per digit), then compact in order.
 //   all waves     16-byte row copies, 2 loads in flight per lane.
 //
 // dora_select_pack_plan also writes the attention work queue of the packed
@@ -96,27 +100,47 @@ __device__ __forceinline__ uint32_t wave_inclusive_sum(uint32_t x) {
   return x;
 }
 
-// Threshold of one wave's valid keys for long rows: T = the need-th largest
-// valid key (counted with multiplicity) and q = how many keys equal to T are
-// kept, found one 8-bit digit at a time from the most significant.  A pass
-// builds the 256-bin histogram (in LDS) of the digit of every valid key that
-// matches the digits fixed so far, and fixes the largest digit whose count
-// of keys at or above it still reaches the number of keys left to take; the
-// keys above that digit are all taken.  Four dependent passes instead of 32
-// one-bit steps.  hist: 256 words of LDS used by this wave only.
-template <int SLOTS>
-__device__ __forceinline__ void digit_threshold(const uint32_t (&key)[SLOTS], const uint64_t (&valid)[SLOTS],
-                                                int need, uint32_t* hist, int lane, uint32_t& T, int& q) {
-  uint4* hist4 = reinterpret_cast<uint4*>(hist);
+// Threshold of the valid keys of a long row, the four waves of the
+// workgroup each holding a quarter of them: T = the need-th largest valid key
+// (counted with multiplicity) and q = how many keys equal to T are kept,
+// found one 8-bit digit at a time from the most significant.  A pass builds
+// the 256-bin histogram of the digit of every valid key that matches the
+// digits fixed so far (each wave into its own copy in LDS, by LDS atomics),
+// and, after a barrier, every wave adds the four copies and fixes the
+// largest digit whose count of keys at or above it still reaches the number
+// of keys left to take; the keys above that digit are all taken.  Four
+// dependent passes instead of 32 one-bit steps; a quarter of the keys per
+// wave, so the same-bin atomics of a pass serialise over a quarter as many
+// lanes.  hist: 2 x 4 x 256 words (two buffers, a copy per wave): a buffer
+// is cleared by its owner one pass after its last reads, behind a barrier.
+template <int S>
+__device__ __forceinline__ void block_digit_threshold(const uint32_t (&key)[S], const uint64_t (&valid)[S],
+                                                      int need, uint32_t* hist, int lane, int wave,
+                                                      uint32_t& T, int& q) {
+  constexpr int kBuf = 4 * 256;
+  reinterpret_cast<uint4*>(hist + wave * 256)[lane] = make_uint4(0u, 0u, 0u, 0u);
+  reinterpret_cast<uint4*>(hist + kBuf + wave * 256)[lane] = make_uint4(0u, 0u, 0u, 0u);
   uint32_t prefix = 0u, fixed = 0u;
   uint32_t left = static_cast<uint32_t>(need);
 #pragma unroll
-  for (int shift = 24; shift >= 0; shift -= 8) {
-    hist4[lane] = make_uint4(0u, 0u, 0u, 0u);
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    uint32_t* buf = hist + (pass & 1) * kBuf;
 #pragma unroll
-    for (int r = 0; r < SLOTS; ++r)
-      if (((valid[r] >> lane) & 1ull) && (key[r] & fixed) == prefix) atomicAdd(&hist[(key[r] >> shift) & 255u], 1u);
-    const uint4 h = hist4[lane];  // bins 4 lane .. 4 lane + 3 (LDS accesses of one wave complete in order)
+    for (int r = 0; r < S; ++r)
+      if (((valid[r] >> lane) & 1ull) && (key[r] & fixed) == prefix)
+        atomicAdd(&buf[wave * 256 + ((key[r] >> shift) & 255u)], 1u);
+    __syncthreads();
+    // bins 4 lane .. 4 lane + 3, summed over the four copies
+    uint4 h = reinterpret_cast<const uint4*>(buf)[lane];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) {
+      const uint4 g = reinterpret_cast<const uint4*>(buf + w * 256)[lane];
+      h = make_uint4(h.x + g.x, h.y + g.y, h.z + g.z, h.w + g.w);
+    }
+    // The other buffer was read by every wave before this pass's barrier:
+    // clear this wave's copy of it for the pass after next.
+    if (pass >= 1) reinterpret_cast<uint4*>(hist + ((pass & 1) ^ 1) * kBuf + wave * 256)[lane] = make_uint4(0u, 0u, 0u, 0u);
     const uint32_t s3 = h.w, s2 = h.z + s3, s1 = h.y + s2, s0 = h.x + s1;
     const uint32_t upto = wave_inclusive_sum(s0);
     const uint32_t above = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(upto), 63)) - upto;
@@ -136,6 +160,61 @@ __device__ __forceinline__ void digit_threshold(const uint32_t (&key)[SLOTS], co
   }
   T = prefix;
   q = static_cast<int>(left);
+}
+
+// Selection and ordered compaction of a long row by the four waves: wave w
+// holds positions (w S + r) 64 + lane, r < S, so the waves' positions are
+// in wave order.  After the threshold, each wave's counts of keys above it
+// and equal to it meet in LDS; a wave's first kept index and first tie rank
+// are the counts of the waves before it.  Every wave of the workgroup calls
+// this (it holds barriers).
+template <int S>
+__device__ __forceinline__ void wide_select(const float (&x)[S], long long n, int kb, int lane, int wave,
+                                            uint32_t* hist, int (*cnt)[4], int32_t* s_idx) {
+  uint32_t key[S];
+  uint64_t valid[S];
+#pragma unroll
+  for (int r = 0; r < S; ++r) {
+    const int pos = (wave * S + r) * 64 + lane;
+    const bool v = pos >= 1 && pos < n;
+    key[r] = v ? keep_key(x[r]) : 0u;
+    valid[r] = __ballot(v);
+  }
+  const int need = kb - 1;
+  uint32_t T = 0xFFFFFFFFu;  // need == 0: nothing compares above or equal
+  int q = 0;
+  if (need > 0) block_digit_threshold<S>(key, valid, need, hist, lane, wave, T, q);
+  int n_above = 0, n_tie = 0;
+#pragma unroll
+  for (int r = 0; r < S; ++r) {
+    const bool is_valid = (valid[r] >> lane) & 1ull;
+    n_above += __popcll(__ballot(is_valid && key[r] > T));
+    n_tie += __popcll(__ballot(is_valid && key[r] == T));
+  }
+  if (lane == 0) {
+    cnt[0][wave] = n_above;
+    cnt[1][wave] = n_tie;
+  }
+  __syncthreads();
+  int cum_eq = 0, cum_keep = wave > 0 ? 1 : 0;  // CLS (position 0) is wave 0's
+  for (int w = 0; w < wave; ++w) {
+    const int t = cnt[1][w];
+    cum_keep += cnt[0][w] + min(max(q - cum_eq, 0), t);
+    cum_eq += t;
+  }
+#pragma unroll
+  for (int r = 0; r < S; ++r) {
+    const int pos = (wave * S + r) * 64 + lane;
+    const bool is_valid = (valid[r] >> lane) & 1ull;
+    const bool above = is_valid && key[r] > T;
+    const bool tie = is_valid && key[r] == T;
+    const uint64_t tie_mask = __ballot(tie);
+    const bool kept = pos == 0 || above || (tie && cum_eq + lanes_below(tie_mask) < q);
+    const uint64_t kept_mask = __ballot(kept);
+    if (kept) s_idx[cum_keep + lanes_below(kept_mask)] = pos;
+    cum_eq += __popcll(tie_mask);
+    cum_keep += __popcll(kept_mask);
+  }
 }
 
 // What the copy writes for one 16-byte piece of a kept row.
@@ -170,8 +249,13 @@ __device__ __forceinline__ u32x4 combine(uint4 x, uint4 y) {
 
 template <int SLOTS, int MODE>
 __device__ __forceinline__ void select_pack_body(const SelectPackParams& p) {
+  // Rows of more than 256 tokens are selected by all four waves, a quarter
+  // of the positions each (kWide); shorter rows by wave 0 alone.
+  constexpr bool kWide = SLOTS >= kDigitSelectSlots;
+  constexpr int kSel = kWide ? SLOTS / 4 : SLOTS;  // score slots per lane of a selecting wave
   __shared__ int32_t s_idx[SLOTS * 64];
-  __shared__ __align__(16) uint32_t s_hist[SLOTS >= kDigitSelectSlots ? 256 : 1];  // digit histogram of the long-row select
+  __shared__ __align__(16) uint32_t s_hist[kWide ? 2 * 4 * 256 : 1];  // digit histograms of the long-row select
+  __shared__ int s_cnt[2][4];                    // long rows: per wave, keys above and at the threshold
   __shared__ long long s_part[kThreads / 64];
   __shared__ long long s_before[kThreads / 64];  // plan items of the sequences with more chunks than b
   __shared__ int s_rank[kThreads / 64];          // sequences of b's chunk count ordered before b
@@ -207,13 +291,14 @@ __device__ __forceinline__ void select_pack_body(const SelectPackParams& p) {
   // candidates), and the empty asm consumes every loaded value, so the
   // compiler cannot sink a load into the branch of its only use, where each
   // would wait alone.
-  float x[SLOTS];
-  if (wave == 0 && seg_ok) {
+  float x[kSel];
+  if ((kWide || wave == 0) && seg_ok) {
     const long long last = off_in + n - 1;
+    const int g0 = kWide ? wave * kSel : 0;  // the wave's first slot
 #pragma unroll
-    for (int r = 0; r < SLOTS; ++r) x[r] = p.scores[min(off_in + r * 64 + lane, last)];
+    for (int r = 0; r < kSel; ++r) x[r] = p.scores[min(off_in + (g0 + r) * 64 + lane, last)];
 #pragma unroll
-    for (int r = 0; r < SLOTS; ++r) asm volatile("" : "+v"(x[r]));
+    for (int r = 0; r < kSel; ++r) asm volatile("" : "+v"(x[r]));
   }
   const bool img_ok = seg_ok && kb >= 1 && kb <= n;
   // With a plan, workgroup (b, 0) writes image b's attention items and
@@ -221,107 +306,111 @@ __device__ __forceinline__ void select_pack_body(const SelectPackParams& p) {
   const bool plan_img = p.plan_hdr != nullptr && s == 0;
   const bool plan_head = p.plan_hdr != nullptr && blockIdx.x == 0;
 
-  if (wave != 0) {
-    if (!p.cu_ready) {
-      // Output offset of image b: keep[0] + ... + keep[b-1].  For the plan
-      // (queue order: longer sequences first, then lower index), b's class
-      // of sequences with its chunk count starts after the items of every
-      // sequence with more chunks; inside the class b's rank is the number of
-      // class members ordered before it.
-      long long part = 0, before = 0, items = 0, kept = 0;
-      int rank = 0, members = 0, bad = 0;
-      const int chb = kb >= 1 && kb <= p.max_seqlen ? attn_chunks(kb) : 0;
-      const int jend = plan_img ? p.B : b;
-      for (int j = tid - 64; j < jend; j += kThreads - 64) {
-        const int kj = p.keep[j];
-        if (j < b) part += kj;
-        if (plan_img) {
-          const bool fits = kj >= 1 && kj <= p.max_seqlen;
-          const int chj = fits ? attn_chunks(kj) : 0;
-          if (chj > chb) before += p.H * chj;
-          if (fits && chj == chb) {
-            ++members;
-            rank += kj > kb || (kj == kb && j < b);
-          }
-          if (plan_head) {
-            items += p.H * chj;
-            kept += kj;
-            bad |= !fits;
-          }
-        }
-      }
-      part = wave_sum(part);
-      if (lane == 0) s_part[wave] = part;
+  // Waves 1-3: output offset of image b, keep[0] + ... + keep[b-1].  For the
+  // plan (queue order: longer sequences first, then lower index), b's class
+  // of sequences with its chunk count starts after the items of every
+  // sequence with more chunks; inside the class b's rank is the number of
+  // class members ordered before it.
+  auto sum_keeps = [&]() {
+    long long part = 0, before = 0, items = 0, kept = 0;
+    int rank = 0, members = 0, bad = 0;
+    const int chb = kb >= 1 && kb <= p.max_seqlen ? attn_chunks(kb) : 0;
+    const int jend = plan_img ? p.B : b;
+    for (int j = tid - 64; j < jend; j += kThreads - 64) {
+      const int kj = p.keep[j];
+      if (j < b) part += kj;
       if (plan_img) {
-        before = wave_sum(before);
-        const long long rk = wave_sum(static_cast<long long>(rank));
-        const long long mb = wave_sum(static_cast<long long>(members));
-        if (lane == 0) {
-          s_before[wave] = before;
-          s_rank[wave] = static_cast<int>(rk);
-          s_members[wave] = static_cast<int>(mb);
+        const bool fits = kj >= 1 && kj <= p.max_seqlen;
+        const int chj = fits ? attn_chunks(kj) : 0;
+        if (chj > chb) before += p.H * chj;
+        if (fits && chj == chb) {
+          ++members;
+          rank += kj > kb || (kj == kb && j < b);
         }
-      }
-      if (plan_head) {
-        items = wave_sum(items);
-        kept = wave_sum(kept);
-        bad = __ballot(bad != 0) != 0ull;
-        if (lane == 0) {
-          s_items[wave] = items;
-          s_kept[wave] = kept;
-          s_bad[wave] = bad;
+        if (plan_head) {
+          items += p.H * chj;
+          kept += kj;
+          bad |= !fits;
         }
       }
     }
-  } else if (img_ok) {
-    // Candidates are positions 1..n-1 (CLS, position 0, is not a candidate).
-    // Position pos = r*64 + lane lives in key[r] of that lane (score x[r],
-    // loaded above).
-    uint32_t key[SLOTS];
-    uint64_t valid[SLOTS];
-#pragma unroll
-    for (int r = 0; r < SLOTS; ++r) {
-      const int pos = r * 64 + lane;
-      const bool v = pos >= 1 && pos < n;
-      key[r] = v ? keep_key(x[r]) : 0u;
-      valid[r] = __ballot(v);
-    }
-    // Threshold T = the need-th largest candidate key; q = how many of the
-    // candidates equal to T are kept (the lowest positions among them).
-    const int need = kb - 1;
-    uint32_t T = 0xFFFFFFFFu;  // need == 0: nothing compares above or equal
-    int q = 0;
-    if (need > 0 && SLOTS >= kDigitSelectSlots) {
-      digit_threshold<SLOTS>(key, valid, need, s_hist, lane, T, q);
-    } else if (need > 0) {
-      T = 0u;
-      for (int bit = 31; bit >= 0; --bit) {
-        const uint32_t t = T | (1u << bit);
-        int cnt = 0;
-#pragma unroll
-        for (int r = 0; r < SLOTS; ++r) cnt += __popcll(__ballot(key[r] >= t));  // t >= 1: invalid keys (0) never count
-        if (cnt >= need) T = t;
+    part = wave_sum(part);
+    if (lane == 0) s_part[wave] = part;
+    if (plan_img) {
+      before = wave_sum(before);
+      const long long rk = wave_sum(static_cast<long long>(rank));
+      const long long mb = wave_sum(static_cast<long long>(members));
+      if (lane == 0) {
+        s_before[wave] = before;
+        s_rank[wave] = static_cast<int>(rk);
+        s_members[wave] = static_cast<int>(mb);
       }
-      int gt = 0;
-#pragma unroll
-      for (int r = 0; r < SLOTS; ++r) gt += __popcll(__ballot(key[r] > T) & valid[r]);
-      q = need - gt;
     }
-    // Ordered compaction: kept positions in ascending order.
-    int cum_eq = 0, cum_keep = 0;
-#pragma unroll
-    for (int r = 0; r < SLOTS; ++r) {
-      const int pos = r * 64 + lane;
-      const bool is_valid = (valid[r] >> lane) & 1ull;
-      const bool above = is_valid && key[r] > T;
-      const bool tie = is_valid && key[r] == T;
-      const uint64_t tie_mask = __ballot(tie);
-      const bool kept = pos == 0 || above || (tie && cum_eq + lanes_below(tie_mask) < q);
-      const uint64_t kept_mask = __ballot(kept);
-      if (kept) s_idx[cum_keep + lanes_below(kept_mask)] = pos;
-      cum_eq += __popcll(tie_mask);
-      cum_keep += __popcll(kept_mask);
+    if (plan_head) {
+      items = wave_sum(items);
+      kept = wave_sum(kept);
+      bad = __ballot(bad != 0) != 0ull;
+      if (lane == 0) {
+        s_items[wave] = items;
+        s_kept[wave] = kept;
+        s_bad[wave] = bad;
+      }
     }
+  };
+  if constexpr (!kWide) {
+    if (wave != 0) {
+      if (!p.cu_ready) sum_keeps();
+    } else if (img_ok) {
+      // Candidates are positions 1..n-1 (CLS, position 0, is not a candidate).
+      // Position pos = r*64 + lane lives in key[r] of that lane (score x[r],
+      // loaded above).
+      uint32_t key[SLOTS];
+      uint64_t valid[SLOTS];
+#pragma unroll
+      for (int r = 0; r < SLOTS; ++r) {
+        const int pos = r * 64 + lane;
+        const bool v = pos >= 1 && pos < n;
+        key[r] = v ? keep_key(x[r]) : 0u;
+        valid[r] = __ballot(v);
+      }
+      // Threshold T = the need-th largest candidate key; q = how many of the
+      // candidates equal to T are kept (the lowest positions among them).
+      const int need = kb - 1;
+      uint32_t T = 0xFFFFFFFFu;  // need == 0: nothing compares above or equal
+      int q = 0;
+      if (need > 0) {
+        T = 0u;
+        for (int bit = 31; bit >= 0; --bit) {
+          const uint32_t t = T | (1u << bit);
+          int cnt = 0;
+#pragma unroll
+          for (int r = 0; r < SLOTS; ++r) cnt += __popcll(__ballot(key[r] >= t));  // t >= 1: invalid keys (0) never count
+          if (cnt >= need) T = t;
+        }
+        int gt = 0;
+#pragma unroll
+        for (int r = 0; r < SLOTS; ++r) gt += __popcll(__ballot(key[r] > T) & valid[r]);
+        q = need - gt;
+      }
+      // Ordered compaction: kept positions in ascending order.
+      int cum_eq = 0, cum_keep = 0;
+#pragma unroll
+      for (int r = 0; r < SLOTS; ++r) {
+        const int pos = r * 64 + lane;
+        const bool is_valid = (valid[r] >> lane) & 1ull;
+        const bool above = is_valid && key[r] > T;
+        const bool tie = is_valid && key[r] == T;
+        const uint64_t tie_mask = __ballot(tie);
+        const bool kept = pos == 0 || above || (tie && cum_eq + lanes_below(tie_mask) < q);
+        const uint64_t kept_mask = __ballot(kept);
+        if (kept) s_idx[cum_keep + lanes_below(kept_mask)] = pos;
+        cum_eq += __popcll(tie_mask);
+        cum_keep += __popcll(kept_mask);
+      }
+    }
+  } else {
+    if (wave != 0 && !p.cu_ready) sum_keeps();
+    if (img_ok) wide_select<kSel>(x, n, kb, lane, wave, s_hist, s_cnt, s_idx);  // img_ok: uniform in the workgroup
   }
   __syncthreads();
   const long long off_out = p.cu_ready ? cu_b : s_part[1] + s_part[2] + s_part[3];
