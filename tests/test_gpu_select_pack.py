@@ -132,9 +132,10 @@ def test_deterministic(gpu):
         assert np.array_equal(x, y)
 
 
-def test_keep_out_of_range_sets_status(gpu):
+@pytest.mark.parametrize("n", [40, 577])  # one-wave and four-wave selection
+def test_keep_out_of_range_sets_status(gpu, n):
     rng = np.random.default_rng(3)
-    B, n = 6, 40
+    B = 6
     scores = rng.standard_normal((B, n)).astype(np.float32)
     tokens = rng.standard_normal((B, n, 4)).astype(np.float32)
     for bad in (0, n + 1, -5):
@@ -144,17 +145,18 @@ def test_keep_out_of_range_sets_status(gpu):
         assert st & gpu.DORA_DEV_KEEP_RANGE and canary
 
 
-def test_capacity_overflow_never_writes_past_cap(gpu):
+@pytest.mark.parametrize("n,kb,cap", [(100, 90, 500), (600, 540, 3000)])  # one-wave and four-wave selection
+def test_capacity_overflow_never_writes_past_cap(gpu, n, kb, cap):
     rng = np.random.default_rng(4)
-    B, n = 8, 100
+    B = 8
     scores = rng.standard_normal((B, n)).astype(np.float32)
-    keep = np.full(B, 90, np.int32)
+    keep = np.full(B, kb, np.int32)
     tokens = rng.integers(0, 2 ** 16, size=(B, n, 16)).astype(np.uint16)
-    idx, cu, packed, st, canary = run_gpu(gpu, scores, keep, tokens, cap=500, guard=64)
+    idx, cu, packed, st, canary = run_gpu(gpu, scores, keep, tokens, cap=cap, guard=64)
     assert st & gpu.DORA_DEV_CAPACITY
     assert canary
     idx_o, cu_o, packed_o, _ = oracle.select_pack(scores, keep, tokens)
-    assert np.array_equal(idx, idx_o[:500]) and np.array_equal(packed, packed_o[:500])
+    assert np.array_equal(idx, idx_o[:cap]) and np.array_equal(packed, packed_o[:cap])
 
 
 def test_invalid_cu_in_sets_status(gpu):
