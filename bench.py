@@ -260,17 +260,22 @@ def summarize_pmc(d: str, workload: str) -> int:
     GRBM_GUI_ACTIVE x SIMDs, rocprofv3's MfmaUtil), bf16 MFMA flops executed
     (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512) against the algorithmic flops, and
     LDS bank conflicts per LDS access cycle.  Averages are per dispatch, over
-    the launches after the first two."""
+    the launches after the first two.  Where a run left its phase log
+    (DIR/<run>/phases.json, from --phase-log), the attention and select/pack
+    counters are also given per timed phase: in the step, and alone (back to
+    back on one buffer set, the MALL-resident regime)."""
     import csv
     w = W.WORKLOADS[workload]
     keep = W.generate(w, parts=("keep",))[0].keep
     alg = {"attn": attn_flops(w, keep)}
     per = collections.defaultdict(lambda: collections.defaultdict(lambda: collections.defaultdict(float)))
     dur = collections.defaultdict(dict)
+    phase_of = {}  # (run, dispatch id) -> phase name
     for sub in sorted(os.listdir(d)):
         f = os.path.join(d, sub, "run_counter_collection.csv")
         if not os.path.exists(f):
             continue
+        order = collections.defaultdict(set)  # kernel key -> dispatch ids of this run
         for r in csv.DictReader(open(f)):
             k = _kernel_key(r["Kernel_Name"])
             if k is None:
@@ -278,11 +283,41 @@ def summarize_pmc(d: str, workload: str) -> int:
             disp = (sub, int(r["Dispatch_Id"]))
             per[k][r["Counter_Name"]][disp] += float(r["Counter_Value"])
             dur[k][disp] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9
+            order[k].add(disp[1])
+        plog = os.path.join(d, sub, "phases.json")
+        if os.path.exists(plog):
+            seq = {k: sorted(v) for k, v in order.items()}
+            for name, ids in split_by_phase(seq, json.load(open(plog))).items():
+                for k, v in ids.items():
+                    for i in v:
+                        phase_of[(sub, i)] = name
 
     def mean(vals):
         vals = [vals[i] for i in sorted(vals)]
         vals = vals[2:] if len(vals) > 3 else vals
         return sum(vals) / len(vals) if vals else float("nan")
+
+    def derived(k, c, t):
+        out = []
+        grbm = c.get("GRBM_GUI_ACTIVE")
+        if grbm and "SQ_VALU_MFMA_BUSY_CYCLES" in c:
+            util = c["SQ_VALU_MFMA_BUSY_CYCLES"] / (grbm / N_XCD * N_SIMD)
+            out.append((f"MFMA busy = MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / {N_XCD} x {N_SIMD} SIMDs)",
+                        f"{100 * util:.1f} %"))
+        if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in c and k in alg:
+            ex = c["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512
+            out.append(("bf16 MFMA flops executed / algorithmic",
+                        f"{ex / 1e9:,.2f} G / {alg[k] / 1e9:,.2f} G = {ex / alg[k]:.2f}"))
+            out.append(("executed bf16 MFMA rate over the duration",
+                        f"{ex / t / 1e12:,.0f} TFLOP/s ({100 * ex / t / 1e12 / MFMA_PEAK_TFLOPS['bf16']:.1f} % of peak)"))
+        if "SQ_LDS_BANK_CONFLICT" in c and "SQ_LDS_IDX_ACTIVE" in c and c["SQ_LDS_IDX_ACTIVE"] > 0:
+            out.append(("LDS bank conflict cycles / LDS active cycles",
+                        f"{c['SQ_LDS_BANK_CONFLICT'] / c['SQ_LDS_IDX_ACTIVE']:.3f}"))
+        if "SQ_WAVE_CYCLES" in c:
+            for name in ("SQ_ACTIVE_INST_VALU", "SQ_ACTIVE_INST_LDS", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY"):
+                if name in c:
+                    out.append((f"{name} / SQ_WAVE_CYCLES", f"{100 * c[name] / c['SQ_WAVE_CYCLES']:.1f} %"))
+        return out
 
     lines = ["| Kernel | Counter / derived | Per launch |", "|---|---|---|"]
     for k in sorted(per):
@@ -294,23 +329,23 @@ def summarize_pmc(d: str, workload: str) -> int:
         grbm = c.get("GRBM_GUI_ACTIVE")
         if grbm:
             lines.append(f"| {k} | clock = GRBM_GUI_ACTIVE / {N_XCD} / duration (GHz) | {grbm / N_XCD / t / 1e9:.2f} |")
-        if grbm and "SQ_VALU_MFMA_BUSY_CYCLES" in c:
-            util = c["SQ_VALU_MFMA_BUSY_CYCLES"] / (grbm / N_XCD * N_SIMD)
-            lines.append(f"| {k} | MFMA busy = MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / {N_XCD} x {N_SIMD} SIMDs) | "
-                         f"{100 * util:.1f} % |")
-        if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in c and k in alg:
-            ex = c["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512
-            lines.append(f"| {k} | bf16 MFMA flops executed / algorithmic | {ex / 1e9:,.2f} G / {alg[k] / 1e9:,.2f} G "
-                         f"= {ex / alg[k]:.2f} |")
-            lines.append(f"| {k} | executed bf16 MFMA rate over the duration | {ex / t / 1e12:,.0f} TFLOP/s "
-                         f"({100 * ex / t / 1e12 / MFMA_PEAK_TFLOPS['bf16']:.1f} % of peak) |")
-        if "SQ_LDS_BANK_CONFLICT" in c and "SQ_LDS_IDX_ACTIVE" in c and c["SQ_LDS_IDX_ACTIVE"] > 0:
-            lines.append(f"| {k} | LDS bank conflict cycles / LDS active cycles | "
-                         f"{c['SQ_LDS_BANK_CONFLICT'] / c['SQ_LDS_IDX_ACTIVE']:.3f} |")
-        if "SQ_WAVE_CYCLES" in c:
-            for name in ("SQ_ACTIVE_INST_VALU", "SQ_ACTIVE_INST_LDS", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY"):
-                if name in c:
-                    lines.append(f"| {k} | {name} / SQ_WAVE_CYCLES | {100 * c[name] / c['SQ_WAVE_CYCLES']:.1f} % |")
+        for name, val in derived(k, c, t):
+            lines.append(f"| {k} | {name} | {val} |")
+    if phase_of:
+        # Per timed phase (warm-up phases left out), for the step kernels.
+        lines += ["", "Per timed phase (averages over the phase's launches in every run that logged its phases):", "",
+                  "| Kernel | Phase | Launches | Duration (us) | Derived |", "|---|---|---|---|---|"]
+        for k in ("attn", "select_pack"):
+            if k not in per:
+                continue
+            names = sorted({phase_of[dd] for dd in dur[k] if dd in phase_of and not phase_of[dd].endswith("warmup")})
+            for ph in names:
+                sel = lambda vals: {dd: v for dd, v in vals.items() if phase_of.get(dd) == ph}
+                c = {name: (sum(sel(v).values()) / len(sel(v)) if sel(v) else float("nan")) for name, v in per[k].items()}
+                dd_ph = sel(dur[k])
+                t = sum(dd_ph.values()) / len(dd_ph)
+                der = "; ".join(f"{n}: {v}" for n, v in derived(k, c, t))
+                lines.append(f"| {k} | {ph} | {len(dd_ph)} | {t * 1e6:,.1f} | {der} |")
     print("\n".join(lines))
     return 0
 
