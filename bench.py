@@ -134,11 +134,14 @@ class PhaseLog:
 
     def __init__(self):
         self.phases = []   # [name, {key: count}]
+        self.paused = False  # while a graph is captured (its launches run, and are counted, at replay)
 
     def start(self, name: str):
         self.phases.append([name, collections.Counter()])
 
     def count(self, *keys):
+        if self.paused:
+            return
         if not self.phases:
             self.start("setup")
         for k in keys:
@@ -498,6 +501,26 @@ class ConfigRun:
         return res
 
 
+def capture(torch, stream, body, phases=None):
+    """body()'s launches (all on `stream`, a non-default stream) captured
+    into a HIP graph, not run.  The entry points allocate nothing, set no
+    memory and never synchronise, so a timed loop can be replayed as one
+    graph: the host's per-call cost (the Python binding takes several
+    microseconds a call) then no longer bounds short kernels."""
+    g = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    if phases is not None:
+        phases.paused = True
+    try:
+        with torch.cuda.graph(g, stream=stream):
+            body()
+    finally:
+        if phases is not None:
+            phases.paused = False
+    torch.cuda.synchronize()
+    return g
+
+
 def time_steps(run: ConfigRun, sets, args, tag: str):
     """Median over repeats of the step time (ms) and of each launch's duration
     (ms, HIP events around every kernel).  Step i uses sets[i % len(sets)].
@@ -511,14 +534,30 @@ def time_steps(run: ConfigRun, sets, args, tag: str):
         run.step(sets[i % len(sets)])
     torch.cuda.synchronize()
     n = 2 * run.R
+    keys = [k for k, _, _ in run.launches(sets[0])]
+
+    def steps():
+        for i in range(args.steps):
+            run.step(sets[i % len(sets)])
+
+    g = None if args.eager else capture(torch, stream, steps, phases)
+    if g is not None:
+        g.replay()  # the graph's first replay, untimed
+        for _ in range(args.steps):
+            phases.count(*keys)
+        torch.cuda.synchronize()
     reps = []
     for rep in range(args.repeats):
         phases.start(f"{run.w.name}:{tag}:bare")
         t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         t0.record(stream)
-        for i in range(args.steps):
-            run.step(sets[i % len(sets)])
+        if g is not None:
+            g.replay()
+            for _ in range(args.steps):
+                phases.count(*keys)
+        else:
+            steps()
         t1.record(stream)
         torch.cuda.synchronize()
         step_ms = t0.elapsed_time(t1) / args.steps
@@ -539,13 +578,28 @@ def time_steps(run: ConfigRun, sets, args, tag: str):
 
 def time_calls(torch, stream, fn, args, phases=None, tag=None, keys=()):
     """Median over repeats of the mean time (ms) of `steps` back-to-back calls
-    of fn (after `warmup` calls), HIP events at the two ends."""
+    of fn (after `warmup` calls), HIP events at the two ends; the calls are
+    replayed as one HIP graph unless --eager."""
     if phases is not None:
         phases.start(f"{tag}:warmup")
     for _ in range(args.warmup):
         fn()
         if phases is not None:
             phases.count(*keys)
+
+    def calls():
+        for _ in range(args.steps):
+            fn()
+            if phases is not None:
+                phases.count(*keys)
+
+    g = None if args.eager else capture(torch, stream, calls, phases)
+    if g is not None:
+        g.replay()  # untimed
+        if phases is not None:
+            for _ in range(args.steps):
+                phases.count(*keys)
+        torch.cuda.synchronize()
     reps = []
     for _ in range(args.repeats):
         if phases is not None:
@@ -553,10 +607,13 @@ def time_calls(torch, stream, fn, args, phases=None, tag=None, keys=()):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         e0.record(stream)
-        for _ in range(args.steps):
-            fn()
+        if g is not None:
+            g.replay()
             if phases is not None:
-                phases.count(*keys)
+                for _ in range(args.steps):
+                    phases.count(*keys)
+        else:
+            calls()
         e1.record(stream)
         torch.cuda.synchronize()
         reps.append(e0.elapsed_time(e1) / args.steps)
@@ -674,6 +731,8 @@ def main() -> int:
     ap.add_argument("--no-peaks", action="store_true", help="skip measuring the copy and MFMA peaks")
     ap.add_argument("--no-adjacent", action="store_true",
                     help="skip the adjacent entry points (residual, actor, LC1, FLOPs, Plackett-Luce)")
+    ap.add_argument("--eager", action="store_true",
+                    help="time the loops as eager back-to-back launches instead of one HIP graph replay")
     ap.add_argument("--no-large-batch", action="store_true",
                     help="skip the select/pack runs at 8192 and 65536 images (their launches would mix "
                          "into the per-launch counter averages of the headline select/pack)")
@@ -706,7 +765,10 @@ def main() -> int:
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dora.load_library()
     torch.cuda.set_device(0)
-    stream = torch.cuda.current_stream()
+    # A stream of its own (graph capture needs a non-default stream), current
+    # for everything the bench does.
+    stream = torch.cuda.Stream()
+    torch.cuda.set_stream(stream)
     phases = PhaseLog()
     w = W.WORKLOADS[args.workload]
     head = ConfigRun(w, torch, dora, stream, phases)
@@ -834,6 +896,9 @@ def main() -> int:
                "step": ms_step * 1e3},
         "repeats": args.repeats,
         "regime": "warm: the same input buffers every step",
+        "timing": ("eager back-to-back launches" if args.eager else
+                   "the K timed steps (and each kernel's K calls alone) replayed as one HIP graph; in-step kernel "
+                   "durations from an eager loop with HIP events around every kernel"),
         "cold": cold,
         "measured_peaks": peaks,
         "parity": None,
