@@ -339,7 +339,8 @@ int dora_pl_logprob(const float* scores, const int32_t* order, const int32_t* cu
  *   out[b, 0:C]    = LN(x_CLS)
  *   out[b, C:2C]   = mean of LN(x_j) over the sequence's other rows
  *                    (NaN when only CLS survives).
- * Arithmetic in fp32 from the exact input values.
+ * Arithmetic in fp32 from the exact input values; 1 / sqrt(var + eps) comes
+ * from the hardware reciprocal square root (within about 1 ulp).
  *
  *   x          dtype [total, C], 16-byte aligned; C * sizeof(dtype) a multiple
  *              of 16 and at most 4096 bytes (else DORA_ERR_UNSUPPORTED).
