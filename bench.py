@@ -501,6 +501,9 @@ class ConfigRun:
         return res
 
 
+CAPTURE_FAILURES = []
+
+
 def capture(torch, stream, body, phases=None):
     """body()'s launches (all on `stream`, a non-default stream) captured
     into a HIP graph, not run.  The entry points allocate nothing, set no
@@ -514,6 +517,11 @@ def capture(torch, stream, body, phases=None):
     try:
         with torch.cuda.graph(g, stream=stream):
             body()
+    except RuntimeError as e:  # the loop is then timed eagerly, and the line says so
+        print(f"[bench] graph capture failed ({e}); timing eagerly", file=sys.stderr, flush=True)
+        CAPTURE_FAILURES.append(str(e))
+        torch.cuda.synchronize()
+        return None
     finally:
         if phases is not None:
             phases.paused = False
@@ -897,6 +905,8 @@ def main() -> int:
         "repeats": args.repeats,
         "regime": "warm: the same input buffers every step",
         "timing": ("eager back-to-back launches" if args.eager else
+                   f"eager back-to-back launches where graph capture failed ({len(CAPTURE_FAILURES)} loops)"
+                   if CAPTURE_FAILURES else
                    "the K timed steps (and each kernel's K calls alone) replayed as one HIP graph; in-step kernel "
                    "durations from an eager loop with HIP events around every kernel"),
         "cold": cold,
