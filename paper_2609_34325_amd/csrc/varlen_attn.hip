@@ -61,6 +61,7 @@ constexpr int kKRes = 256;             // keys resident in LDS per stage (bf16)
 // query tiles of an item, so the queue's latency lands where there is slack.
 constexpr int kQueueThread = kThreads - 64;
 constexpr int kPlanThreads = 1024;
+constexpr int kPlanMaxChunks = (DORA_MAX_SEQLEN + kAttnQTile - 1) / kAttnQTile;  // chunks of the longest sequence
 constexpr int kPlanBins = 1024;
 constexpr float kLog2e = 1.4426950408889634f;
 
@@ -126,6 +127,7 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanParams p) {
   __shared__ uint32_t order[kPlanMaxB];  // sequence | len << 13, by decreasing length
   __shared__ int base[kPlanMaxB + 1];    // first item of each sorted position
   __shared__ int wave_sums[kPlanThreads / 64 + 1];
+  __shared__ int cls_lo[kPlanMaxChunks + 1], cls_hi[kPlanMaxChunks + 1];  // class bounds by chunk count
   __shared__ int s_bad;
   const int tid = threadIdx.x;
   // Length bins: bin 0 for empty sequences, then (len - 1) >> shift + 1.
@@ -189,38 +191,29 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanParams p) {
   if (tid == 0) base[p.B] = n_items;
   __syncthreads();
 
-  // Emit: the t-th item in (position, head, chunk) order belongs to the last
-  // sorted position whose first item <= t; it goes to its slot in the class
-  // of sequences with its chunk count (attn_item_slot).
+  // Class bounds: sorted positions [cls_lo[ch], cls_hi[ch]) hold the
+  // sequences of ch chunks (chunk counts fall with position).
   auto chunks_at = [&](int pos) { return attn_chunks(static_cast<int>(order[pos] >> 13)); };
-  for (int t = tid; t < n_items; t += kPlanThreads) {
-    int lo = 0, hi = p.B - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (base[mid] <= t) lo = mid;
-      else hi = mid - 1;
-    }
-    const uint32_t o = order[lo];
+  for (int pos = tid; pos < p.B; pos += kPlanThreads) {
+    const int ch = chunks_at(pos);
+    if (pos == 0 || chunks_at(pos - 1) != ch) cls_lo[ch] = pos;
+    if (pos == p.B - 1 || chunks_at(pos + 1) != ch) cls_hi[ch] = pos + 1;
+  }
+  __syncthreads();
+  // Emit, one sorted position per thread at a time: its H x chunks items go
+  // to their slots in the class (attn_item_slot).
+  for (int pos = tid; pos < p.B; pos += kPlanThreads) {
+    const uint32_t o = order[pos];
     const int b = static_cast<int>(o & 0x1FFFu);
     const int len = static_cast<int>(o >> 13);
-    const int chunks = attn_chunks(len);
-    const int li = t - base[lo];
-    const int h = li / chunks, c = li - h * chunks;
-    // The class: positions [c0, c1) with this chunk count (counts fall with position).
-    int c0 = 0, c1 = lo;
-    while (c0 < c1) {
-      const int mid = (c0 + c1) >> 1;
-      if (chunks_at(mid) > chunks) c0 = mid + 1;
-      else c1 = mid;
-    }
-    int e0 = lo + 1, e1 = p.B;
-    while (e0 < e1) {
-      const int mid = (e0 + e1) >> 1;
-      if (chunks_at(mid) >= chunks) e0 = mid + 1;
-      else e1 = mid;
-    }
-    const long long slot = attn_item_slot(base[c0], (e0 - c0) * p.H, chunks, (lo - c0) * p.H + h, c);
-    p.items[slot] = encode_item(s_cu[b], len, h, c);
+    const int ch = attn_chunks(len);
+    if (ch == 0) continue;
+    const int c0 = cls_lo[ch];
+    const int groups = (cls_hi[ch] - c0) * p.H;
+    const long long cbase = base[c0];
+    for (int h = 0; h < p.H; ++h)
+      for (int c = 0; c < ch; ++c)
+        p.items[attn_item_slot(cbase, groups, ch, (pos - c0) * p.H + h, c)] = encode_item(s_cu[b], len, h, c);
   }
   if (tid < 32) p.hdr->zero_row[tid] = 0u;
   if (tid == 0) write_plan_header(p.hdr, n_items, p.B, p.H, p.max_seqlen, p.total);
