@@ -117,6 +117,12 @@ def test_long_sequence_and_many_heads(gpu):
     lens = np.array([77, 200, 5])
     q, k, v = qkv(rng, lens, 16, "bf16")
     full_compare(gpu, q, k, v, cu_of(lens), "bf16", what="H=16")
+    lens = np.array([40, 3, 193])  # 256 heads (the most a plan item can name), one sequence of two chunks
+    q, k, v = qkv(rng, lens, 256, "bf16")
+    full_compare(gpu, q, k, v, cu_of(lens), "bf16", what="H=256")
+    lens = np.array([1])
+    q, k, v = qkv(rng, lens, 1, "f32")
+    full_compare(gpu, q, k, v, cu_of(lens), "f32", what="H=1, one token")
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])

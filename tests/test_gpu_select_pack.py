@@ -114,6 +114,21 @@ def test_row_widths(gpu, C, dtype):
     check_round(gpu, scores, keep, tokens)
 
 
+@pytest.mark.parametrize("C,dtype", [(262144, np.float32), (524288, np.uint16)])
+def test_widest_rows(gpu, C, dtype):
+    """Rows of 1 MB, the widest the library takes (4096 16-byte pieces per
+    thread block step): a short batch, bit-exact."""
+    rng = np.random.default_rng(C + 1)
+    B, n = 3, 5
+    scores = rng.standard_normal((B, n)).astype(np.float32)
+    keep = np.array([5, 1, 3], np.int32)
+    if dtype == np.float32:
+        tokens = rng.standard_normal((B, n, C)).astype(np.float32)
+    else:
+        tokens = rng.integers(0, 2 ** 16, size=(B, n, C)).astype(np.uint16)
+    check_round(gpu, scores, keep, tokens)
+
+
 def test_many_images(gpu):
     rng = np.random.default_rng(77)
     B, n = 3000, 50
