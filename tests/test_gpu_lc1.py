@@ -164,3 +164,44 @@ def test_invalid_sequence_on_the_split_path(gpu):
         want = oracle.lc1_readout(xb, seg, gamma, beta, 1e-6, "bf16")[0]
         tol = fp32_bound(oracle.widen(xb, "bf16"), seg, gamma.astype(np.float64), beta.astype(np.float64), 1e-6)
         assert np.all(np.abs(o[b] - want) <= tol[0]), b
+
+
+@pytest.mark.parametrize("with_ws", [False, True])
+def test_many_short_sequences(gpu, with_ws):
+    """3000 sequences of 1 to 40 rows (more images than workgroups fit at
+    once), with and without a workspace."""
+    rng = np.random.default_rng(3000 + with_ws)
+    C = 768
+    lens = rng.integers(1, 41, 3000)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    x = W.f32_to_bf16_bits((rng.standard_normal((int(cu[-1]), C)) + rng.standard_normal(C)).astype(np.float32))
+    gamma = rng.uniform(0.5, 1.5, C).astype(np.float32)
+    beta = (0.1 * rng.standard_normal(C)).astype(np.float32)
+    want = oracle.lc1_readout(x, cu, gamma, beta, 1e-6, "bf16")
+    tol = fp32_bound(oracle.widen(x, "bf16"), cu, gamma.astype(np.float64), beta.astype(np.float64), 1e-6)
+    kw = {"workspace": gpu.new_lc1_workspace(len(lens), C)} if with_ws else {}
+    got = run_lc1(gpu, x, cu, gamma, beta, **kw)
+    nan = np.isnan(want)
+    assert np.array_equal(np.isnan(got), nan)
+    err = np.where(nan, 0.0, np.abs(got - want))
+    assert np.all(err <= tol[:, None]), (err.max(), tol.min())
+
+
+def test_constant_rows_without_eps(gpu):
+    """eps = 0: a constant row has zero variance, so its normalised values are
+    0/0 = NaN, in the kernel (0 times the reciprocal square root of 0) as in
+    the oracle; a sequence without such a row stays finite."""
+    rng = np.random.default_rng(5)
+    C = 256
+    x = rng.standard_normal((12, C)).astype(np.float32)
+    x[0] = 3.0   # CLS of sequence 0 constant
+    x[6] = -1.5  # a visual row of sequence 1 constant
+    cu = np.array([0, 4, 9, 12], np.int32)
+    gamma = rng.uniform(0.5, 1.5, C).astype(np.float32)
+    beta = (0.1 * rng.standard_normal(C)).astype(np.float32)
+    want = oracle.lc1_readout(x, cu, gamma, beta, 0.0, "f32")
+    got = run_lc1(gpu, x, cu, gamma, beta, eps=0.0)
+    assert np.all(np.isnan(want[0, :C])) and np.all(np.isnan(want[1, C:])) and np.all(np.isfinite(want[2]))
+    assert np.array_equal(np.isnan(got), np.isnan(want))
+    ok = ~np.isnan(want)
+    assert np.max(np.abs(got[ok] - want[ok])) < 1e-4
