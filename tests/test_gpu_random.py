@@ -36,7 +36,7 @@ def random_select_case(seed):
     return scores, keep, tokens, cu_in, N
 
 
-@pytest.mark.parametrize("seed", range(12))
+@pytest.mark.parametrize("seed", range(24))
 def test_random_select_pack(gpu, seed):
     scores, keep, tokens, cu_in, N = random_select_case(seed)
     print(f"[random] select seed {seed}: B={len(keep)} N={N} C={tokens.shape[-1]} {tokens.dtype} "
@@ -52,7 +52,7 @@ def test_random_select_pack(gpu, seed):
     assert np.array_equal(to_host_bits(packed), want[2])
 
 
-@pytest.mark.parametrize("seed", range(8))
+@pytest.mark.parametrize("seed", range(16))
 def test_random_attention(gpu, seed):
     rng = np.random.default_rng(2000 + seed)
     B = int(rng.integers(1, 40))
@@ -103,17 +103,30 @@ def test_random_pl_sample(gpu, seed):
     pl.check(gpu, s, g, k, cu=cu, N=N if packed else None)
 
 
-@pytest.mark.parametrize("seed", range(4))
+@pytest.mark.parametrize("seed", range(12))
 def test_random_lc1(gpu, seed):
+    """Row widths that fill their lane groups and widths that leave a padded
+    last piece, with and without a workspace (the split path)."""
     import test_gpu_lc1 as lc
     rng = np.random.default_rng(5000 + seed)
     dtype = "bf16" if rng.random() < 0.7 else "f32"
-    C = int(rng.choice([8, 64, 384, 768, 1024])) if dtype == "bf16" else int(rng.choice([4, 192, 768]))
+    C = int(rng.choice([8, 64, 200, 384, 520, 768, 1000, 1024])) if dtype == "bf16" \
+        else int(rng.choice([4, 100, 192, 516, 768]))
     lens = rng.integers(1, int(rng.choice([8, 200, 1500])) + 1, int(rng.integers(1, 64)))
     cu = cu_of(lens)
     x = (rng.standard_normal((int(cu[-1]), C)) * rng.uniform(0.2, 3, C) + rng.standard_normal(C)).astype(np.float32)
     xs = W.f32_to_bf16_bits(x) if dtype == "bf16" else x
     gamma = rng.uniform(0.5, 1.5, C).astype(np.float32)
     beta = (0.1 * rng.standard_normal(C)).astype(np.float32)
-    print(f"[random] lc1 seed {seed}: B={len(lens)} C={C} {dtype}", flush=True)
-    lc.compare(gpu, xs, cu, gamma, beta, dtype)
+    split = rng.random() < 0.5
+    print(f"[random] lc1 seed {seed}: B={len(lens)} C={C} {dtype} workspace={split}", flush=True)
+    if not split:
+        lc.compare(gpu, xs, cu, gamma, beta, dtype)
+        return
+    want = oracle.lc1_readout(xs, cu, gamma, beta, 1e-6, dtype)
+    tol = lc.fp32_bound(oracle.widen(xs, dtype), cu, gamma.astype(np.float64), beta.astype(np.float64), 1e-6)
+    got = lc.run_lc1(gpu, xs, cu, gamma, beta, workspace=gpu.new_lc1_workspace(len(lens), C))
+    nan = np.isnan(want)
+    assert np.array_equal(np.isnan(got), nan)
+    err = np.where(nan, 0.0, np.abs(got - want))
+    assert np.all(err <= tol[:, None]), (err.max(), tol.min())
