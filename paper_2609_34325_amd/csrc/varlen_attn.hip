@@ -591,6 +591,20 @@ __device__ __forceinline__ void softmax_pv_block(const LanePtrs& lp, int kb, int
   }
 }
 
+// Wave priority by progress through a stage.  The three waves of a SIMD
+// have the same work per stage, but the instruction arbiter favours the
+// oldest wave, so left alone one wave finishes its blocks first, then the
+// next, and the last runs alone on its SIMD (little to overlap its matrix
+// and VALU work with) while the others wait at the stage barrier.  A stage
+// starts every wave at priority 3 and each finished 64-key block lowers it
+// by one, so the wave that is behind is served first and the three finish
+// close together.
+__device__ __forceinline__ void prio_after_block(int b) {
+  if (b == 0) __builtin_amdgcn_s_setprio(2);
+  else if (b == 1) __builtin_amdgcn_s_setprio(1);
+  else __builtin_amdgcn_s_setprio(0);
+}
+
 // All key blocks of one stage (nk >= 1 keys in LDS): 64-key blocks, except
 // that a last block of at most 32 keys runs as a 32-key half block after the
 // others.  Two key blocks are in flight: the MFMAs of block kb+64 are issued
@@ -606,12 +620,15 @@ __device__ __forceinline__ void attend_stage(const LanePtrs& lp, int nk, bool fi
     if (nm > 64) qk_block<ACT1, false>(lp, 64, qf, sbk);
     if (first) softmax_pv_block<ACT1, true, false>(lp, 0, nm, scale_log2, ones, sa, sm);
     else softmax_pv_block<ACT1, false, false>(lp, 0, nm, scale_log2, ones, sa, sm);
+    prio_after_block(0);
     for (int kb = 64; kb < nm; kb += 128) {
       if (kb + 64 < nm) qk_block<ACT1, false>(lp, kb + 64, qf, sa);
       softmax_pv_block<ACT1, false, false>(lp, kb, nm - kb, scale_log2, ones, sbk, sm);
+      prio_after_block(kb >> 6);
       if (kb + 64 >= nm) break;
       if (kb + 128 < nm) qk_block<ACT1, false>(lp, kb + 128, qf, sbk);
       softmax_pv_block<ACT1, false, false>(lp, kb + 64, nm - kb - 64, scale_log2, ones, sa, sm);
+      prio_after_block((kb >> 6) + 1);
     }
   }
   if (nm < nk) {
@@ -710,6 +727,7 @@ __device__ __forceinline__ bool attn_stage(const KernelCtx& c, Sched& s, const c
   if (nst == 4) asm volatile("s_waitcnt vmcnt(4) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   else if (nst == 2) asm volatile("s_waitcnt vmcnt(2) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  __builtin_amdgcn_s_setprio(3);
   if (s.shift) {
     const int2 raw = uniform_raw(s_raw[1 - B]);
     const bool nn_valid = raw.x != -1;
