@@ -301,6 +301,7 @@ constexpr int kRowBytes = kD * 2;
 constexpr int kStageElems = kKRes * kD;
 
 typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) const char lds_cchar;
 
 // Byte address of element (row0, head h, dim 0) of a packed [rows, H, 64]
 // tensor.  Every argument is the same in all lanes, so this is scalar
@@ -363,16 +364,27 @@ __device__ __forceinline__ LdsOffsets lds_offsets() {
 // the 16-bit offset range of LDS instructions for the second buffer) sits in
 // the lane's address register and each read inside the loop carries only the
 // block and step offsets.
+
+
 struct LanePtrs {
-  const char* k0;
-  const char* k1;
+  lds_cchar* k0;
+  lds_cchar* k1;
   const char* v[4];
 };
 
+// The K buffer's LDS address (past the 64 KB that the 16-bit offset field of
+// an LDS instruction reaches) is hidden from the compiler, which would
+// otherwise fold it into every K read and pay an add for each; this way it
+// is added once per stage and each read carries its row offset as the
+// immediate.  (The V buffers lie below 64 KB, so their reads need no such
+// step; they keep their pointers' provenance, without which the compiler
+// makes the transposing V reads wait for the LDS DMA in flight.)
 __device__ __forceinline__ LanePtrs lane_ptrs(const char* Ks, const char* Vs, const LdsOffsets& lo) {
+  uint32_t kbase = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_cchar*)Ks));
+  asm volatile("" : "+s"(kbase));
   LanePtrs lp;
-  lp.k0 = Ks + lo.k0;
-  lp.k1 = Ks + lo.k1;
+  lp.k0 = reinterpret_cast<lds_cchar*>(static_cast<uintptr_t>(kbase + lo.k0));
+  lp.k1 = reinterpret_cast<lds_cchar*>(static_cast<uintptr_t>(kbase + lo.k1));
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) lp.v[dt] = Vs + lo.v[dt];
   return lp;
@@ -450,8 +462,9 @@ __device__ __forceinline__ void qk_block(const LanePtrs& lp, int kb, const bf16x
 #pragma unroll
   for (int kt = 0; kt < (HALF ? 2 : 4); ++kt) {
     const int off = (kb + kt * 16) * kRowBytes;
-    const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(lp.k0 + off);
-    const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(lp.k1 + off);
+    typedef __attribute__((address_space(3))) const bf16x8 lds_bf16x8;
+    const bf16x8 a0 = *reinterpret_cast<lds_bf16x8*>(lp.k0 + off);
+    const bf16x8 a1 = *reinterpret_cast<lds_bf16x8*>(lp.k1 + off);
     s[0][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
         a1, qf[0][1], __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, qf[0][0], zero, 0, 0, 0), 0, 0, 0);
     if (ACT1)
@@ -492,6 +505,22 @@ __device__ __forceinline__ void softmax_pv_block(const LanePtrs& lp, int kb, int
   constexpr int kKs = HALF ? 1 : 2;  // 32-key P.V steps in the block
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4;
+  // V^T operands of the block's P.V steps, read first (and kept first by a
+  // scheduling barrier) so that the reads are in flight while the softmax
+  // runs: the compiler otherwise issues them pairwise just before each P.V
+  // product and waits out the LDS latency eight times per block.
+  // A operand V^T: lane (c16, g) holds dim dt*16 + c16 at keys ks*32 + 4g + 0..3
+  // and ks*32 + 16 + 4g + 0..3, the key order of P^T.
+  bf16x8 va[kKs][4];
+#pragma unroll
+  for (int ks = 0; ks < kKs; ++ks)
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+      const char* lo_rows = lp.v[dt] + (kb + ks * 32) * kRowBytes;
+      va[ks][dt] = __builtin_shufflevector(v_column4(lo_rows), v_column4(lo_rows + 16 * kRowBytes), 0, 1, 2, 3, 4, 5,
+                                           6, 7);
+    }
+  __builtin_amdgcn_sched_barrier(0);
   // The lane's maximum over its 16 (8) scores (raw units; the scale is positive).
   float lm[2];
 #pragma unroll
@@ -556,14 +585,10 @@ __device__ __forceinline__ void softmax_pv_block(const LanePtrs& lp, int kb, int
     const bool init = FIRST && ks == 0;
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) {
-      // A operand V^T: lane (c16, g) holds dim dt*16 + c16 at keys ks*32 + 4g + 0..3
-      // and ks*32 + 16 + 4g + 0..3, the key order of P^T.
-      const char* lo_rows = lp.v[dt] + (kb + ks * 32) * kRowBytes;
-      const bf16x8 a = __builtin_shufflevector(v_column4(lo_rows), v_column4(lo_rows + 16 * kRowBytes),
-                                               0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
       for (int j = 0; j < kTiles; ++j)
-        st.o[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[j][ks], init ? zero : st.o[j][dt], 0, 0, 0);
+        st.o[j][dt] =
+            __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[ks][dt], pb[j][ks], init ? zero : st.o[j][dt], 0, 0, 0);
     }
   }
   if (kvalid < kKs * 32) {
@@ -621,7 +646,10 @@ __device__ __forceinline__ void attend_stage(const LanePtrs& lp, int nk, bool fi
     if (first) softmax_pv_block<ACT1, true, false>(lp, 0, nm, scale_log2, ones, sa, sm);
     else softmax_pv_block<ACT1, false, false>(lp, 0, nm, scale_log2, ones, sa, sm);
     prio_after_block(0);
-    for (int kb = 64; kb < nm; kb += 128) {
+    // Unrolled over the stage (nm <= kKRes), so every block's LDS offsets are immediates.
+#pragma unroll
+    for (int kb = 64; kb < kKRes; kb += 128) {
+      if (kb >= nm) break;
       if (kb + 64 < nm) qk_block<ACT1, false>(lp, kb + 64, qf, sa);
       softmax_pv_block<ACT1, false, false>(lp, kb, nm - kb, scale_log2, ones, sbk, sm);
       prio_after_block(kb >> 6);
