@@ -353,10 +353,24 @@ def summarize_pmc(d: str, workload: str) -> int:
     return 0
 
 
+def copy_fracs(achieved_gbs: float, peaks: dict) -> dict:
+    """An HBM-bound kernel's rate as fractions of the measured copies:
+    the runtime's copy (`frac_of_measured_copy`), the streaming kernel with
+    plain stores and with write-through stores."""
+    out = {}
+    for key, name in (("copy_GBs", "frac_of_measured_copy"), ("copy_kernel_GBs", "frac_of_copy_kernel"),
+                      ("copy_kernel_through_GBs", "frac_of_copy_kernel_through")):
+        if key in peaks:
+            out[name] = achieved_gbs / peaks[key]
+    return out
+
+
 def measure_peaks(torch, stream) -> dict:
-    """What this device sustains: a plain 256 MiB device-to-device copy
-    (read + write bytes over time) and a loop of independent bf16 MFMAs on
-    every SIMD (paper_2609_34325_amd/csrc/calibrate.hip)."""
+    """What this device sustains: a 256 MiB device-to-device copy by the
+    runtime (read + write bytes over time), the same copy by a streaming
+    kernel with plain stores and with the library's write-through stores,
+    and a loop of independent bf16 MFMAs on every SIMD
+    (paper_2609_34325_amd/csrc/calibrate.hip)."""
     import ctypes
     peaks = {}
     nbytes = 256 * 2 ** 20
@@ -390,6 +404,23 @@ def measure_peaks(torch, stream) -> dict:
         torch.cuda.synchronize()
         flops = 5 * lib.dora_calibrate_mfma_bf16_flops(blocks, iters)
         peaks["mfma_bf16_TFLOPs"] = flops / (e0.elapsed_time(e1) * 1e-3) / 1e12
+        del out
+        lib.dora_calibrate_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_int,
+                                            ctypes.c_void_p]
+        src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        cblocks = 4 * torch.cuda.get_device_properties(0).multi_processor_count
+        for through, key in ((0, "copy_kernel_GBs"), (1, "copy_kernel_through_GBs")):
+            for _ in range(3):
+                assert lib.dora_calibrate_copy(src.data_ptr(), dst.data_ptr(), nbytes, cblocks, through,
+                                               stream.cuda_stream) == 0
+            e0.record(stream)
+            for _ in range(10):
+                lib.dora_calibrate_copy(src.data_ptr(), dst.data_ptr(), nbytes, cblocks, through, stream.cuda_stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            peaks[key] = 2 * nbytes * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+        del src, dst
     return peaks
 
 
@@ -864,8 +895,7 @@ def main() -> int:
                 "resident": {"regime": "attention alone, back to back on one Q/K/V/O set resident in the MALL",
                              "us": at0["us_alone"], "tflops": at0["tflops_alone"], "mfma_frac": at0["mfma_frac_alone"],
                              "GBs": at0["GBs_alone"]}}
-    if "copy_GBs" in peaks:
-        roofline["hbm_view"]["frac_of_measured_copy"] = roofline["hbm_view"]["achieved"] / peaks["copy_GBs"]
+    roofline["hbm_view"].update(copy_fracs(roofline["hbm_view"]["achieved"], peaks))
     if "mfma_bf16_TFLOPs" in peaks and w.dtype == "bf16":
         roofline["frac_of_measured_mfma"] = roofline["achieved"] / peaks["mfma_bf16_TFLOPs"]
     sp_b, sp_al = sp0["algorithmic_bytes"], sp0["us_alone"] * 1e-6
@@ -875,8 +905,7 @@ def main() -> int:
                    "duration_source": "dora_select_pack_plan alone, back to back on the same buffers",
                    "in_step_events": {"us": sp0["us_in_step_events"], "GBs": sp0["GBs_in_step"],
                                       "frac": sp0["GBs_in_step"] / HBM_PEAK_GBS}}
-    if "copy_GBs" in peaks:
-        roofline_sp["frac_of_measured_copy"] = roofline_sp["achieved"] / peaks["copy_GBs"]
+    roofline_sp.update(copy_fracs(roofline_sp["achieved"], peaks))
 
     result = {
         "metric": METRIC,
@@ -917,8 +946,7 @@ def main() -> int:
     for k in ("residual_select_pack", "lc1_readout"):
         if k in result:
             result[k]["traffic"] = traffic.get("residual" if k.startswith("residual") else "lc1")
-            if "copy_GBs" in peaks:
-                result[k]["frac_of_measured_copy"] = result[k]["achieved"] / peaks["copy_GBs"]
+            result[k].update(copy_fracs(result[k]["achieved"], peaks))
 
     if not args.no_cpu_baseline:
         threads = len(os.sched_getaffinity(0))
