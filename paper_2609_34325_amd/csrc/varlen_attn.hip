@@ -359,13 +359,9 @@ __device__ __forceinline__ LdsOffsets lds_offsets() {
   return o;
 }
 
-// Per-lane read pointers into one staged K/V buffer.  They are formed once
-// per stage, outside the key-block loop, so the buffer's base (which lies past
-// the 16-bit offset range of LDS instructions for the second buffer) sits in
-// the lane's address register and each read inside the loop carries only the
-// block and step offsets.
-
-
+// Per-lane read pointers into one staged K/V buffer, formed once per stage
+// outside the key-block loop, so each read inside it carries only the block
+// and step offsets as its immediate.
 struct LanePtrs {
   lds_cchar* k0;
   lds_cchar* k1;
