@@ -87,6 +87,92 @@ __device__ __forceinline__ long long block_sum_ll(long long v, long long* s_red)
   return t;
 }
 
+// Larger and smaller of a lane's 64-bit word and the word of lane ^ STRIDE
+// (STRIDE < 64, all lanes active), without a trip through the LDS crossbar
+// where the hardware offers a register path: DPP quad permutations (1, 2),
+// a DPP row rotation by 8 (XOR 8 within a row of 16 lanes), the swizzle's
+// XOR mode (4), and the row swaps of v_permlane16/32_swap (16, 32), which
+// hand each lane both words of its pair in some order -- all a min/max
+// needs.
+template <int STRIDE>
+__device__ __forceinline__ void xor_minmax(unsigned long long x, unsigned long long& mx, unsigned long long& mn) {
+  const uint32_t lo = static_cast<uint32_t>(x), hi = static_cast<uint32_t>(x >> 32);
+  unsigned long long a = x, b;
+  if constexpr (STRIDE == 16 || STRIDE == 32) {
+    const auto l2 = STRIDE == 16 ? __builtin_amdgcn_permlane16_swap(lo, lo, false, false)
+                                 : __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
+    const auto h2 = STRIDE == 16 ? __builtin_amdgcn_permlane16_swap(hi, hi, false, false)
+                                 : __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
+    a = (static_cast<unsigned long long>(h2[0]) << 32) | l2[0];
+    b = (static_cast<unsigned long long>(h2[1]) << 32) | l2[1];
+  } else {
+    uint32_t pl, ph;
+    if constexpr (STRIDE == 1) {  // quad_perm [1, 0, 3, 2]
+      pl = __builtin_amdgcn_update_dpp(0u, lo, 0xB1, 0xF, 0xF, false);
+      ph = __builtin_amdgcn_update_dpp(0u, hi, 0xB1, 0xF, 0xF, false);
+    } else if constexpr (STRIDE == 2) {  // quad_perm [2, 3, 0, 1]
+      pl = __builtin_amdgcn_update_dpp(0u, lo, 0x4E, 0xF, 0xF, false);
+      ph = __builtin_amdgcn_update_dpp(0u, hi, 0x4E, 0xF, 0xF, false);
+    } else if constexpr (STRIDE == 8) {  // row_ror:8
+      pl = __builtin_amdgcn_update_dpp(0u, lo, 0x128, 0xF, 0xF, false);
+      ph = __builtin_amdgcn_update_dpp(0u, hi, 0x128, 0xF, 0xF, false);
+    } else {  // STRIDE == 4: swizzle, bitmask mode, xor_mask 4, and_mask 0x1F
+      static_assert(STRIDE == 4, "stride");
+      pl = static_cast<uint32_t>(__builtin_amdgcn_ds_swizzle(static_cast<int>(lo), 0x101F));
+      ph = static_cast<uint32_t>(__builtin_amdgcn_ds_swizzle(static_cast<int>(hi), 0x101F));
+    }
+    b = (static_cast<unsigned long long>(ph) << 32) | pl;
+  }
+  mx = a > b ? a : b;
+  mn = a < b ? a : b;
+}
+
+// Descending bitonic sort of the kPLThreads sort words in LDS, one word per
+// thread (element e = thread id, kept in a register).  The same network as
+// the LDS sort (pairs (lo, lo + stride), descending where lo & size == 0):
+// a step with stride < 64 pairs lanes of one wave (xor_minmax, no barrier);
+// the three steps with stride 64 or 128 pair waves through LDS between two
+// barriers.  Called by every thread of the workgroup (uniformly), after the
+// words are in LDS and a barrier; the sorted words are back in LDS after a
+// final barrier.
+__device__ __forceinline__ void cross_lane(unsigned long long& x, int lane, int stride, bool take_max) {
+  unsigned long long mx, mn;
+  switch (stride) {
+    case 1: xor_minmax<1>(x, mx, mn); break;
+    case 2: xor_minmax<2>(x, mx, mn); break;
+    case 4: xor_minmax<4>(x, mx, mn); break;
+    case 8: xor_minmax<8>(x, mx, mn); break;
+    case 16: xor_minmax<16>(x, mx, mn); break;
+    default: xor_minmax<32>(x, mx, mn); break;
+  }
+  x = take_max ? mx : mn;
+}
+
+__device__ void block_sort_256(unsigned long long* words) {
+  static_assert(kPLThreads == 256, "one word per thread");
+  const int e = threadIdx.x, lane = e & 63;
+  unsigned long long x = words[e];
+#pragma unroll
+  for (int size = 2; size <= kPLThreads; size <<= 1) {
+#pragma unroll
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      const bool take_max = ((e & stride) == 0) == ((e & size) == 0);  // lo of a descending pair, or hi of an ascending one
+      if (stride >= 64) {
+        __syncthreads();  // every read of the previous exchange is done
+        words[e] = x;
+        __syncthreads();
+        const unsigned long long y = words[e ^ stride];
+        x = take_max ? (x > y ? x : y) : (x < y ? x : y);
+      } else {
+        cross_lane(x, lane, stride, take_max);
+      }
+    }
+  }
+  __syncthreads();
+  words[e] = x;
+  __syncthreads();
+}
+
 // In place: A[u] <- sum_{v >= u} A[v] over [0, P), P a multiple of kPLThreads.
 // Thread t owns the consecutive slots [t c, (t + 1) c), c = P / kPLThreads.
 __device__ void reverse_inclusive_scan(float* A, int P, float* s_red) {
@@ -182,19 +268,25 @@ __global__ __launch_bounds__(kPLThreads) void pl_kernel(PLParams p) {
 
   if constexpr (SAMPLE) {
     if (ok) {
-      // Bitonic sort, descending (earliest draw first).
-      for (int size = 2; size <= P; size <<= 1) {
-        for (int stride = size >> 1; stride > 0; stride >>= 1) {
-          for (int i = tid; i < P / 2; i += kPLThreads) {
-            const int lo = 2 * i - (i & (stride - 1)), hi = lo + stride;
-            const bool desc = (lo & size) == 0;
-            const unsigned long long x = s_word[lo], y = s_word[hi];
-            if ((x < y) == desc) {
-              s_word[lo] = y;
-              s_word[hi] = x;
+      // Bitonic sort, descending (earliest draw first): in registers, one
+      // word per thread, when the words fit one workgroup width (up to 256
+      // visual tokens); else in LDS, a barrier per step.
+      if (P == kPLThreads) {
+        block_sort_256(s_word);
+      } else {
+        for (int size = 2; size <= P; size <<= 1) {
+          for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            for (int i = tid; i < P / 2; i += kPLThreads) {
+              const int lo = 2 * i - (i & (stride - 1)), hi = lo + stride;
+              const bool desc = (lo & size) == 0;
+              const unsigned long long x = s_word[lo], y = s_word[hi];
+              if ((x < y) == desc) {
+                s_word[lo] = y;
+                s_word[hi] = x;
+              }
             }
+            __syncthreads();
           }
-          __syncthreads();
         }
       }
       for (int u = tid; u < P; u += kPLThreads) {
