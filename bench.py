@@ -1107,7 +1107,7 @@ def adjacent_legs(head: ConfigRun, cold_sets, args, torch, dora, stream, phases)
     assert int(st_p.item()) == 0, f"device status {int(st_p.item())}"
     out["pl_sample"] = {"entry": "dora_pl_sample", "kernel": "pl_kernel", "bound": "latency", "us": ms_pl * 1e3,
                         "draws": int(k_h.sum()), "images": w.B,
-                        "note": "one workgroup per image: bitonic sort of the visual keys (in registers up to 256 tokens) and a block scan"}
+                        "note": "one workgroup per image: bitonic sort of the visual keys (in registers up to 1024 words) and a block scan"}
     print(f"[bench] trajectory flops {ms_fl * 1e3:.1f} us, pl sample {ms_pl * 1e3:.1f} us",
           file=sys.stderr, flush=True)
     del s_d, g_d

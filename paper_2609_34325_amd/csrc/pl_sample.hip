@@ -127,15 +127,16 @@ __device__ __forceinline__ void xor_minmax(unsigned long long x, unsigned long l
   mn = a < b ? a : b;
 }
 
-// Descending bitonic sort of the kPLThreads sort words in LDS, one word per
-// thread (element e = thread id, kept in a register).  The same network as
-// the LDS sort (pairs (lo, lo + stride), descending where lo & size == 0):
-// a step with stride < 64 pairs lanes of one wave (xor_minmax, no barrier);
-// the three steps with stride 64 or 128 pair waves through LDS between two
-// barriers.  Called by every thread of the workgroup (uniformly), after the
+// Descending bitonic sort of the P = E * kPLThreads sort words in LDS, E
+// words per thread in registers (element e = i * kPLThreads + thread id in
+// x[i]).  The same network as the LDS sort (pairs (lo, lo + stride),
+// descending where lo & size == 0): a step with stride < 64 pairs lanes of
+// one wave (xor_minmax, no barrier); stride 64 or 128 pairs waves through
+// LDS between two barriers; stride >= kPLThreads pairs two registers of a
+// thread.  Called by every thread of the workgroup (uniformly), after the
 // words are in LDS and a barrier; the sorted words are back in LDS after a
 // final barrier.
-__device__ __forceinline__ void cross_lane(unsigned long long& x, int lane, int stride, bool take_max) {
+__device__ __forceinline__ void cross_lane(unsigned long long& x, int stride, bool take_max) {
   unsigned long long mx, mn;
   switch (stride) {
     case 1: xor_minmax<1>(x, mx, mn); break;
@@ -148,28 +149,52 @@ __device__ __forceinline__ void cross_lane(unsigned long long& x, int lane, int 
   x = take_max ? mx : mn;
 }
 
-__device__ void block_sort_256(unsigned long long* words) {
-  static_assert(kPLThreads == 256, "one word per thread");
-  const int e = threadIdx.x, lane = e & 63;
-  unsigned long long x = words[e];
+template <int E>
+__device__ void block_sort(unsigned long long* words) {
+  static_assert(kPLThreads == 256, "waves of 64 lanes, four per workgroup");
+  const int t = threadIdx.x;
+  unsigned long long x[E];
 #pragma unroll
-  for (int size = 2; size <= kPLThreads; size <<= 1) {
+  for (int i = 0; i < E; ++i) x[i] = words[i * kPLThreads + t];
+#pragma unroll
+  for (int size = 2; size <= E * kPLThreads; size <<= 1) {
 #pragma unroll
     for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      const bool take_max = ((e & stride) == 0) == ((e & size) == 0);  // lo of a descending pair, or hi of an ascending one
-      if (stride >= 64) {
+      if (stride >= kPLThreads) {
+        const int rs = stride / kPLThreads;
+#pragma unroll
+        for (int i = 0; i < E; ++i) {
+          if (i & rs) continue;
+          const bool desc = ((i * kPLThreads + t) & size) == 0;
+          const unsigned long long a = x[i], b = x[i | rs];
+          const unsigned long long mx = a > b ? a : b, mn = a < b ? a : b;
+          x[i] = desc ? mx : mn;
+          x[i | rs] = desc ? mn : mx;
+        }
+      } else if (stride >= 64) {
         __syncthreads();  // every read of the previous exchange is done
-        words[e] = x;
+#pragma unroll
+        for (int i = 0; i < E; ++i) words[i * kPLThreads + t] = x[i];
         __syncthreads();
-        const unsigned long long y = words[e ^ stride];
-        x = take_max ? (x > y ? x : y) : (x < y ? x : y);
+#pragma unroll
+        for (int i = 0; i < E; ++i) {
+          const int e = i * kPLThreads + t;
+          const unsigned long long y = words[e ^ stride];
+          const bool take_max = ((e & stride) == 0) == ((e & size) == 0);  // lo of a descending pair, or hi of an ascending one
+          x[i] = take_max ? (x[i] > y ? x[i] : y) : (x[i] < y ? x[i] : y);
+        }
       } else {
-        cross_lane(x, lane, stride, take_max);
+#pragma unroll
+        for (int i = 0; i < E; ++i) {
+          const int e = i * kPLThreads + t;
+          cross_lane(x[i], stride, ((e & stride) == 0) == ((e & size) == 0));
+        }
       }
     }
   }
   __syncthreads();
-  words[e] = x;
+#pragma unroll
+  for (int i = 0; i < E; ++i) words[i * kPLThreads + t] = x[i];
   __syncthreads();
 }
 
@@ -268,11 +293,15 @@ __global__ __launch_bounds__(kPLThreads) void pl_kernel(PLParams p) {
 
   if constexpr (SAMPLE) {
     if (ok) {
-      // Bitonic sort, descending (earliest draw first): in registers, one
-      // word per thread, when the words fit one workgroup width (up to 256
-      // visual tokens); else in LDS, a barrier per step.
+      // Bitonic sort, descending (earliest draw first): in registers, P / 256
+      // words per thread, up to 1024 words; wider rows in LDS, a barrier
+      // per step.
       if (P == kPLThreads) {
-        block_sort_256(s_word);
+        block_sort<1>(s_word);
+      } else if (P == 2 * kPLThreads) {
+        block_sort<2>(s_word);
+      } else if (P == 4 * kPLThreads) {
+        block_sort<4>(s_word);
       } else {
         for (int size = 2; size <= P; size <<= 1) {
           for (int stride = size >> 1; stride > 0; stride >>= 1) {
