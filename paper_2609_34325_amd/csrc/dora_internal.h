@@ -79,8 +79,7 @@ struct AttnQueueLine {
 };
 
 struct AttnPlanHeader {
-  int32_t unused;
-  int32_t exit_count;  // workgroups that have left the current execute
+  int32_t unused[2];
   int32_t n_items;     // items in this plan
   int32_t magic;       // kPlanMagic once planned
   int32_t B, H, max_seqlen, q_tile;
@@ -88,9 +87,14 @@ struct AttnPlanHeader {
   int32_t reserved[22];
   uint32_t zero_row[32];  // one 128-byte row of zeros (bf16 V rows past a sequence's end)
   AttnQueueLine queue[kSubQueues];
-  int32_t reserved2[192];
+  // Workgroups that have left the current execute.  On a line of its own:
+  // every workgroup's exit atomic would otherwise queue behind, or hold up,
+  // the loads of the plan fields that other workgroups make at their start.
+  int32_t exit_count;
+  int32_t reserved2[191];
 };
 static_assert(sizeof(AttnPlanHeader) == 2048, "header must fill its slot");
+static_assert(__builtin_offsetof(AttnPlanHeader, exit_count) == 256 + kSubQueues * 128, "exit counter on its own line");
 static_assert(__builtin_offsetof(AttnPlanHeader, zero_row) == 128, "zero row is the header's second line");
 static_assert(__builtin_offsetof(AttnPlanHeader, queue) == 256, "queue counters start on a line of their own");
 

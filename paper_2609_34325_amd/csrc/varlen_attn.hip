@@ -1215,6 +1215,10 @@ extern "C" int dora_varlen_attn_execute(const void* q, const void* k, const void
   const int rc = dtype == DORA_BF16 ? persistent_grid(attn_fwd_bf16_kernel, kThreads, 0, &grid)
                                     : persistent_grid(attn_fwd_f32_kernel, kF32Threads, 1, &grid);
   if (rc != DORA_OK) return rc;
+  // No more workgroups than the plan can hold tickets: a small batch then
+  // launches (and retires, each with its exit atomic) only what it can use.
+  const int64_t max_tickets = L.max_items * (dtype == DORA_BF16 ? 1 : kF32Parts);
+  if (max_tickets < grid) grid = static_cast<int>(max_tickets < 1 ? 1 : max_tickets);
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (dtype == DORA_BF16)
     hipLaunchKernelGGL(attn_fwd_bf16_kernel, dim3(grid), dim3(kThreads), 0, st, p);

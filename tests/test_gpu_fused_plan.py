@@ -24,6 +24,7 @@ Q_TILE = 192       # queries per item, as the library's workspace layout defines
 HDR_BYTES = 2048   # plan header: sizes, a row of zeros, eight queue counters
 ITEMS_OFF = HDR_BYTES
 QUEUE_INTS = [64 + 32 * q for q in range(8)]   # one counter per 128-byte line
+EXIT_INT = 64 + 32 * 8                          # the exit counter, on the line after them
 
 
 SUB_QUEUES = 8      # item i is served by sub-queue i % 8
@@ -176,7 +177,7 @@ def test_fused_plan_replaces_a_stale_plan(gpu):
         hdr, n, items = read_plan(ws)
         assert n == len(expected_items(r.keep, w.H, w.N))
         assert np.array_equal(items, expected_items(r.keep, w.H, w.N))
-        assert int(hdr[1]) == 0 and all(int(hdr[i]) == 0 for i in QUEUE_INTS)   # counters reset
+        assert int(hdr[EXIT_INT]) == 0 and all(int(hdr[i]) == 0 for i in QUEUE_INTS)   # counters reset
         assert np.all(hdr[32:64] == 0)                         # the row of zeros
 
 
