@@ -221,6 +221,20 @@ def test_maximum_sequence_length(gpu):
     print(f"[attn] len {n} max err {mx:.2e} mean {mean:.2e}", flush=True)
 
 
+def test_maximum_sequence_length_f32(gpu):
+    """The fp32 kernel on one sequence of DORA_MAX_SEQLEN tokens (256 key
+    blocks per 64-query part), every output row against the oracle at 1e-5."""
+    n = gpu.DORA_MAX_SEQLEN
+    rng = np.random.default_rng(44)
+    q, k, v = qkv(rng, [n], 1, "f32")
+    cu = cu_of([n])
+    out, st = gpu_attn(gpu, q, k, v, cu)
+    assert st == 0
+    want = oracle.varlen_attn_rows(q, k, v, cu, np.arange(n), "f32")
+    mx, mean = assert_attn_close(widen(out), want, "f32", "len 16384 f32")
+    print(f"[attn] f32 len {n} max err {mx:.2e} mean {mean:.2e}", flush=True)
+
+
 def test_maximum_sequence_count(gpu):
     """8192 short sequences (the most one plan orders), lengths 1..4, H = 2."""
     rng = np.random.default_rng(43)
